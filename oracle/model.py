@@ -1,0 +1,267 @@
+"""Plain CPU definition of the verification step (test infrastructure only).
+
+Each function states the passage of the paper it follows.  The paper fixes the
+verification interface and acceptance rule but not the target architecture; the
+architecture below is the Llama-style decoder the workloads use, written as its
+textbook definition.  Readings of points the paper leaves open:
+
+* the committed block is always the accepted tokens plus one target token
+  (also on full acceptance, where that token is the bonus), which the
+  cycles-per-1K identity of App. C / Table 4 pins;
+* the forward covers k + 1 rows: the pending (last committed, not yet cached)
+  token followed by the k draft tokens; k = 0 is one greedy step;
+* argmax ties go to the lowest token id;
+* RMSNorm eps and the rotary base come from the model config; rotary uses the
+  rotate-half pairing (j, j + dh/2) with angle p * theta^(-2j/dh) at 0-based
+  absolute position p; no biases, no QK-norm, untied LM head; q-head h reads
+  kv-head floor(h / (Hq / Hkv)).
+
+Nothing here is blocked, fused or reordered beyond processing query rows in
+groups during prefill, which leaves every row's arithmetic unchanged.
+"""
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+
+def bf16_bits_to_float(u16, dtype=np.float64) -> np.ndarray:
+    """bf16 bit pattern -> float (exact widening)."""
+    u = np.asarray(u16, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(dtype)
+
+
+class OracleModel:
+    """Target model M: config plus a mapping from canonical tensor names to
+    bf16 bit arrays ([out, in] row-major for matrices)."""
+
+    def __init__(self, cfg, weights, dtype=np.float64, cache: bool = True):
+        self.cfg = cfg
+        self.weights = weights
+        self.dtype = np.dtype(dtype)
+        self.cache = cache
+        self._conv = {}
+
+    def w(self, name: str) -> np.ndarray:
+        if name in self._conv:
+            return self._conv[name]
+        arr = bf16_bits_to_float(self.weights[name], self.dtype)
+        if self.cache:
+            self._conv[name] = arr
+        return arr
+
+
+# ------------------------------------------------------------------ layers
+
+def rms_norm(x, g, eps):
+    """x / sqrt(mean(x^2) + eps) * g over the last axis."""
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * g
+
+
+def rotary(x, pos, theta):
+    """Rotate-half rotary embedding of x [n, H, dh] at positions pos [n]."""
+    dh = x.shape[-1]
+    half = dh // 2
+    inv_freq = float(theta) ** (-(2.0 * np.arange(half, dtype=np.float64)) / dh)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+    cos = np.cos(ang).astype(x.dtype)[:, None, :]
+    sin = np.sin(ang).astype(x.dtype)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def softmax_rows(s):
+    m = np.max(s, axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def attend(q, K, V, q_pos):
+    """Causal grouped-query attention.  q [n, Hq, dh]; K, V [T, Hkv, dh] hold
+    positions 0..T-1; row i attends to key positions j <= q_pos[i]."""
+    n, Hq, dh = q.shape
+    T, Hkv, _ = K.shape
+    group = Hq // Hkv
+    j = np.arange(T)
+    allowed = j[None, :] <= np.asarray(q_pos)[:, None]
+    out = np.empty_like(q)
+    scale = 1.0 / np.sqrt(dh)
+    for h in range(Hq):
+        g = h // group
+        s = (q[:, h, :] @ K[:, g, :].T) * scale
+        s = np.where(allowed, s, -np.inf)
+        out[:, h, :] = softmax_rows(s) @ V[:, g, :]
+    return out
+
+
+def silu(z):
+    with np.errstate(over="ignore"):
+        return z / (1.0 + np.exp(-z))
+
+
+def forward(model: OracleModel, K_cache, V_cache, tokens, positions, want_logits=True):
+    """Decoder forward of rows ``tokens`` at ``positions`` over cached K/V.
+
+    K_cache[l], V_cache[l]: [ctx, Hkv, dh] for positions 0..ctx-1 (None = empty);
+    positions must be ctx, ctx+1, ....  Returns (logits [n, V] or None,
+    new K rows per layer, new V rows per layer).
+    """
+    c = model.cfg
+    dt = model.dtype
+    tokens = np.asarray(tokens, dtype=np.int64)
+    positions = np.asarray(positions, dtype=np.int64)
+    n = tokens.shape[0]
+    x = model.w("embed")[tokens] if model.cache else bf16_bits_to_float(
+        np.asarray(model.weights["embed"])[tokens], dt)
+    new_k, new_v = [], []
+    for l in range(c.n_layers):
+        p = f"layers.{l}."
+        h = rms_norm(x, model.w(p + "attn_norm"), c.rms_eps)
+        q = (h @ model.w(p + "wq").T).reshape(n, c.n_q_heads, c.head_dim)
+        k = (h @ model.w(p + "wk").T).reshape(n, c.n_kv_heads, c.head_dim)
+        v = (h @ model.w(p + "wv").T).reshape(n, c.n_kv_heads, c.head_dim)
+        q = rotary(q, positions, c.rope_theta)
+        k = rotary(k, positions, c.rope_theta)
+        Kc = k if K_cache is None or K_cache[l] is None else np.concatenate([K_cache[l], k], axis=0)
+        Vc = v if V_cache is None or V_cache[l] is None else np.concatenate([V_cache[l], v], axis=0)
+        o = attend(q, Kc, Vc, positions).reshape(n, c.q_dim)
+        x = x + o @ model.w(p + "wo").T
+        h2 = rms_norm(x, model.w(p + "mlp_norm"), c.rms_eps)
+        a = silu(h2 @ model.w(p + "wg").T) * (h2 @ model.w(p + "wu").T)
+        x = x + a @ model.w(p + "wd").T
+        new_k.append(k)
+        new_v.append(v)
+    logits = None
+    if want_logits:
+        logits = rms_norm(x, model.w("final_norm"), c.rms_eps) @ model.w("lm_head").T
+    return logits, new_k, new_v
+
+
+# ------------------------------------------------------- verification rule
+
+def argmax_lowest(logits) -> np.ndarray:
+    """Row-wise argmax; np.argmax returns the first (lowest-index) maximum."""
+    return np.argmax(np.asarray(logits), axis=-1).astype(np.int64)
+
+
+def accept_length(g, d) -> int:
+    """Accepted length (label equation of §3.3 / App. B): the largest l in
+    {0..k} such that the draft prefix d[0:l] equals the target continuation.
+    Row i of the verify forward predicts the token after draft prefix d[0:i],
+    so the target continuation token compared with d[i] is g[i]."""
+    k = len(d)
+    best = 0
+    for l in range(k + 1):
+        if all(int(d[j]) == int(g[j]) for j in range(l)):
+            best = l
+    return best
+
+
+@dataclass
+class SeqState:
+    """Committed prefix x_{1:t} of one sequence (§3.1).  tokens includes the
+    pending token tokens[-1], whose K/V is not cached yet; ctx = len - 1."""
+    tokens: List[int]
+    K: list = field(default_factory=list)
+    V: list = field(default_factory=list)
+
+    @property
+    def ctx(self) -> int:
+        return len(self.tokens) - 1
+
+    @property
+    def pending(self) -> int:
+        return self.tokens[-1]
+
+
+@dataclass
+class VerifyResult:
+    """(a_t, z_t) = Verify(x_{1:t}, d_t; M) of §3.1, plus the per-row argmax,
+    the logits and the tentative K/V rows needed by commit."""
+    accepted: int
+    next_token: int
+    draft: np.ndarray
+    argmax: np.ndarray
+    logits: Optional[np.ndarray]
+    new_k: list
+    new_v: list
+
+    @property
+    def committed(self) -> List[int]:
+        """z_t: the accepted draft prefix followed by one target token."""
+        return [int(t) for t in self.draft[:self.accepted]] + [int(self.next_token)]
+
+
+def prefill(model: OracleModel, prompt, row_block: int = 2048) -> SeqState:
+    """Cache K/V of prompt[0..n-2]; the last prompt token becomes pending."""
+    prompt = [int(t) for t in prompt]
+    assert len(prompt) >= 1
+    c = model.cfg
+    st = SeqState(tokens=list(prompt))
+    K = [None] * c.n_layers
+    V = [None] * c.n_layers
+    body = np.asarray(prompt[:-1], dtype=np.int64)
+    for s in range(0, body.shape[0], row_block):
+        rows = body[s:s + row_block]
+        _, nk, nv = forward(model, K, V, rows, np.arange(s, s + rows.shape[0]), want_logits=False)
+        K = [nk[l] if K[l] is None else np.concatenate([K[l], nk[l]]) for l in range(c.n_layers)]
+        V = [nv[l] if V[l] is None else np.concatenate([V[l], nv[l]]) for l in range(c.n_layers)]
+    st.K, st.V = K, V
+    return st
+
+
+def verify(model: OracleModel, st: SeqState, draft, want_logits: bool = True) -> VerifyResult:
+    """One verification step: forward the pending token and the draft at
+    positions ctx..ctx+k, take the argmax of every row, and apply the accept
+    rule (§3.1 Verify; §3.4; Alg. 1 Verify step)."""
+    d = np.asarray(draft, dtype=np.int64).reshape(-1)
+    rows = np.concatenate([[st.pending], d]).astype(np.int64)
+    pos = np.arange(st.ctx, st.ctx + rows.shape[0])
+    logits, nk, nv = forward(model, st.K if st.ctx else None, st.V if st.ctx else None, rows, pos)
+    g = argmax_lowest(logits)
+    a = accept_length(g, d)
+    return VerifyResult(a, int(g[a]), d, g, logits if want_logits else None, nk, nv)
+
+
+def commit(st: SeqState, res: VerifyResult, keep: Optional[int] = None) -> SeqState:
+    """Append the committed block (Alg. 1: append z to x).  keep <= a draft
+    tokens are kept (default a); the K/V of the pending row and the kept draft
+    rows enter the cache, the rest is discarded."""
+    keep = res.accepted if keep is None else int(keep)
+    assert 0 <= keep <= res.accepted
+    n_rows = keep + 1
+    K = [nk[:n_rows] if (st.K is None or not st.K or st.K[l] is None)
+         else np.concatenate([st.K[l], nk[:n_rows]]) for l, nk in enumerate(res.new_k)]
+    V = [nv[:n_rows] if (st.V is None or not st.V or st.V[l] is None)
+         else np.concatenate([st.V[l], nv[:n_rows]]) for l, nv in enumerate(res.new_v)]
+    toks = list(st.tokens) + [int(t) for t in res.draft[:keep]] + [int(res.argmax[keep])]
+    return SeqState(tokens=toks, K=K, V=V)
+
+
+def greedy_decode(model: OracleModel, st: SeqState, n: int):
+    """n plain greedy steps (verify with an empty draft, commit).  Returns the
+    generated tokens and the final state."""
+    out = []
+    for _ in range(n):
+        r = verify(model, st, [], want_logits=False)
+        st = commit(st, r)
+        out.append(r.next_token)
+    return out, st
+
+
+def brute_force_greedy(model: OracleModel, tokens, n: int):
+    """Greedy decoding without any cache: recompute the whole forward over the
+    full token list for every new token.  Returns (new tokens, last-row logits
+    of every step)."""
+    toks = [int(t) for t in tokens]
+    out, rows = [], []
+    for _ in range(n):
+        logits, _, _ = forward(model, None, None, toks, np.arange(len(toks)))
+        last = logits[-1]
+        nxt = int(argmax_lowest(last[None, :])[0])
+        out.append(nxt)
+        rows.append(last)
+        toks.append(nxt)
+    return out, np.stack(rows)

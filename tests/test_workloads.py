@@ -1,0 +1,79 @@
+"""The seeded input generators: deterministic, thread-count independent, and
+shaped as the workloads state."""
+
+import numpy as np
+
+from workloads import ModelConfig, TINY, make_tensor, make_weights, canonical_tensors, tokens as wt
+from workloads.weights import f32_to_bf16_bits
+
+
+def test_weights_deterministic_and_thread_independent():
+    from concurrent.futures import ThreadPoolExecutor
+    cfg = ModelConfig("w", 1, 2048, 4, 4, 512, 4096, 3000, 1e4)
+    a = make_tensor(cfg, "layers.0.wg", seed=42)
+    with ThreadPoolExecutor(4) as pool:
+        b = make_tensor(cfg, "layers.0.wg", seed=42, pool=pool)
+    np.testing.assert_array_equal(a, b)
+    c = make_tensor(cfg, "layers.0.wu", seed=42)
+    assert not np.array_equal(a, c)
+    x = (a.astype(np.uint32) << 16).view(np.float32)
+    assert abs(x.std() - 0.02) < 2e-4 and abs(x.mean()) < 2e-4
+
+
+def test_canonical_order_and_shapes():
+    names = [n for n, *_ in canonical_tensors(TINY)]
+    assert names[0] == "embed" and names[-2:] == ["final_norm", "lm_head"]
+    assert names[1:10] == [f"layers.0.{n}" for n in
+                           ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")]
+    w = make_weights(TINY, threads=2)
+    assert w["layers.1.wd"].shape == (TINY.d_model, TINY.ffn_dim)
+    assert w["layers.0.wk"].shape == (TINY.kv_dim, TINY.d_model)
+    assert np.all(w["final_norm"] == 0x3F80)
+
+
+def test_bf16_round_to_nearest_even():
+    import torch
+    x = np.random.default_rng(0).standard_normal(100000).astype(np.float32) * 7
+    x[:4] = [1.00390625, 1.01171875, -1.00390625, 65504.0]  # exact ties
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(f32_to_bf16_bits(x), ref)
+
+
+def test_zipf_context_rank_frequency():
+    rng = wt.rng_for("context", 0)
+    t = wt.zipf_context(rng, 200000, 128256, s=1.1)
+    assert t.min() >= 0 and t.max() < 128256
+    c = np.bincount(t, minlength=10)
+    # P(r=1)/P(r=2) = 2^1.1
+    assert abs(c[0] / c[1] - 2 ** 1.1) < 0.1
+
+
+def test_segment_context_repeats():
+    rng = wt.rng_for("context", 1)
+    t = wt.segment_context(rng, 16384, 128256)
+    assert t.shape == (16384,)
+    segs = t.reshape(256, 64)
+    # each segment agrees with some other segment on most positions (shared base)
+    agree = max(np.mean(segs[0] == segs[j]) for j in range(1, 256))
+    assert agree > 0.5
+
+
+def test_plant_chain():
+    rng = wt.rng_for("draft", 0)
+    g = np.arange(100, 120)
+    for a in range(0, 9):
+        d = wt.plant_chain(rng, g, a, 8, 50000)
+        assert len(d) == 8
+        assert list(d[:a]) == list(g[:a])
+        if a < 8:
+            assert d[a] != g[a]
+
+
+def test_acceptance_samplers():
+    rng = wt.rng_for("accept", 0)
+    geo = [wt.geometric_accept(rng, 0.3, 8) for _ in range(20000)]
+    # mean of min(G, 8), G geometric with P(G = n) = 0.3 * 0.7^n
+    exact = sum(min(n, 8) * 0.3 * 0.7 ** n for n in range(200))
+    assert abs(np.mean(geo) - exact) < 0.05
+    bi = [wt.bimodal_accept(rng, 64) for _ in range(4000)]
+    assert all(0 <= a <= 2 or 32 <= a <= 64 for a in bi)
