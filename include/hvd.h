@@ -1,0 +1,169 @@
+/*
+ * hvd.h -- C ABI of the target-model verification step of Hybrid Verified
+ * Decoding (arxiv 2606.01019) on one AMD Instinct MI355X (gfx950).
+ *
+ * The paper's interface (section 3.1, "Verified Drafting as a Common
+ * Interface"; section 3.4 and Alg. 1, Verify step) is
+ *     (a_t, z_t) = Verify(x_{1:t}, d_t; M)
+ * for a prefix x_{1:t}, a chain draft d_t of k tokens and the unchanged target
+ * model M: a_t in {0..k} is the number of accepted draft tokens and z_t, the
+ * committed block, is the accepted draft prefix followed by one target token
+ * (the correction token when the draft is rejected early, the bonus token when
+ * all k are accepted).  Alg. 1 then appends z_t to the prefix.
+ *
+ * Under greedy decoding (temperature 0, App. A generation table) the target
+ * token after the accepted prefix is the argmax of the model's logits, and the
+ * accepted length is the longest draft prefix that equals the target's own
+ * argmax continuation (the label equation of section 3.3 / App. B).
+ *
+ * Model: Llama-style decoder (RMSNorm, rotary embedding with rotate-half
+ * pairing, grouped-query attention, SwiGLU MLP, untied LM head), bf16 weights.
+ * The KV cache holds fp16 (the paper's data type, App. A) in 16-token pages.
+ *
+ * Conventions for every call:
+ *  - Host pointers (const T* / T*) are owned by the caller and read or written
+ *    only during the call.  "device" pointers point to GPU memory.
+ *  - A borrowed device buffer (dev_buf != NULL) stays owned by the caller; it
+ *    must outlive the handle and is never freed by the library.  With
+ *    dev_buf == NULL the library allocates (hipMalloc) and frees the memory.
+ *  - Work is queued on the HIP stream given at load/alloc time (the caller's
+ *    torch stream), and every call returns only after its results are in host
+ *    memory (synchronous).  A handle is not thread-safe.
+ *  - Every call returns an hvd_status.  On any error the library state is left
+ *    unchanged (no partial page allocation, no partial commit) and
+ *    hvd_last_error() describes the failure.
+ */
+#ifndef HVD_H
+#define HVD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HVD_OK = 0,
+  HVD_ERR_ARG = -1,    /* bad pointer/size, unknown or duplicate seq id, keep > accepted */
+  HVD_ERR_STATE = -2,  /* ctx_lens disagree with the library, verify pending, commit without verify */
+  HVD_ERR_OOM = -3,    /* page pool or row workspace cannot hold the request (checked before any work) */
+  HVD_ERR_RANGE = -4,  /* token outside [0, vocab), draft length outside [0, max_draft], position >= max_pos */
+  HVD_ERR_DEVICE = -5  /* a HIP runtime error; message in hvd_last_error() */
+} hvd_status;
+
+/* Model shape.  Requirements (HVD_ERR_ARG otherwise): d_model % 64 == 0,
+ * ffn_dim % 32 == 0, vocab % 32 == 0, head_dim in {64, 128},
+ * n_q_heads % n_kv_heads == 0, page_size == 16, 0 <= max_draft <= 64,
+ * max_pos >= 32. */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t ffn_dim;
+  int32_t vocab;
+  int32_t max_draft;   /* longest chain draft hvd_verify accepts */
+  int32_t page_size;   /* tokens per KV page (16) */
+  int32_t max_pos;     /* rotary table length: every position must be < max_pos */
+  float rope_theta;
+  float rms_eps;
+} hvd_config;
+
+typedef struct hvd_model_s* hvd_model;
+typedef struct hvd_kv_s* hvd_kv;
+
+/* Device bytes needed by hvd_model_load for this config (packed weights,
+ * gains, rotary table). */
+size_t hvd_model_bytes(const hvd_config* cfg);
+
+/* Upload and pack the weights.  tensors[i] are host bf16 bit patterns
+ * (uint16) in canonical order, each row-major with torch Linear layout
+ * [out_features, in_features]:
+ *   embed [V, D];
+ *   for each layer: attn_norm [D], wq [Hq*dh, D], wk [Hkv*dh, D],
+ *     wv [Hkv*dh, D], wo [D, Hq*dh], mlp_norm [D], wg [F, D], wu [F, D],
+ *     wd [D, F];
+ *   final_norm [D], lm_head [V, D].
+ * Count = 3 + 9 * n_layers.  dev_buf (nullable) must hold hvd_model_bytes.
+ * stream is a hipStream_t (NULL = default stream).  Temporary staging memory
+ * is allocated and freed inside the call. */
+hvd_status hvd_model_load(const hvd_config* cfg, const uint16_t* const* tensors, void* dev_buf,
+                          size_t dev_bytes, void* stream, hvd_model* out);
+void hvd_model_free(hvd_model m);
+
+/* Device bytes for a KV pool of n_pages pages plus the per-step workspace for
+ * up to max_seqs sequences verified together. */
+size_t hvd_kv_bytes(const hvd_config* cfg, int32_t max_seqs, int32_t n_pages);
+
+/* Create a KV cache bound to model m.  Sequence ids are 0..max_seqs-1.
+ * dev_buf (nullable) must hold hvd_kv_bytes.  Work of this handle runs on
+ * stream (hipStream_t, NULL = default stream). */
+hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_pages, void* dev_buf,
+                        size_t dev_bytes, void* stream, hvd_kv* out);
+void hvd_kv_free(hvd_kv kv);
+
+/* Start sequence seq_id from a prompt of n >= 1 tokens: caches K/V of
+ * tokens[0..n-2] (positions 0..n-2) and makes tokens[n-1] the pending token,
+ * so ctx_len = n - 1.  No logits are produced.  seq_id must be free. */
+hvd_status hvd_prefill(hvd_model m, hvd_kv kv, int32_t seq_id, const int32_t* tokens, int32_t n);
+
+/* One verification step for `batch` distinct sequences (section 3.1 Verify).
+ * Sequence b (id seq_ids[b], current length ctx_lens[b], which must equal the
+ * library's) contributes k_b = draft_lens[b] draft tokens, packed in
+ * draft_tokens in batch order (sum k_b entries).  One forward covers, for each
+ * b, the pending token and the draft at positions ctx_b..ctx_b+k_b.
+ * Outputs (host, [batch]): accepted_len[b] = a_b in [0, k_b]; next_token[b] =
+ * the target's argmax after the accepted prefix (lowest id on ties).  The
+ * committed block is draft[0:a_b] followed by next_token[b].
+ * logits (nullable, DEVICE pointer) receives fp32 logits [sum(k_b+1)][vocab],
+ * rows packed by sequence -- for parity checks only (extra HBM writes).
+ * K/V of all k_b + 1 rows is written tentatively; hvd_commit decides how many
+ * stay.  A second verify of a sequence before its commit is HVD_ERR_STATE. */
+hvd_status hvd_verify(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_ids,
+                      const int32_t* ctx_lens, const int32_t* draft_tokens, const int32_t* draft_lens,
+                      int32_t* accepted_len, int32_t* next_token, float* logits);
+
+/* Commit the last verify of each listed sequence (Alg. 1: append z_t).
+ * keep_lens (nullable = the accepted lengths) keeps 0 <= keep <= a_b draft
+ * tokens: ctx_len += keep + 1 and the new pending token is the target's argmax
+ * after draft[0:keep] (which equals draft[keep] when keep < a_b).  K/V rows of
+ * the rejected suffix are dropped by metadata only; pages wholly past the new
+ * end return to the pool. */
+hvd_status hvd_commit(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_ids,
+                      const int32_t* keep_lens);
+
+/* Roll sequence seq_id back to an earlier committed length: 0 <= new_ctx_len
+ * <= ctx_len, pending_token is the committed token at position new_ctx_len.
+ * Cancels an uncommitted verify. */
+hvd_status hvd_truncate(hvd_kv kv, int32_t seq_id, int32_t new_ctx_len, int32_t pending_token);
+
+/* Release a sequence and its pages. */
+hvd_status hvd_seq_free(hvd_kv kv, int32_t seq_id);
+
+/* Query a sequence: ctx_len, pending token, 1 if a verify awaits commit.
+ * Any output pointer may be NULL. */
+hvd_status hvd_seq_info(hvd_kv kv, int32_t seq_id, int32_t* ctx_len, int32_t* pending_token,
+                        int32_t* verify_pending);
+
+/* Number of free pages in the pool. */
+int32_t hvd_kv_free_pages(hvd_kv kv);
+
+/* Per-kernel timing: while enabled, every launch of a kernel family is
+ * bracketed by HIP events on the handle's stream and its algorithmic HBM bytes
+ * (weights streamed, KV read) are accumulated.  family: 0 = weight-streaming
+ * GEMMs, 1 = verify attention, 2 = everything else.  hvd_profile_read returns
+ * the summed event time (ms), launch count and algorithmic bytes since the
+ * last enable. */
+hvd_status hvd_profile_enable(hvd_kv kv, int32_t enable);
+hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* launches, double* bytes);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* hvd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HVD_H */

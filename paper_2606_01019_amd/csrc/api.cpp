@@ -1,0 +1,858 @@
+// C ABI of libhvd: model loading and packing, the KV cache handle, and the
+// verify / commit / prefill drivers that enqueue the gfx950 kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/hvd.h"
+#include "host_state.h"
+#include "kernels.h"
+
+using namespace hvd;
+
+namespace {
+
+thread_local std::string g_err;
+
+hvd_status set_err(hvd_status s, const std::string& m) {
+  g_err = m;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                          \
+  do {                                                                                         \
+    hipError_t e_ = (expr);                                                                    \
+    if (e_ != hipSuccess) return set_err(HVD_ERR_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr int kPrefillRows = 128;  // rows per prefill chunk
+constexpr int kMaxMTile = 8;       // 16-row tiles one GEMM workgroup covers
+constexpr int kAttnRows = 128;     // query rows per attention work item
+constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items)
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Bump allocator over one device buffer.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  template <class T>
+  T* take(size_t n) {
+    T* p = base ? (T*)(base + off) : nullptr;
+    off = align_up(off + n * sizeof(T));
+    return p;
+  }
+};
+
+hvd_status check_config(const hvd_config* c) {
+  if (!c) return set_err(HVD_ERR_ARG, "null config");
+  if (c->n_layers < 1 || c->d_model < 64 || c->d_model % 64) return set_err(HVD_ERR_ARG, "d_model must be a positive multiple of 64");
+  if (c->head_dim != 64 && c->head_dim != 128) return set_err(HVD_ERR_ARG, "head_dim must be 64 or 128");
+  if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads) return set_err(HVD_ERR_ARG, "n_q_heads must be a multiple of n_kv_heads");
+  if (c->ffn_dim < 32 || c->ffn_dim % 32) return set_err(HVD_ERR_ARG, "ffn_dim must be a positive multiple of 32");
+  if (c->vocab < 32 || c->vocab % 32) return set_err(HVD_ERR_ARG, "vocab must be a positive multiple of 32");
+  if (c->page_size != kPage) return set_err(HVD_ERR_ARG, "page_size must be 16");
+  if (c->max_draft < 0 || c->max_draft > 64) return set_err(HVD_ERR_ARG, "max_draft must be in [0, 64]");
+  if (c->max_pos < 32) return set_err(HVD_ERR_ARG, "max_pos must be >= 32");
+  if (!(c->rope_theta > 0.f) || !(c->rms_eps > 0.f)) return set_err(HVD_ERR_ARG, "rope_theta and rms_eps must be > 0");
+  return HVD_OK;
+}
+
+struct LayerW {
+  uint16_t *qkv, *o, *gu, *down;
+  float *g_attn, *g_mlp;
+};
+
+}  // namespace
+
+struct hvd_model_s {
+  hvd_config cfg;
+  void* base = nullptr;
+  bool owned = false;
+  size_t bytes = 0;
+  uint16_t* embed = nullptr;
+  std::vector<LayerW> layers;
+  float* g_final = nullptr;
+  uint16_t* lm = nullptr;
+  float2* rope = nullptr;
+  hipStream_t stream = nullptr;
+};
+
+namespace {
+
+// Lay out (or size, with base == null) the model buffer.
+size_t carve_model(hvd_model_s* m, void* base) {
+  const hvd_config& c = m->cfg;
+  Carver cv(base);
+  const size_t D = c.d_model, F = c.ffn_dim, V = c.vocab, qd = (size_t)c.n_q_heads * c.head_dim,
+               kd = (size_t)c.n_kv_heads * c.head_dim;
+  m->embed = cv.take<uint16_t>(V * D);
+  m->layers.resize(c.n_layers);
+  for (auto& L : m->layers) {
+    L.qkv = cv.take<uint16_t>((qd + 2 * kd) * D);
+    L.o = cv.take<uint16_t>(D * qd);
+    L.gu = cv.take<uint16_t>(2 * F * D);
+    L.down = cv.take<uint16_t>(D * F);
+    L.g_attn = cv.take<float>(D);
+    L.g_mlp = cv.take<float>(D);
+  }
+  m->g_final = cv.take<float>(D);
+  m->lm = cv.take<uint16_t>(V * D);
+  m->rope = cv.take<float2>((size_t)c.max_pos * (c.head_dim / 2));
+  return cv.off;
+}
+
+}  // namespace
+
+extern "C" size_t hvd_model_bytes(const hvd_config* cfg) {
+  if (check_config(cfg) != HVD_OK) return 0;
+  hvd_model_s tmp;
+  tmp.cfg = *cfg;
+  return carve_model(&tmp, nullptr);
+}
+
+namespace {
+
+float bf16_bits_to_float(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+hvd_status upload_gain(const uint16_t* src, float* dst, int n, hipStream_t s) {
+  std::vector<float> g(n);
+  for (int i = 0; i < n; ++i) g[i] = bf16_bits_to_float(src[i]);
+  HIP_TRY(hipMemcpyAsync(dst, g.data(), n * sizeof(float), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return HVD_OK;
+}
+
+// Copy rows of host tensors into the staging buffer back to back, then pack
+// them into fragment order through rowmap.
+hvd_status pack_group(const std::vector<std::pair<const uint16_t*, size_t>>& parts, const std::vector<int32_t>& rowmap,
+                      int K, uint16_t* staging, int32_t* dmap, uint16_t* dst, hipStream_t s) {
+  size_t off = 0;
+  for (auto& p : parts) {
+    HIP_TRY(hipMemcpyAsync(staging + off, p.first, p.second * sizeof(uint16_t), hipMemcpyHostToDevice, s));
+    off += p.second;
+  }
+  HIP_TRY(hipMemcpyAsync(dmap, rowmap.data(), rowmap.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_pack(staging, dmap, dst, (int)rowmap.size(), K, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return HVD_OK;
+}
+
+}  // namespace
+
+extern "C" hvd_status hvd_model_load(const hvd_config* cfg, const uint16_t* const* t, void* dev_buf, size_t dev_bytes,
+                                     void* stream, hvd_model* out) {
+  if (hvd_status st = check_config(cfg); st != HVD_OK) return st;
+  if (!t || !out) return set_err(HVD_ERR_ARG, "null tensors or out");
+  const hvd_config& c = *cfg;
+  const int n_t = 3 + 9 * c.n_layers;
+  for (int i = 0; i < n_t; ++i)
+    if (!t[i]) return set_err(HVD_ERR_ARG, "null tensor pointer");
+  auto* m = new hvd_model_s();
+  m->cfg = c;
+  m->stream = (hipStream_t)stream;
+  const size_t need = carve_model(m, nullptr);
+  if (dev_buf) {
+    if (dev_bytes < need) {
+      delete m;
+      return set_err(HVD_ERR_ARG, "dev_buf smaller than hvd_model_bytes");
+    }
+    m->base = dev_buf;
+  } else {
+    if (hipMalloc(&m->base, need) != hipSuccess) {
+      delete m;
+      return set_err(HVD_ERR_OOM, "hipMalloc of model weights failed");
+    }
+    m->owned = true;
+  }
+  m->bytes = need;
+  carve_model(m, m->base);
+  hipStream_t s = m->stream;
+
+  const size_t D = c.d_model, F = c.ffn_dim, V = c.vocab, dh = c.head_dim, qd = (size_t)c.n_q_heads * dh,
+               kd = (size_t)c.n_kv_heads * dh;
+  size_t stage_elems = std::max({(qd + 2 * kd) * D, 2 * F * D, D * F, V * D, D * qd});
+  size_t map_elems = std::max({qd + 2 * kd, 2 * F, V, D});
+  uint16_t* staging = nullptr;
+  int32_t* dmap = nullptr;
+  hvd_status st = HVD_OK;
+  auto fail = [&](hvd_status e) {
+    if (staging) (void)hipFree(staging);
+    if (dmap) (void)hipFree(dmap);
+    if (m->owned) (void)hipFree(m->base);
+    delete m;
+    return e;
+  };
+  if (hipMalloc(&staging, stage_elems * 2) != hipSuccess || hipMalloc(&dmap, map_elems * 4) != hipSuccess)
+    return fail(set_err(HVD_ERR_OOM, "hipMalloc of load staging failed"));
+
+  auto ident = [](size_t n) {
+    std::vector<int32_t> r(n);
+    for (size_t i = 0; i < n; ++i) r[i] = (int32_t)i;
+    return r;
+  };
+  // q and k output rows permuted inside each head so that the rotate-half
+  // pairs (j, j + dh/2) become adjacent columns (2j, 2j+1).
+  std::vector<int32_t> qkv_map(qd + 2 * kd);
+  for (size_t n = 0; n < qd + 2 * kd; ++n) {
+    if (n < qd + kd) {
+      size_t base = n < qd ? 0 : qd;
+      size_t head = (n - base) / dh, dp = (n - base) % dh;
+      size_t d = (dp % 2 == 0) ? dp / 2 : dh / 2 + dp / 2;
+      qkv_map[n] = (int32_t)(base + head * dh + d);
+    } else {
+      qkv_map[n] = (int32_t)n;
+    }
+  }
+  // gate/up interleaved by 16-row strips: strip 2s = gate rows 16s.., 2s+1 = up rows.
+  std::vector<int32_t> gu_map(2 * F);
+  for (size_t n = 0; n < 2 * F; ++n) {
+    size_t strip = n / 16;
+    gu_map[n] = (int32_t)((strip % 2 ? F : 0) + (strip / 2) * 16 + n % 16);
+  }
+  const std::vector<int32_t> map_D = ident(D), map_V = ident(V);
+
+  if (hipMemcpyAsync(m->embed, t[0], V * D * 2, hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(set_err(HVD_ERR_DEVICE, "embedding upload failed"));
+  for (int l = 0; l < c.n_layers && st == HVD_OK; ++l) {
+    const uint16_t* const* lt = t + 1 + 9 * l;
+    LayerW& L = m->layers[l];
+    if ((st = upload_gain(lt[0], L.g_attn, (int)D, s)) != HVD_OK) break;
+    if ((st = pack_group({{lt[1], qd * D}, {lt[2], kd * D}, {lt[3], kd * D}}, qkv_map, (int)D, staging, dmap, L.qkv, s)) != HVD_OK) break;
+    if ((st = pack_group({{lt[4], D * qd}}, map_D, (int)qd, staging, dmap, L.o, s)) != HVD_OK) break;
+    if ((st = upload_gain(lt[5], L.g_mlp, (int)D, s)) != HVD_OK) break;
+    if ((st = pack_group({{lt[6], F * D}, {lt[7], F * D}}, gu_map, (int)D, staging, dmap, L.gu, s)) != HVD_OK) break;
+    if ((st = pack_group({{lt[8], D * F}}, map_D, (int)F, staging, dmap, L.down, s)) != HVD_OK) break;
+  }
+  if (st == HVD_OK) st = upload_gain(t[1 + 9 * c.n_layers], m->g_final, (int)D, s);
+  if (st == HVD_OK) st = pack_group({{t[2 + 9 * c.n_layers], V * D}}, map_V, (int)D, staging, dmap, m->lm, s);
+  if (st != HVD_OK) return fail(st);
+
+  // rotary table: angle = pos * theta^(-2j/dh) in double, stored as fp32 (cos, sin)
+  {
+    const int half = c.head_dim / 2;
+    std::vector<float2> tab((size_t)c.max_pos * half);
+    for (int p = 0; p < c.max_pos; ++p)
+      for (int j = 0; j < half; ++j) {
+        double ang = (double)p * std::pow((double)c.rope_theta, -(2.0 * j) / c.head_dim);
+        tab[(size_t)p * half + j] = float2{(float)std::cos(ang), (float)std::sin(ang)};
+      }
+    if (hipMemcpyAsync(m->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return fail(set_err(HVD_ERR_DEVICE, "rotary table upload failed"));
+  }
+  (void)hipFree(staging);
+  (void)hipFree(dmap);
+  *out = m;
+  return HVD_OK;
+}
+
+extern "C" void hvd_model_free(hvd_model m) {
+  if (!m) return;
+  if (m->owned && m->base) (void)hipFree(m->base);
+  delete m;
+}
+
+// ------------------------------------------------------------------ KV handle
+
+struct ProfRec {
+  hipEvent_t a, b;
+  int family;
+  double bytes;
+};
+
+struct hvd_kv_s {
+  hvd_model_s* m = nullptr;
+  HostState* hs = nullptr;
+  void* base = nullptr;
+  bool owned = false;
+  hipStream_t stream = nullptr;
+  int32_t n_pages = 0;
+  _Float16* pool = nullptr;
+  size_t page_stride = 0;   // halves per (layer, page): K and V of every kv head
+  size_t layer_stride = 0;  // halves per layer
+  int32_t* pt = nullptr;
+  int pt_stride = 0;
+  int max_rows = 0, MTmax = 0;
+  float* X = nullptr;
+  float* ss = nullptr;
+  uint16_t *Nhi = nullptr, *Nlo = nullptr;
+  _Float16* Q = nullptr;
+  uint16_t *Ohi = nullptr, *Olo = nullptr;
+  uint16_t *Ahi = nullptr, *Alo = nullptr;
+  float* lm_val = nullptr;
+  int32_t* lm_idx = nullptr;
+  int n_part_lm = 0;
+  int32_t* g = nullptr;
+  int32_t* out = nullptr;
+  uint32_t* counter = nullptr;
+  float* part_o = nullptr;
+  float* part_ml = nullptr;
+  int32_t* meta_dev = nullptr;
+  int32_t* meta_host = nullptr;
+  size_t meta_ints = 0;
+  int32_t* out_host = nullptr;
+  // profiling
+  bool prof = false;
+  std::vector<ProfRec> prof_pending;
+  std::vector<hipEvent_t> ev_pool;
+  double prof_ms[3] = {0, 0, 0}, prof_bytes[3] = {0, 0, 0};
+  int64_t prof_n[3] = {0, 0, 0};
+};
+
+namespace {
+
+// Upper bound of one step's metadata: rows, sequences, attention items and
+// combine heads (units = sequence x kv head x row group), page-table updates.
+size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int pt_stride) {
+  const int G = c.n_q_heads / c.n_kv_heads;
+  const size_t rg_verify = ((size_t)(c.max_draft + 1) * G + kAttnRows - 1) / kAttnRows;
+  const size_t rg_prefill = ((size_t)kPrefillRows * G + kAttnRows - 1) / kAttnRows;
+  const size_t units = std::max((size_t)max_seqs * rg_verify, rg_prefill) * c.n_kv_heads;
+  return 4 * (size_t)max_rows + 4 * (size_t)max_seqs + 8 * (2 * units + kPartSlots) +
+         3 * (size_t)max_seqs * pt_stride + 64;
+}
+
+size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, void* base) {
+  Carver cv(base);
+  const size_t D = c.d_model, F = c.ffn_dim, qd = (size_t)c.n_q_heads * c.head_dim;
+  k->page_stride = (size_t)2 * c.n_kv_heads * kPage * c.head_dim;
+  k->layer_stride = k->page_stride * n_pages;
+  k->pool = cv.take<_Float16>(k->layer_stride * c.n_layers);
+  k->pt_stride = (c.max_pos + kPage) / kPage + 1;
+  k->pt = cv.take<int32_t>((size_t)max_seqs * k->pt_stride);
+  k->max_rows = std::max(max_seqs * (c.max_draft + 1), kPrefillRows);
+  k->MTmax = (k->max_rows + 15) / 16;
+  const size_t Mp = (size_t)k->MTmax * 16;
+  k->X = cv.take<float>(Mp * D);
+  k->ss = cv.take<float>(Mp * (D / 16));
+  k->Nhi = cv.take<uint16_t>(Mp * D);
+  k->Nlo = cv.take<uint16_t>(Mp * D);
+  k->Q = cv.take<_Float16>(Mp * qd);
+  k->Ohi = cv.take<uint16_t>(Mp * qd);
+  k->Olo = cv.take<uint16_t>(Mp * qd);
+  k->Ahi = cv.take<uint16_t>(Mp * F);
+  k->Alo = cv.take<uint16_t>(Mp * F);
+  k->n_part_lm = c.vocab / 16 / gemm_strips_per_block(EPI_LM);
+  k->lm_val = cv.take<float>(Mp * k->n_part_lm);
+  k->lm_idx = cv.take<int32_t>(Mp * k->n_part_lm);
+  k->g = cv.take<int32_t>(Mp);
+  k->out = cv.take<int32_t>(2 * (size_t)max_seqs);
+  k->counter = cv.take<uint32_t>(64);
+  k->part_o = cv.take<float>((size_t)kPartSlots * kAttnRows * c.head_dim);
+  k->part_ml = cv.take<float>((size_t)kPartSlots * kAttnRows * 2);
+  k->meta_ints = meta_capacity_ints(c, k->max_rows, max_seqs, k->pt_stride);
+  k->meta_dev = cv.take<int32_t>(k->meta_ints);
+  return cv.off;
+}
+
+}  // namespace
+
+extern "C" size_t hvd_kv_bytes(const hvd_config* cfg, int32_t max_seqs, int32_t n_pages) {
+  if (check_config(cfg) != HVD_OK || max_seqs < 1 || n_pages < 1) return 0;
+  hvd_kv_s tmp;
+  return carve_kv(&tmp, *cfg, max_seqs, n_pages, nullptr);
+}
+
+extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_pages, void* dev_buf, size_t dev_bytes,
+                                   void* stream, hvd_kv* out) {
+  if (!m || !out) return set_err(HVD_ERR_ARG, "null model or out");
+  if (max_seqs < 1 || n_pages < 1) return set_err(HVD_ERR_ARG, "max_seqs and n_pages must be >= 1");
+  const hvd_config& c = m->cfg;
+  auto* k = new hvd_kv_s();
+  k->m = m;
+  k->stream = (hipStream_t)stream;
+  k->n_pages = n_pages;
+  const size_t need = carve_kv(k, c, max_seqs, n_pages, nullptr);
+  if (dev_buf) {
+    if (dev_bytes < need) {
+      delete k;
+      return set_err(HVD_ERR_ARG, "dev_buf smaller than hvd_kv_bytes");
+    }
+    k->base = dev_buf;
+  } else {
+    if (hipMalloc(&k->base, need) != hipSuccess) {
+      delete k;
+      return set_err(HVD_ERR_OOM, "hipMalloc of the KV pool failed");
+    }
+    k->owned = true;
+  }
+  carve_kv(k, c, max_seqs, n_pages, k->base);
+  if (hipHostMalloc((void**)&k->meta_host, k->meta_ints * 4, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&k->out_host, 2 * (size_t)max_seqs * 4, hipHostMallocDefault) != hipSuccess) {
+    if (k->meta_host) (void)hipHostFree(k->meta_host);
+    if (k->owned) (void)hipFree(k->base);
+    delete k;
+    return set_err(HVD_ERR_OOM, "pinned host staging allocation failed");
+  }
+  // Zero the whole workspace once: padding rows of every operand stay finite.
+  // (KV pages are zeroed too; their contents are only read once written.)
+  if (hipMemsetAsync(k->base, 0, need, k->stream) != hipSuccess || hipStreamSynchronize(k->stream) != hipSuccess) {
+    (void)hipHostFree(k->meta_host);
+    (void)hipHostFree(k->out_host);
+    if (k->owned) (void)hipFree(k->base);
+    delete k;
+    return set_err(HVD_ERR_DEVICE, "workspace clear failed");
+  }
+  k->hs = new HostState(max_seqs, n_pages, kPage, c.max_pos, c.max_draft, c.vocab);
+  *out = k;
+  return HVD_OK;
+}
+
+extern "C" void hvd_kv_free(hvd_kv k) {
+  if (!k) return;
+  for (auto e : k->ev_pool) (void)hipEventDestroy(e);
+  for (auto& r : k->prof_pending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  if (k->meta_host) (void)hipHostFree(k->meta_host);
+  if (k->out_host) (void)hipHostFree(k->out_host);
+  if (k->owned && k->base) (void)hipFree(k->base);
+  delete k->hs;
+  delete k;
+}
+
+// ------------------------------------------------------------------ forward
+
+namespace {
+
+hipEvent_t take_event(hvd_kv_s* k) {
+  if (!k->ev_pool.empty()) {
+    hipEvent_t e = k->ev_pool.back();
+    k->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+
+// Bracket one launch with events when profiling.
+struct ProfScope {
+  hvd_kv_s* k;
+  ProfRec r{};
+  ProfScope(hvd_kv_s* k_, int family, double bytes) : k(k_) {
+    if (!k->prof) return;
+    r.a = take_event(k);
+    r.b = take_event(k);
+    r.family = family;
+    r.bytes = bytes;
+    (void)hipEventRecord(r.a, k->stream);
+  }
+  ~ProfScope() {
+    if (!k->prof) return;
+    (void)hipEventRecord(r.b, k->stream);
+    k->prof_pending.push_back(r);
+  }
+};
+
+void prof_collect(hvd_kv_s* k) {
+  for (auto& r : k->prof_pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      k->prof_ms[r.family] += ms;
+      k->prof_n[r.family] += 1;
+      k->prof_bytes[r.family] += r.bytes;
+    }
+    k->ev_pool.push_back(r.a);
+    k->ev_pool.push_back(r.b);
+  }
+  k->prof_pending.clear();
+}
+
+struct Plan {
+  std::vector<AttnItem> items, heads;
+  int chunk = 0;
+};
+
+// Split every (sequence, kv head, row group) into KV chunks of `chunk`
+// positions, chosen so the launch has enough workgroups to fill the GPU.
+bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, Plan& p) {
+  const int G = c.n_q_heads / c.n_kv_heads;
+  struct Unit { int b, g, rg, keys; };
+  std::vector<Unit> units;
+  int64_t total_keys = 0;
+  for (int b = 0; b < (int)seqs.size(); ++b) {
+    const SeqMeta& s = seqs[b];
+    const int R = (s.k + 1) * G;
+    const int n_rg = (R + kAttnRows - 1) / kAttnRows;
+    for (int g = 0; g < c.n_kv_heads; ++g)
+      for (int rg = 0; rg < n_rg; ++rg) {
+        const int i_max = std::min(s.k, ((rg + 1) * kAttnRows - 1) / G);
+        const int keys = s.ctx + i_max + 1;
+        units.push_back({b, g, rg, keys});
+        total_keys += keys;
+      }
+  }
+  int chunk = (int)std::min<int64_t>(1 << 20, std::max<int64_t>(64, ((total_keys / 512) + 31) / 32 * 32));
+  for (;;) {
+    p.items.clear();
+    p.heads.clear();
+    int slots = 0;
+    for (const Unit& u : units) {
+      const int nch = (u.keys + chunk - 1) / chunk;
+      if (nch == 1) {
+        p.items.push_back({u.b, u.g, 0, 1, u.rg, -1, 0, 0});
+      } else {
+        p.heads.push_back({u.b, u.g, 0, nch, u.rg, slots, 0, 0});
+        for (int ci = 0; ci < nch; ++ci) p.items.push_back({u.b, u.g, ci, nch, u.rg, slots + ci, 0, 0});
+        slots += nch;
+      }
+    }
+    if (slots <= kPartSlots && (int)p.items.size() <= 65535 * 4) break;
+    chunk *= 2;
+  }
+  p.chunk = chunk;
+  return true;
+}
+
+hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vector<RowMeta>& rows, bool lm_head,
+                   float* logits) {
+  hvd_model_s* m = k->m;
+  const hvd_config& c = m->cfg;
+  hipStream_t s = k->stream;
+  const int M = (int)rows.size();
+  const int MT = (M + 15) / 16;
+  if (MT > k->MTmax) return set_err(HVD_ERR_OOM, "row workspace too small");
+  const int B = (int)seqs.size();
+  const int D = c.d_model, F = c.ffn_dim, dh = c.head_dim, qd = c.n_q_heads * dh, kvd = c.n_kv_heads * dh;
+  const int G = c.n_q_heads / c.n_kv_heads;
+
+  Plan plan;
+  plan_attention(c, seqs, plan);
+  std::vector<PageUpdate> upd_raw = k->hs->take_updates();
+  // keep the last update of each (slot, index): they are applied in parallel
+  std::map<std::pair<int, int>, int> last;
+  for (auto& u : upd_raw) last[{u.slot, u.index}] = u.page;
+
+  // pack metadata: rows | seqs | items | heads | updates
+  int32_t* h = k->meta_host;
+  size_t off = 0;
+  auto put = [&](const void* src, size_t ints) {
+    std::memcpy(h + off, src, ints * 4);
+    size_t o = off;
+    off += (ints + 3) / 4 * 4;
+    return o;
+  };
+  const size_t need_ints = 4 * (size_t)M + 4 * (size_t)B + 8 * (plan.items.size() + plan.heads.size()) +
+                           3 * last.size() + 32;
+  if (need_ints > k->meta_ints) {
+    k->hs->take_updates();
+    return set_err(HVD_ERR_OOM, "metadata buffer too small");
+  }
+  const size_t o_rows = put(rows.data(), 4 * (size_t)M);
+  const size_t o_seqs = put(seqs.data(), 4 * (size_t)B);
+  const size_t o_items = put(plan.items.data(), 8 * plan.items.size());
+  const size_t o_heads = put(plan.heads.data(), 8 * plan.heads.size());
+  std::vector<int32_t> upd;
+  for (auto& kv : last) {
+    upd.push_back(kv.first.first);
+    upd.push_back(kv.first.second);
+    upd.push_back(kv.second);
+  }
+  const size_t o_upd = put(upd.data(), upd.size());
+  HIP_TRY(hipMemcpyAsync(k->meta_dev, h, off * 4, hipMemcpyHostToDevice, s));
+  const RowMeta* d_rows = (const RowMeta*)(k->meta_dev + o_rows);
+  const SeqMeta* d_seqs = (const SeqMeta*)(k->meta_dev + o_seqs);
+  const AttnItem* d_items = (const AttnItem*)(k->meta_dev + o_items);
+  const AttnItem* d_heads = (const AttnItem*)(k->meta_dev + o_heads);
+
+  {
+    EmbedArgs e{};
+    e.E = m->embed;
+    e.rows = d_rows;
+    e.M = M;
+    e.Mpad = MT * 16;
+    e.D = D;
+    e.gain = m->layers[0].g_attn;
+    e.X = k->X;
+    e.Nhi = k->Nhi;
+    e.Nlo = k->Nlo;
+    e.ss_out = k->ss;
+    e.MTtot = MT;
+    e.upd = k->meta_dev + o_upd;
+    e.n_upd = (int)last.size();
+    e.pt = k->pt;
+    e.pt_stride = k->pt_stride;
+    ProfScope ps(k, 2, 0.0);
+    HIP_TRY(launch_embed(e, s));
+  }
+
+  const int mt_block = std::min(MT, kMaxMTile);
+  const int mblocks = (MT + mt_block - 1) / mt_block;
+  auto gemm = [&](int epi, GemmArgs& a, int N, int K) -> hvd_status {
+    a.KT = K / 32;
+    a.NT = N / 16;
+    a.MTtot = MT;
+    a.M = M;
+    ProfScope ps(k, 0, (double)N * K * 2.0);
+    HIP_TRY(launch_gemm(epi, a, mblocks, mt_block, s));
+    return HVD_OK;
+  };
+  double kv_bytes = 0;
+  for (auto& sq : seqs) kv_bytes += (double)(sq.ctx + sq.k + 1) * kvd * 2 * 2;
+
+  for (int l = 0; l < c.n_layers; ++l) {
+    const LayerW& L = m->layers[l];
+    _Float16* kvl = k->pool + (size_t)l * k->layer_stride;
+    {
+      GemmArgs a{};
+      a.W = (const uint4*)L.qkv;
+      a.Ahi = (const uint4*)k->Nhi;
+      a.Alo = (const uint4*)k->Nlo;
+      a.ss = k->ss;
+      a.ss_n = D / 16;
+      a.inv_dim = 1.f / D;
+      a.eps = c.rms_eps;
+      a.Q = k->Q;
+      a.kv = kvl;
+      a.page_stride = k->page_stride;
+      a.q_cols = qd;
+      a.kv_cols = kvd;
+      a.Hkv = c.n_kv_heads;
+      a.dh = dh;
+      a.pt = k->pt;
+      a.pt_stride = k->pt_stride;
+      a.rows = d_rows;
+      a.rope = m->rope;
+      if (hvd_status st = gemm(EPI_QKV, a, qd + 2 * kvd, D); st != HVD_OK) return st;
+    }
+    {
+      AttnArgs a{};
+      a.Q = k->Q;
+      a.kv = kvl;
+      a.page_stride = k->page_stride;
+      a.Hq = c.n_q_heads;
+      a.Hkv = c.n_kv_heads;
+      a.dh = dh;
+      a.group = G;
+      a.pt = k->pt;
+      a.pt_stride = k->pt_stride;
+      a.seqs = d_seqs;
+      a.items = d_items;
+      a.chunk = plan.chunk;
+      a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
+      a.Ohi = k->Ohi;
+      a.Olo = k->Olo;
+      a.MTtot = MT;
+      a.part_o = k->part_o;
+      a.part_ml = k->part_ml;
+      {
+        ProfScope ps(k, 1, kv_bytes);
+        HIP_TRY(launch_attn(a, (int)plan.items.size(), s));
+      }
+      if (!plan.heads.empty()) {
+        CombineArgs cb{};
+        cb.seqs = d_seqs;
+        cb.heads = d_heads;
+        cb.Hq = c.n_q_heads;
+        cb.Hkv = c.n_kv_heads;
+        cb.dh = dh;
+        cb.group = G;
+        cb.part_o = k->part_o;
+        cb.part_ml = k->part_ml;
+        cb.Ohi = k->Ohi;
+        cb.Olo = k->Olo;
+        cb.MTtot = MT;
+        ProfScope ps(k, 2, 0.0);
+        HIP_TRY(launch_combine(cb, (int)plan.heads.size(), s));
+      }
+    }
+    {
+      GemmArgs a{};
+      a.W = (const uint4*)L.o;
+      a.Ahi = (const uint4*)k->Ohi;
+      a.Alo = (const uint4*)k->Olo;
+      a.X = k->X;
+      a.D = D;
+      a.gain_next = L.g_mlp;
+      a.Nhi = k->Nhi;
+      a.Nlo = k->Nlo;
+      a.ss_out = k->ss;
+      if (hvd_status st = gemm(EPI_RESID, a, D, qd); st != HVD_OK) return st;
+    }
+    {
+      GemmArgs a{};
+      a.W = (const uint4*)L.gu;
+      a.Ahi = (const uint4*)k->Nhi;
+      a.Alo = (const uint4*)k->Nlo;
+      a.ss = k->ss;
+      a.ss_n = D / 16;
+      a.inv_dim = 1.f / D;
+      a.eps = c.rms_eps;
+      a.act_hi = k->Ahi;
+      a.act_lo = k->Alo;
+      if (hvd_status st = gemm(EPI_SILU, a, 2 * F, D); st != HVD_OK) return st;
+    }
+    {
+      GemmArgs a{};
+      a.W = (const uint4*)L.down;
+      a.Ahi = (const uint4*)k->Ahi;
+      a.Alo = (const uint4*)k->Alo;
+      a.X = k->X;
+      a.D = D;
+      a.gain_next = (l + 1 < c.n_layers) ? m->layers[l + 1].g_attn : m->g_final;
+      a.Nhi = k->Nhi;
+      a.Nlo = k->Nlo;
+      a.ss_out = k->ss;
+      if (hvd_status st = gemm(EPI_RESID, a, D, F); st != HVD_OK) return st;
+    }
+  }
+  if (lm_head) {
+    GemmArgs a{};
+    a.W = (const uint4*)m->lm;
+    a.Ahi = (const uint4*)k->Nhi;
+    a.Alo = (const uint4*)k->Nlo;
+    a.ss = k->ss;
+    a.ss_n = D / 16;
+    a.inv_dim = 1.f / D;
+    a.eps = c.rms_eps;
+    a.logits = logits;
+    a.vocab = c.vocab;
+    a.part_val = k->lm_val;
+    a.part_idx = k->lm_idx;
+    a.n_part = k->n_part_lm;
+    if (hvd_status st = gemm(EPI_LM, a, c.vocab, D); st != HVD_OK) return st;
+    AcceptArgs ac{};
+    ac.part_val = k->lm_val;
+    ac.part_idx = k->lm_idx;
+    ac.n_part = k->n_part_lm;
+    ac.M = M;
+    ac.g = k->g;
+    ac.seqs = d_seqs;
+    ac.rows = d_rows;
+    ac.B = B;
+    ac.out = k->out;
+    ac.counter = k->counter;
+    {
+      ProfScope ps(k, 2, 0.0);
+      HIP_TRY(launch_accept(ac, s));
+    }
+    HIP_TRY(hipMemcpyAsync(k->out_host, k->out, 2 * (size_t)B * 4, hipMemcpyDeviceToHost, s));
+  }
+  HIP_TRY(hipStreamSynchronize(s));
+  if (k->prof) prof_collect(k);
+  return HVD_OK;
+}
+
+hvd_status from_host(int code, hvd_kv_s* k) {
+  if (code == HS_OK) return HVD_OK;
+  return set_err((hvd_status)code, k->hs->error());
+}
+
+}  // namespace
+
+extern "C" hvd_status hvd_prefill(hvd_model m, hvd_kv k, int32_t seq_id, const int32_t* tokens, int32_t n) {
+  if (!m || !k) return set_err(HVD_ERR_ARG, "null handle");
+  if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
+  if (hvd_status st = from_host(k->hs->begin_prefill(seq_id, tokens, n), k); st != HVD_OK) return st;
+  const int body = n - 1;
+  for (int s0 = 0; s0 < body; s0 += kPrefillRows) {
+    const int cnt = std::min(kPrefillRows, body - s0);
+    std::vector<SeqMeta> seqs{{seq_id, s0, cnt - 1, 0}};
+    std::vector<RowMeta> rows(cnt);
+    for (int i = 0; i < cnt; ++i) rows[i] = {tokens[s0 + i], seq_id, s0 + i, 0};
+    hvd_status st = forward(k, seqs, rows, false, nullptr);
+    if (st != HVD_OK) {
+      k->hs->abort_prefill(seq_id);
+      return st;
+    }
+  }
+  return HVD_OK;
+}
+
+extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids, const int32_t* ctx_lens,
+                                 const int32_t* draft_tokens, const int32_t* draft_lens, int32_t* accepted_len,
+                                 int32_t* next_token, float* logits) {
+  if (!m || !k) return set_err(HVD_ERR_ARG, "null handle");
+  if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
+  if (!accepted_len || !next_token) return set_err(HVD_ERR_ARG, "null output");
+  if (hvd_status st = from_host(k->hs->begin_verify(batch, seq_ids, ctx_lens, draft_tokens, draft_lens), k);
+      st != HVD_OK)
+    return st;
+  std::vector<SeqMeta> seqs(batch);
+  std::vector<RowMeta> rows;
+  int64_t off = 0;
+  for (int b = 0; b < batch; ++b) {
+    const SeqSlot& sl = k->hs->seq(seq_ids[b]);
+    const int kk = draft_lens[b];
+    seqs[b] = {seq_ids[b], sl.ctx, kk, (int32_t)rows.size()};
+    rows.push_back({sl.pending, seq_ids[b], sl.ctx, 0});
+    for (int i = 0; i < kk; ++i) rows.push_back({draft_tokens[off + i], seq_ids[b], sl.ctx + 1 + i, 0});
+    off += kk;
+  }
+  hvd_status st = forward(k, seqs, rows, true, logits);
+  if (st != HVD_OK) {
+    k->hs->abort_verify(batch, seq_ids);
+    return st;
+  }
+  for (int b = 0; b < batch; ++b) {
+    accepted_len[b] = k->out_host[2 * b];
+    next_token[b] = k->out_host[2 * b + 1];
+  }
+  k->hs->finish_verify(batch, seq_ids, draft_tokens, draft_lens, accepted_len, next_token);
+  return HVD_OK;
+}
+
+extern "C" hvd_status hvd_commit(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids, const int32_t* keep) {
+  if (!m || !k) return set_err(HVD_ERR_ARG, "null handle");
+  if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
+  return from_host(k->hs->commit(batch, seq_ids, keep), k);
+}
+
+extern "C" hvd_status hvd_truncate(hvd_kv k, int32_t seq_id, int32_t new_ctx_len, int32_t pending_token) {
+  if (!k) return set_err(HVD_ERR_ARG, "null handle");
+  return from_host(k->hs->truncate(seq_id, new_ctx_len, pending_token), k);
+}
+
+extern "C" hvd_status hvd_seq_free(hvd_kv k, int32_t seq_id) {
+  if (!k) return set_err(HVD_ERR_ARG, "null handle");
+  return from_host(k->hs->free_seq(seq_id), k);
+}
+
+extern "C" hvd_status hvd_seq_info(hvd_kv k, int32_t seq_id, int32_t* ctx_len, int32_t* pending, int32_t* vp) {
+  if (!k) return set_err(HVD_ERR_ARG, "null handle");
+  if (seq_id < 0 || seq_id >= k->hs->max_seqs() || !k->hs->seq(seq_id).live)
+    return set_err(HVD_ERR_ARG, "unknown seq_id");
+  const SeqSlot& s = k->hs->seq(seq_id);
+  if (ctx_len) *ctx_len = s.ctx;
+  if (pending) *pending = s.pending;
+  if (vp) *vp = s.verify_pending ? 1 : 0;
+  return HVD_OK;
+}
+
+extern "C" int32_t hvd_kv_free_pages(hvd_kv k) { return k ? k->hs->free_pages() : -1; }
+
+extern "C" hvd_status hvd_profile_enable(hvd_kv k, int32_t enable) {
+  if (!k) return set_err(HVD_ERR_ARG, "null handle");
+  k->prof = enable != 0;
+  for (int i = 0; i < 3; ++i) {
+    k->prof_ms[i] = 0;
+    k->prof_bytes[i] = 0;
+    k->prof_n[i] = 0;
+  }
+  return HVD_OK;
+}
+
+extern "C" hvd_status hvd_profile_read(hvd_kv k, int32_t family, double* ms, int64_t* launches, double* bytes) {
+  if (!k || family < 0 || family > 2) return set_err(HVD_ERR_ARG, "bad handle or family");
+  if (ms) *ms = k->prof_ms[family];
+  if (launches) *launches = k->prof_n[family];
+  if (bytes) *bytes = k->prof_bytes[family];
+  return HVD_OK;
+}
+
+extern "C" const char* hvd_last_error(void) { return g_err.c_str(); }

@@ -1,0 +1,55 @@
+// Shared device types and helpers for the gfx950 kernels of libhvd.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+namespace hvd {
+
+constexpr int kWave = 64;
+
+constexpr int kFragElems = 512;  // one 16x32 MFMA operand fragment: 64 lanes x 8 halves
+
+// Round-to-nearest-even float -> bf16 bits (inputs are finite).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// Split v into hi + lo bf16 parts: hi = bf16(v), lo = bf16(v - hi).  hi + lo
+// carries about 16 significant bits of v.
+__device__ __forceinline__ void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
+  hi = f2bf(v);
+  lo = f2bf(v - bf2f(hi));
+}
+
+// Offset (in halves) of element (row, col) inside a fragment-packed operand
+// with `mtiles` 16-row tiles: fragment (kt = col/32, mt = row/16) is 64 lanes
+// x 8 halves; lane = row%16 + 16*((col%32)/8), half = col%8.
+__device__ __forceinline__ size_t afrag_off(int row, int col, int mtiles) {
+  int kt = col >> 5, mt = row >> 4;
+  int lane = (row & 15) + ((col & 31) >> 3) * 16;
+  return ((size_t)(kt * mtiles + mt) * 64 + lane) * 8 + (col & 7);
+}
+
+__device__ __forceinline__ f32x4 mfma_bf16(const u32x4& a, const u32x4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_f16(const f16x8& a, const f16x8& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+}  // namespace hvd

@@ -1,0 +1,136 @@
+// Kernel argument blocks and host-side launchers of libhvd (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hvd {
+
+constexpr int kPage = 16;  // tokens per KV page
+
+// Row metadata of one forward: token, sequence slot, absolute position.
+struct RowMeta {
+  int32_t tok, slot, pos, pad;
+};
+// Sequence metadata of one forward: slot, cached length, draft length k,
+// first row (rows cu .. cu+k).
+struct SeqMeta {
+  int32_t slot, ctx, k, cu;
+};
+// One attention work item: sequence entry b, kv head g, KV chunk c of nch,
+// the row group rg (rows [rg*128, rg*128+128) of the (k+1)*group rows) and,
+// for multi-chunk items, the partial slot `part`.
+struct AttnItem {
+  int32_t b, g, c, nch, rg, part, pad0, pad1;
+};
+
+enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_LM = 3 };
+
+struct GemmArgs {
+  const uint4* W;    // packed weights, fragment (nt, kt) at (nt*KT + kt)*64 lanes
+  const uint4* Ahi;  // packed activations (hi part), fragment (kt, mt) at (kt*MTtot + mt)*64
+  const uint4* Alo;  // packed activations (lo part)
+  int KT, NT, MTtot, M;
+  // inverse RMS of the GEMM's input rows, from per-16-column sums of squares
+  const float* ss;   // [MTtot*16][ss_n] (null: no row scaling)
+  int ss_n;
+  float inv_dim, eps;
+  // EPI_QKV
+  _Float16* Q;       // [M][Hq*dh], d in rotary-pair order
+  _Float16* kv;      // this layer's KV pool: page p, K at p*page_stride, V at +Hkv*16*dh
+  size_t page_stride;
+  int q_cols, kv_cols, Hkv, dh;
+  const int32_t* pt;  // page table [max_seqs][pt_stride]
+  int pt_stride;
+  const RowMeta* rows;
+  const float2* rope;  // [max_pos][dh/2] (cos, sin)
+  // EPI_RESID
+  float* X;            // residual stream [MTtot*16][D] fp32
+  int D;
+  const float* gain_next;  // gain of the norm that consumes X next
+  uint16_t* Nhi;       // next GEMM's A operand (hi), K = D
+  uint16_t* Nlo;
+  float* ss_out;       // [MTtot*16][D/16]
+  // EPI_SILU
+  uint16_t* act_hi;    // down GEMM's A operand, K = F
+  uint16_t* act_lo;
+  // EPI_LM
+  float* logits;       // [M][vocab] or null
+  int vocab;
+  float* part_val;     // [M][n_part]
+  int32_t* part_idx;
+  int n_part;
+};
+
+struct AttnArgs {
+  const _Float16* Q;
+  const _Float16* kv;  // this layer's pool
+  size_t page_stride;
+  int Hq, Hkv, dh, group;
+  const int32_t* pt;
+  int pt_stride;
+  const SeqMeta* seqs;
+  const AttnItem* items;
+  int chunk;           // positions per KV chunk (multiple of 32)
+  float scale_log2;    // log2(e) / sqrt(dh)
+  uint16_t* Ohi;       // O GEMM A operand (K = Hq*dh)
+  uint16_t* Olo;
+  int MTtot;
+  float* part_o;       // [slots][128][dh] fp32 unnormalized output of one chunk
+  float* part_ml;      // [slots][128][2] running max (base 2) and sum
+};
+
+struct CombineArgs {
+  const SeqMeta* seqs;
+  const AttnItem* heads;  // one entry per (b, g, rg) whose nch > 1; part = first slot
+  int Hq, Hkv, dh, group;
+  const float* part_o;
+  const float* part_ml;
+  uint16_t* Ohi;
+  uint16_t* Olo;
+  int MTtot;
+};
+
+struct EmbedArgs {
+  const uint16_t* E;   // embedding [V][D] bf16
+  const RowMeta* rows;
+  int M, Mpad, D;
+  const float* gain;
+  float* X;
+  uint16_t* Nhi;
+  uint16_t* Nlo;
+  float* ss_out;
+  int MTtot;
+  // page-table updates applied before any KV write of this step
+  const int32_t* upd;  // [n_upd][3]: slot, index, page
+  int n_upd;
+  int32_t* pt;
+  int pt_stride;
+};
+
+struct AcceptArgs {
+  const float* part_val;
+  const int32_t* part_idx;
+  int n_part;
+  int M;
+  int32_t* g;          // [M] argmax per row
+  const SeqMeta* seqs;
+  const RowMeta* rows;
+  int B;
+  int32_t* out;        // [B][2]: accepted, next
+  uint32_t* counter;   // one uint32, zero between launches
+};
+
+// Launchers: all enqueue on `s` and return the launch status.
+hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst, int N, int K,
+                       hipStream_t s);
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+hipError_t launch_gemm(int epi, const GemmArgs& a, int mblocks, int mt_block, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, int n_items, hipStream_t s);
+hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+
+// Strips (16 output columns) handled by one GEMM workgroup for an epilogue.
+int gemm_strips_per_block(int epi);
+
+}  // namespace hvd

@@ -1,0 +1,144 @@
+// Small kernels of the verify step: weight packing (load time), embedding
+// gather with the first RMSNorm's operand, and the fused argmax finalize +
+// greedy accept.
+#include "common.h"
+#include "kernels.h"
+
+namespace hvd {
+
+// dst fragment (s, kt), lane l, half j = src[rowmap[16 s + l%16]][32 kt + 8 (l/16) + j]
+__global__ void pack_weight(const uint16_t* __restrict__ src, const int32_t* __restrict__ rowmap,
+                            uint16_t* __restrict__ dst, int N, int K) {
+  const int KT = K >> 5;
+  const size_t total = (size_t)(N >> 4) * KT * 64;
+  for (size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (size_t)gridDim.x * blockDim.x) {
+    const int l = (int)(t & 63);
+    const size_t frag = t >> 6;
+    const int kt = (int)(frag % KT);
+    const int s = (int)(frag / KT);
+    const int srow = rowmap[s * 16 + (l & 15)];
+    const uint4 v = *(const uint4*)(src + (size_t)srow * K + kt * 32 + (l >> 4) * 8);
+    *(uint4*)(dst + t * 8) = v;
+  }
+}
+
+hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst, int N, int K, hipStream_t s) {
+  size_t total = (size_t)(N / 16) * (K / 32) * 64;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 65535 * 8) blocks = 65535 * 8;
+  hipLaunchKernelGGL(pack_weight, dim3(blocks), dim3(256), 0, s, src, rowmap, dst, N, K);
+  return hipGetLastError();
+}
+
+// One block per (padded) row: X = fp32(E[tok]), the first norm's operand
+// bf16 split of X * gain, per-16-column sums of squares.  Block 0 first
+// applies this step's page-table updates.
+__global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
+  if (blockIdx.x == 0)
+    for (int u = threadIdx.x; u < a.n_upd; u += blockDim.x)
+      a.pt[(size_t)a.upd[u * 3] * a.pt_stride + a.upd[u * 3 + 1]] = a.upd[u * 3 + 2];
+  const int R = blockIdx.x;
+  const bool valid = R < a.M;
+  const uint16_t* er = valid ? a.E + (size_t)a.rows[R].tok * a.D : nullptr;
+  const int noct = a.D >> 3;
+  for (int base = 0; base < noct; base += 256) {
+    const int o = base + threadIdx.x;
+    const bool ok = o < noct;
+    float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (ok && valid) {
+      const uint4 v = *(const uint4*)(er + o * 8);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[2 * j] = __uint_as_float(w[j] << 16);
+        x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+      }
+    }
+    float sq = 0.f;
+    if (ok) {
+      const int C = o * 8;
+      float* xp = a.X + (size_t)R * a.D + C;
+      *(float4*)xp = float4{x[0], x[1], x[2], x[3]};
+      *(float4*)(xp + 4) = float4{x[4], x[5], x[6], x[7]};
+      uint16_t hi[8], lo[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        sq += x[j] * x[j];
+        split_bf16(x[j] * a.gain[C + j], hi[j], lo[j]);
+      }
+      const size_t off = afrag_off(R, C, a.MTtot);
+      *(uint4*)(a.Nhi + off) = uint4{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16),
+                                     hi[4] | ((uint32_t)hi[5] << 16), hi[6] | ((uint32_t)hi[7] << 16)};
+      *(uint4*)(a.Nlo + off) = uint4{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16),
+                                     lo[4] | ((uint32_t)lo[5] << 16), lo[6] | ((uint32_t)lo[7] << 16)};
+    }
+    const float other = __shfl_xor(sq, 1);
+    if (ok && (o & 1) == 0) a.ss_out[(size_t)R * (a.D >> 4) + (o >> 1)] = sq + other;
+  }
+}
+
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(embed_rows, dim3(a.Mpad), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// One block per row: reduce the LM head's per-block (max, lowest argmax)
+// partials to the row argmax g[r] (ties -> lowest token id).  The last block
+// to finish applies the accept rule to every sequence: a = number of leading
+// draft tokens equal to the target argmax of the row before them, next =
+// argmax of row a.  It then resets the arrival counter.
+__global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
+  const int r = blockIdx.x;
+  const float* pv = a.part_val + (size_t)r * a.n_part;
+  const int32_t* pi = a.part_idx + (size_t)r * a.n_part;
+  float best = -INFINITY;
+  int bidx = 0x7fffffff;
+  for (int j = threadIdx.x; j < a.n_part; j += 256) {
+    const float v = pv[j];
+    const int id = pi[j];
+    if (v > best || (v == best && id < bidx)) { best = v; bidx = id; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(best, o);
+    const int oi = __shfl_xor(bidx, o);
+    if (ov > best || (ov == best && oi < bidx)) { best = ov; bidx = oi; }
+  }
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  __shared__ bool last;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) { sv[wave] = best; si[wave] = bidx; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (sv[w] > best || (sv[w] == best && si[w] < bidx)) { best = sv[w]; bidx = si[w]; }
+    a.g[r] = bidx;
+    __threadfence();
+    const unsigned prev = atomicAdd(a.counter, 1u);
+    last = (prev == (unsigned)a.M - 1);
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  for (int b = threadIdx.x; b < a.B; b += 256) {
+    const SeqMeta sq = a.seqs[b];
+    int acc = 0;
+    while (acc < sq.k) {
+      const int drafted = a.rows[sq.cu + acc + 1].tok;  // draft token acc
+      const int target = __atomic_load_n(&a.g[sq.cu + acc], __ATOMIC_RELAXED);
+      if (drafted != target) break;
+      ++acc;
+    }
+    a.out[2 * b] = acc;
+    a.out[2 * b + 1] = __atomic_load_n(&a.g[sq.cu + acc], __ATOMIC_RELAXED);
+  }
+  if (threadIdx.x == 0) *a.counter = 0u;
+}
+
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(argmax_accept, dim3(a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace hvd

@@ -1,0 +1,225 @@
+"""ctypes binding of libhvd (include/hvd.h): argument marshalling only.
+
+Every step of the verify path runs in the library's HIP kernels.  PyTorch
+supplies device memory (borrowed buffers) and the HIP stream.  If the built
+library is missing, loading fails loudly; there is no fallback.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhvd.so")
+
+HVD_OK, HVD_ERR_ARG, HVD_ERR_STATE, HVD_ERR_OOM, HVD_ERR_RANGE, HVD_ERR_DEVICE = 0, -1, -2, -3, -4, -5
+_STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM", -4: "HVD_ERR_RANGE",
+           -5: "HVD_ERR_DEVICE"}
+
+EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
+           "hvd_prefill", "hvd_verify", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
+           "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_last_error")
+
+
+LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
+
+
+def tensor_names(n_layers: int):
+    """Canonical order of the tensors hvd_model_load takes (include/hvd.h)."""
+    return (["embed"] + [f"layers.{l}.{n}" for l in range(n_layers) for n in LAYER_TENSORS]
+            + ["final_norm", "lm_head"])
+
+
+class HvdError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("max_draft", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("max_pos", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+
+    @classmethod
+    def from_model_config(cls, c):
+        return cls(c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
+                   c.max_draft, c.page_size, c.max_pos, c.rope_theta, c.rms_eps)
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libhvd.so (built by paper_2606_01019_amd.build); raises if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libhvd.so not built at {path}: run `python -m paper_2606_01019_amd.build`")
+    L = ctypes.CDLL(path)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    PI32 = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "hvd_model_bytes": (SZ, [ctypes.POINTER(Config)]),
+        "hvd_model_load": (I32, [ctypes.POINTER(Config), ctypes.POINTER(P), P, SZ, P, ctypes.POINTER(P)]),
+        "hvd_model_free": (None, [P]),
+        "hvd_kv_bytes": (SZ, [ctypes.POINTER(Config), I32, I32]),
+        "hvd_kv_alloc": (I32, [P, I32, I32, P, SZ, P, ctypes.POINTER(P)]),
+        "hvd_kv_free": (None, [P]),
+        "hvd_prefill": (I32, [P, P, I32, PI32, I32]),
+        "hvd_verify": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
+        "hvd_commit": (I32, [P, P, I32, PI32, PI32]),
+        "hvd_truncate": (I32, [P, I32, I32, I32]),
+        "hvd_seq_free": (I32, [P, I32]),
+        "hvd_seq_info": (I32, [P, I32, PI32, PI32, PI32]),
+        "hvd_kv_free_pages": (I32, [P]),
+        "hvd_profile_enable": (I32, [P, I32]),
+        "hvd_profile_read": (I32, [P, I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
+                                   ctypes.POINTER(ctypes.c_double)]),
+        "hvd_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status):
+    if status != HVD_OK:
+        raise HvdError(status, load_library().hvd_last_error().decode())
+
+
+def _i32(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if a is not None and a.size else None
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Model:
+    """Target model on the GPU.  ``tensors`` maps canonical names (see
+    workloads.weights) to uint16 bf16 arrays, or is a list in canonical order."""
+
+    def __init__(self, cfg, tensors, names=None, stream=None):
+        import torch
+        self.lib = load_library()
+        self.cfg = cfg
+        self.ccfg = Config.from_model_config(cfg)
+        if isinstance(tensors, dict):
+            arrs = [np.ascontiguousarray(tensors[n], dtype=np.uint16) for n in tensor_names(cfg.n_layers)]
+        else:
+            arrs = [np.ascontiguousarray(t, dtype=np.uint16) for t in tensors]
+        ptrs = (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
+        nbytes = self.lib.hvd_model_bytes(ctypes.byref(self.ccfg))
+        if nbytes == 0:
+            raise HvdError(HVD_ERR_ARG, "unsupported config")
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        self.stream = stream
+        h = ctypes.c_void_p()
+        _check(self.lib.hvd_model_load(ctypes.byref(self.ccfg), ptrs, ctypes.c_void_p(self.buf.data_ptr()),
+                                       nbytes, _stream(stream), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.hvd_model_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class KVCache:
+    """Paged KV cache plus per-step workspace bound to one Model."""
+
+    def __init__(self, model: Model, max_seqs: int, n_pages: int, stream=None):
+        import torch
+        self.lib = model.lib
+        self.model = model
+        nbytes = self.lib.hvd_kv_bytes(ctypes.byref(model.ccfg), max_seqs, n_pages)
+        if nbytes == 0:
+            raise HvdError(HVD_ERR_ARG, "bad max_seqs / n_pages")
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        h = ctypes.c_void_p()
+        _check(self.lib.hvd_kv_alloc(model.handle, max_seqs, n_pages, ctypes.c_void_p(self.buf.data_ptr()), nbytes,
+                                     _stream(stream), ctypes.byref(h)))
+        self.handle = h
+        self.max_seqs = max_seqs
+
+    # -- calls of the C ABI
+    def prefill(self, seq_id: int, tokens):
+        t = _i32(tokens)
+        _check(self.lib.hvd_prefill(self.model.handle, self.handle, seq_id, _ptr(t), t.size))
+
+    def verify(self, seq_ids, ctx_lens, drafts, logits=None):
+        """drafts: list of 1-D token arrays.  logits: optional torch float32
+        CUDA tensor [sum(k+1), vocab].  Returns (accepted, next_token)."""
+        ids = _i32(seq_ids)
+        ctx = _i32(ctx_lens)
+        lens = _i32([len(d) for d in drafts])
+        flat = _i32(np.concatenate([np.asarray(d, dtype=np.int64).reshape(-1) for d in drafts])
+                    if len(drafts) else np.zeros(0))
+        acc = np.zeros(ids.size, dtype=np.int32)
+        nxt = np.zeros(ids.size, dtype=np.int32)
+        lp = None
+        if logits is not None:
+            rows = int(lens.sum()) + ids.size
+            assert logits.is_cuda and logits.dtype.is_floating_point and logits.element_size() == 4
+            assert logits.is_contiguous() and logits.numel() >= rows * self.model.cfg.vocab
+            lp = ctypes.c_void_p(logits.data_ptr())
+        _check(self.lib.hvd_verify(self.model.handle, self.handle, ids.size, _ptr(ids), _ptr(ctx), _ptr(flat),
+                                   _ptr(lens), _ptr(acc), _ptr(nxt), lp))
+        return acc, nxt
+
+    def commit(self, seq_ids, keep=None):
+        ids = _i32(seq_ids)
+        kp = _i32(keep) if keep is not None else None
+        _check(self.lib.hvd_commit(self.model.handle, self.handle, ids.size, _ptr(ids), _ptr(kp)))
+
+    def truncate(self, seq_id, new_ctx, pending):
+        _check(self.lib.hvd_truncate(self.handle, seq_id, new_ctx, pending))
+
+    def seq_free(self, seq_id):
+        _check(self.lib.hvd_seq_free(self.handle, seq_id))
+
+    def seq_info(self, seq_id):
+        a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(self.lib.hvd_seq_info(self.handle, seq_id, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
+        return a.value, b.value, bool(c.value)
+
+    def free_pages(self):
+        return self.lib.hvd_kv_free_pages(self.handle)
+
+    def profile_enable(self, on=True):
+        _check(self.lib.hvd_profile_enable(self.handle, 1 if on else 0))
+
+    def profile_read(self, family):
+        ms, n, b = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
+        _check(self.lib.hvd_profile_read(self.handle, family, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b)))
+        return ms.value, n.value, b.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.hvd_kv_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
