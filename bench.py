@@ -1,0 +1,222 @@
+"""Verify-step benchmark on one MI355X.
+
+Workload (default): Llama-3-8B-shaped random-init bf16 decoder (32 layers,
+d_model 4096, 32 q / 8 kv heads of 128, SwiGLU 14336, vocab 128256, rotary
+theta 5e5), batch 1, context 2048 Zipf(1.1) tokens, chain drafts whose length
+cycles through k = 1, 2, 4, 8, 16 with planted acceptance min(G, k),
+G ~ Geometric(p = 0.3).  A step is one hvd_verify + hvd_commit (the whole
+hot path: embed, 32 layers, LM head, argmax + accept, commit).  Drafts are
+planted from the model's own greedy continuation, computed before the timed
+region.
+
+Prints one JSON line: committed tokens/s (value), ms per step, latency per
+k, the roofline of the dominant kernel (the weight-streaming GEMM, timed with
+HIP events around every launch in a second pass of the same steps) and the
+CPU oracle timed on a bounded sample of the same step.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+K_CYCLE = (1, 2, 4, 8, 16)
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(cfg, ctx, k):
+    """bf16 weights of every layer + LM head, fp16 K/V of the attended keys."""
+    D, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
+    qd, kd = cfg.q_dim, cfg.kv_dim
+    layer = D * (qd + 2 * kd) + qd * D + 3 * D * F
+    weights = 2.0 * (cfg.n_layers * layer + V * D)
+    kv = 2.0 * 2 * kd * cfg.n_layers * (ctx + k + 1)
+    return weights + kv
+
+
+def plan_steps(n, seed_key):
+    from workloads import tokens as wt
+    rng = wt.rng_for("accept", *seed_key)
+    ks = [K_CYCLE[i % len(K_CYCLE)] for i in range(n)]
+    return ks, [wt.geometric_accept(rng, 0.3, k) for k in ks]
+
+
+def cpu_baseline(cfg, ctx_len, committed_per_step, mean_k):
+    """Time the CPU oracle on a bounded sample of the same step: one verify of
+    k = 8 at full width over a ctx_len-token cache, with 1 and with 2 decoder
+    layers; the per-layer cost is scaled to the full depth."""
+    import oracle
+    from oracle.model import SeqState
+    from workloads import make_weights, tokens as wt
+    threads = len(os.sched_getaffinity(0))
+    times = {}
+    rng = np.random.default_rng(0)
+    for L in (1, 2):
+        c = cfg.with_layers(L)
+        w = make_weights(c, seed=42)
+        om = oracle.OracleModel(c, w, cache=False)
+        toks = list(wt.zipf_context(wt.rng_for("context", 2), ctx_len + 1, c.vocab))
+        K = [rng.standard_normal((ctx_len, c.n_kv_heads, c.head_dim)) for _ in range(L)]
+        V = [rng.standard_normal((ctx_len, c.n_kv_heads, c.head_dim)) for _ in range(L)]
+        st = SeqState(tokens=toks, K=K, V=V)
+        d = wt.random_chain(rng, 8, c.vocab)
+        oracle.verify(om, st, d)  # warm
+        t0 = time.perf_counter()
+        oracle.verify(om, st, d)
+        times[L] = time.perf_counter() - t0
+        del w, om, K, V
+    per_layer = max(times[2] - times[1], 1e-9)
+    fixed = max(times[1] - per_layer, 0.0)
+    step_s = fixed + per_layer * cfg.n_layers
+    return {
+        "value": committed_per_step / step_s,
+        "unit": "committed tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"float64 numpy oracle, one k=8 verify over a {ctx_len}-token cache at full width with 1 and "
+                   f"2 decoder layers ({times[1]:.2f}s, {times[2]:.2f}s); per-layer cost scaled to "
+                   f"{cfg.n_layers} layers -> {step_s:.2f}s per step; committed tokens per step taken "
+                   f"from the GPU run ({committed_per_step:.2f})"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--ctx", type=int, default=2048)
+    ap.add_argument("--layers", type=int, default=0, help="override depth (0 = full 32)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the verify step of one "
+              f"sequence batch does not shard across GPUs in this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_01019_amd as hvd
+    from workloads import SHAPE_8B, make_weights, tokens as wt
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = SHAPE_8B if not args.layers else SHAPE_8B.with_layers(args.layers)
+    t0 = time.time()
+    w = make_weights(cfg, seed=42)
+    log(f"weights drawn in {time.time() - t0:.1f}s")
+    t0 = time.time()
+    model = hvd.Model(cfg, w)
+    del w
+    log(f"model loaded in {time.time() - t0:.1f}s")
+    n_total = args.warmup + args.steps
+    ks, planned = plan_steps(n_total, (2, 0))
+    ctx_tokens = wt.zipf_context(wt.rng_for("context", 2), args.ctx, cfg.vocab)
+    max_ctx = args.ctx + sum(planned) + n_total + max(K_CYCLE) + 16
+    kv = hvd.KVCache(model, max_seqs=1, n_pages=max_ctx // 16 + 8)
+    t0 = time.time()
+    kv.prefill(0, ctx_tokens)
+    c0, p0, _ = kv.seq_info(0)
+    log(f"prefill {args.ctx} tokens in {time.time() - t0:.2f}s")
+
+    # greedy continuation from the initial state (k = 0 steps), then roll back
+    need = sum(a + 1 for a in planned) + max(K_CYCLE) + 1
+    greedy = []
+    t0 = time.time()
+    while len(greedy) < need:
+        c, _, _ = kv.seq_info(0)
+        a, n = kv.verify([0], [c], [np.zeros(0, np.int32)])
+        kv.commit([0])
+        greedy.append(int(n[0]))
+    kv.truncate(0, c0, p0)
+    log(f"greedy continuation of {len(greedy)} tokens in {time.time() - t0:.2f}s")
+
+    drng = wt.rng_for("draft", 2)
+    drafts, pos = [], 0
+    for k, a in zip(ks, planned):
+        drafts.append(wt.plant_chain(drng, greedy[pos:], a, k, cfg.vocab))
+        pos += a + 1
+
+    def run(steps_slice, lat=None):
+        acc = []
+        for i in steps_slice:
+            c, _, _ = kv.seq_info(0)
+            t = time.perf_counter()
+            a, n = kv.verify([0], [c], [drafts[i]])
+            kv.commit([0])
+            if lat is not None:
+                lat.setdefault(ks[i], []).append(time.perf_counter() - t)
+            acc.append(int(a[0]))
+        return acc
+
+    run(range(args.warmup))
+    lat = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    acc = run(range(args.warmup, n_total), lat)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    committed = sum(a + 1 for a in acc)
+    mismatched = sum(1 for a, p in zip(acc, planned[args.warmup:]) if a != p)
+
+    # second pass over the same steps with HIP events around every launch
+    kv.truncate(0, c0, p0)
+    run(range(args.warmup))
+    kv.profile_enable(True)
+    run(range(args.warmup, n_total))
+    g_ms, g_n, g_bytes = kv.profile_read(0)
+    a_ms, a_n, a_bytes = kv.profile_read(1)
+    o_ms, o_n, _ = kv.profile_read(2)
+    kv.profile_enable(False)
+    achieved = g_bytes / (g_ms * 1e-3) / 1e9
+    step_bytes = np.mean([algorithmic_bytes(cfg, args.ctx + 0, ks[i]) for i in range(args.warmup, n_total)])
+    ms_step = elapsed / args.steps * 1e3
+
+    out = {
+        "metric": "committed tokens/s (verify-step latency vs draft length k; % HBM roofline)",
+        "value": committed / elapsed,
+        "unit": "committed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": (f"8B-shaped random-init decoder ({cfg.n_layers} layers), batch 1, context "
+                                f"{args.ctx} Zipf(1.1) tokens, chain drafts k in {list(K_CYCLE)} planted "
+                                f"geometric(p=0.3) acceptance"),
+                   "global_batch": 1, "seq_len": args.ctx, "parallelism": "none"},
+        "latency_us_by_k": {str(k): float(np.median(v) * 1e6) for k, v in sorted(lat.items())},
+        "mean_accepted": float(np.mean(acc)),
+        "accept_mismatch_vs_plant": mismatched,
+        "step_roofline": {"bound": "hbm", "algorithmic_bytes_per_step": step_bytes,
+                          "achieved_GBs": step_bytes / (ms_step * 1e-3) / 1e9,
+                          "frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        "roofline": {"bound": "hbm", "kernel": "gemm_skinny (weight-streaming GEMMs)", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "avg_launch_us": g_ms * 1e3 / max(g_n, 1), "launches": g_n,
+                     "bytes_per_launch": g_bytes / max(g_n, 1)},
+        "kernel_time_share": {"gemm_ms_per_step": g_ms / args.steps, "attn_ms_per_step": a_ms / args.steps,
+                              "attn_GBs": a_bytes / max(a_ms * 1e-3, 1e-12) / 1e9,
+                              "other_ms_per_step": o_ms / args.steps},
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        out["cpu_baseline"] = cpu_baseline(SHAPE_8B, args.ctx, committed / args.steps, np.mean(ks))
+        log(f"cpu baseline in {time.time() - t0:.1f}s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -53,7 +53,7 @@ typedef enum {
 } hvd_status;
 
 /* Model shape.  Requirements (HVD_ERR_ARG otherwise): d_model % 64 == 0,
- * ffn_dim % 32 == 0, vocab % 32 == 0, head_dim in {64, 128},
+ * ffn_dim % 32 == 0, vocab % 64 == 0, head_dim in {64, 128},
  * n_q_heads % n_kv_heads == 0, page_size == 16, 0 <= max_draft <= 64,
  * max_pos >= 32. */
 typedef struct {

@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <string>
@@ -32,7 +33,10 @@ hvd_status set_err(hvd_status s, const std::string& m) {
 
 constexpr size_t kAlign = 256;
 constexpr int kPrefillRows = 128;  // rows per prefill chunk
-constexpr int kMaxMTile = 8;       // 16-row tiles one GEMM workgroup covers
+constexpr int kGemmMinBlocks = 256;          // GEMM workgroups wanted per launch (one per CU)
+constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
+constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
+constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
 constexpr int kAttnRows = 128;     // query rows per attention work item
 constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items)
 
@@ -57,7 +61,7 @@ hvd_status check_config(const hvd_config* c) {
   if (c->head_dim != 64 && c->head_dim != 128) return set_err(HVD_ERR_ARG, "head_dim must be 64 or 128");
   if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads) return set_err(HVD_ERR_ARG, "n_q_heads must be a multiple of n_kv_heads");
   if (c->ffn_dim < 32 || c->ffn_dim % 32) return set_err(HVD_ERR_ARG, "ffn_dim must be a positive multiple of 32");
-  if (c->vocab < 32 || c->vocab % 32) return set_err(HVD_ERR_ARG, "vocab must be a positive multiple of 32");
+  if (c->vocab < 64 || c->vocab % 64) return set_err(HVD_ERR_ARG, "vocab must be a positive multiple of 64");
   if (c->page_size != kPage) return set_err(HVD_ERR_ARG, "page_size must be 16");
   if (c->max_draft < 0 || c->max_draft > 64) return set_err(HVD_ERR_ARG, "max_draft must be in [0, 64]");
   if (c->max_pos < 32) return set_err(HVD_ERR_ARG, "max_pos must be >= 32");
@@ -295,6 +299,9 @@ struct hvd_kv_s {
   float* lm_val = nullptr;
   int32_t* lm_idx = nullptr;
   int n_part_lm = 0;
+  int gemm_min_blocks = kGemmMinBlocks;
+  int attn_min_items = kAttnMinItems;
+  float* gemm_part = nullptr;
   int32_t* g = nullptr;
   int32_t* out = nullptr;
   uint32_t* counter = nullptr;
@@ -321,7 +328,7 @@ size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int p
   const size_t rg_verify = ((size_t)(c.max_draft + 1) * G + kAttnRows - 1) / kAttnRows;
   const size_t rg_prefill = ((size_t)kPrefillRows * G + kAttnRows - 1) / kAttnRows;
   const size_t units = std::max((size_t)max_seqs * rg_verify, rg_prefill) * c.n_kv_heads;
-  return 4 * (size_t)max_rows + 4 * (size_t)max_seqs + 8 * (2 * units + kPartSlots) +
+  return 4 * (size_t)max_rows + 4 * (size_t)max_seqs + 16 * (2 * units + kPartSlots) +
          3 * (size_t)max_seqs * pt_stride + 64;
 }
 
@@ -345,9 +352,10 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->Olo = cv.take<uint16_t>(Mp * qd);
   k->Ahi = cv.take<uint16_t>(Mp * F);
   k->Alo = cv.take<uint16_t>(Mp * F);
-  k->n_part_lm = c.vocab / 16 / gemm_strips_per_block(EPI_LM);
+  k->n_part_lm = c.vocab / 16;  // LM-head partials per row (upper bound: one per strip)
   k->lm_val = cv.take<float>(Mp * k->n_part_lm);
   k->lm_idx = cv.take<int32_t>(Mp * k->n_part_lm);
+  k->gemm_part = cv.take<float>(kGemmPartBytes / 4);
   k->g = cv.take<int32_t>(Mp);
   k->out = cv.take<int32_t>(2 * (size_t)max_seqs);
   k->counter = cv.take<uint32_t>(64);
@@ -407,6 +415,12 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
     return set_err(HVD_ERR_DEVICE, "workspace clear failed");
   }
   k->hs = new HostState(max_seqs, n_pages, kPage, c.max_pos, c.max_draft, c.vocab);
+  if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
+  if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
+  if (hipError_t e = attn_set_lds_limit(); e != hipSuccess) {
+    hvd_kv_free(k);
+    return set_err(HVD_ERR_DEVICE, std::string("attention LDS limit: ") + hipGetErrorString(e));
+  }
   *out = k;
   return HVD_OK;
 }
@@ -480,9 +494,18 @@ struct Plan {
 
 // Split every (sequence, kv head, row group) into KV chunks of `chunk`
 // positions, chosen so the launch has enough workgroups to fill the GPU.
-bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, Plan& p) {
+bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, int min_items, Plan& p) {
   const int G = c.n_q_heads / c.n_kv_heads;
   struct Unit { int b, g, rg, keys; };
+  auto item = [&](const Unit& u, int c, int nch, int part, int chunk) {
+    const SeqMeta& s = seqs[u.b];
+    AttnItem it{};
+    it.slot = s.slot; it.ctx = s.ctx; it.k = s.k; it.cu = s.cu;
+    it.g = u.g; it.c = c; it.nch = nch; it.rg = u.rg; it.part = part;
+    it.p_begin = c * chunk;
+    it.p_end = std::min(s.ctx + s.k + 1, (c + 1) * chunk);
+    return it;
+  };
   std::vector<Unit> units;
   int64_t total_keys = 0;
   for (int b = 0; b < (int)seqs.size(); ++b) {
@@ -497,7 +520,10 @@ bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, Plan&
         total_keys += keys;
       }
   }
-  int chunk = (int)std::min<int64_t>(1 << 20, std::max<int64_t>(64, ((total_keys / 512) + 31) / 32 * 32));
+  // smallest chunk (multiple of 32, <= kAttnChunk) that still yields about
+  // min_items workgroups; longer chunks mean fewer partials to combine
+  int chunk = (int)((total_keys + min_items - 1) / min_items);
+  chunk = std::max(32, std::min(kAttnChunk, (chunk + 31) / 32 * 32));
   for (;;) {
     p.items.clear();
     p.heads.clear();
@@ -505,15 +531,17 @@ bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, Plan&
     for (const Unit& u : units) {
       const int nch = (u.keys + chunk - 1) / chunk;
       if (nch == 1) {
-        p.items.push_back({u.b, u.g, 0, 1, u.rg, -1, 0, 0});
+        p.items.push_back(item(u, 0, 1, -1, chunk));
       } else {
-        p.heads.push_back({u.b, u.g, 0, nch, u.rg, slots, 0, 0});
-        for (int ci = 0; ci < nch; ++ci) p.items.push_back({u.b, u.g, ci, nch, u.rg, slots + ci, 0, 0});
+        p.heads.push_back(item(u, 0, nch, slots, chunk));
+        for (int ci = 0; ci < nch; ++ci) p.items.push_back(item(u, ci, nch, slots + ci, chunk));
         slots += nch;
       }
     }
-    if (slots <= kPartSlots && (int)p.items.size() <= 65535 * 4) break;
-    chunk *= 2;
+    if (slots <= kPartSlots) break;
+    if (chunk >= (1 << 20)) return false;
+    // longer chunks: multiples of kAttnChunk above it (looped in LDS-sized pieces)
+    chunk = chunk < kAttnChunk ? std::min(kAttnChunk, chunk * 2) : chunk * 2;
   }
   p.chunk = chunk;
   return true;
@@ -532,7 +560,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   const int G = c.n_q_heads / c.n_kv_heads;
 
   Plan plan;
-  plan_attention(c, seqs, plan);
+  if (!plan_attention(c, seqs, k->attn_min_items, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
   std::vector<PageUpdate> upd_raw = k->hs->take_updates();
   // keep the last update of each (slot, index): they are applied in parallel
   std::map<std::pair<int, int>, int> last;
@@ -547,7 +575,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     off += (ints + 3) / 4 * 4;
     return o;
   };
-  const size_t need_ints = 4 * (size_t)M + 4 * (size_t)B + 8 * (plan.items.size() + plan.heads.size()) +
+  const size_t need_ints = 4 * (size_t)M + 4 * (size_t)B + 16 * (plan.items.size() + plan.heads.size()) +
                            3 * last.size() + 32;
   if (need_ints > k->meta_ints) {
     k->hs->take_updates();
@@ -555,8 +583,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   }
   const size_t o_rows = put(rows.data(), 4 * (size_t)M);
   const size_t o_seqs = put(seqs.data(), 4 * (size_t)B);
-  const size_t o_items = put(plan.items.data(), 8 * plan.items.size());
-  const size_t o_heads = put(plan.heads.data(), 8 * plan.heads.size());
+  const size_t o_items = put(plan.items.data(), 16 * plan.items.size());
+  const size_t o_heads = put(plan.heads.data(), 16 * plan.heads.size());
   std::vector<int32_t> upd;
   for (auto& kv : last) {
     upd.push_back(kv.first.first);
@@ -591,15 +619,37 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     HIP_TRY(launch_embed(e, s));
   }
 
-  const int mt_block = std::min(MT, kMaxMTile);
+  const int mt_block = std::min(MT, kGemmMaxMT);
   const int mblocks = (MT + mt_block - 1) / mt_block;
+  // Workgroup shape per GEMM: 64-column blocks (each activation fragment
+  // feeds 4 weight fragments) when there are enough of them; otherwise a K
+  // split across workgroups for long-K GEMMs (partial tiles + a finish pass),
+  // else 16-column blocks (more workgroups, more activation re-reads).
+  int lm_parts = 0;
   auto gemm = [&](int epi, GemmArgs& a, int N, int K) -> hvd_status {
     a.KT = K / 32;
     a.NT = N / 16;
     a.MTtot = MT;
     a.M = M;
+    a.part = k->gemm_part;
+    int ns = 4, splits = 1;
+    const int nb4 = N / 64 * mblocks;
+    if (nb4 < k->gemm_min_blocks) {
+      if (a.KT >= kGemmLongK) {
+        splits = std::min((k->gemm_min_blocks + nb4 - 1) / nb4, a.KT / 64);
+        while (splits > 1 && (size_t)nb4 * splits * mt_block * 16 * 64 * 4 > kGemmPartBytes) --splits;
+      } else if (epi != EPI_SILU) {
+        ns = (N / 32 * mblocks >= k->gemm_min_blocks) ? 2 : 1;
+      } else {
+        ns = 2;
+      }
+    }
+    if (epi == EPI_LM) {
+      lm_parts = a.NT / ns;
+      a.n_part = lm_parts;
+    }
     ProfScope ps(k, 0, (double)N * K * 2.0);
-    HIP_TRY(launch_gemm(epi, a, mblocks, mt_block, s));
+    HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, s));
     return HVD_OK;
   };
   double kv_bytes = 0;
@@ -641,9 +691,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.group = G;
       a.pt = k->pt;
       a.pt_stride = k->pt_stride;
-      a.seqs = d_seqs;
       a.items = d_items;
-      a.chunk = plan.chunk;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
       a.Ohi = k->Ohi;
       a.Olo = k->Olo;
@@ -656,7 +704,6 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       }
       if (!plan.heads.empty()) {
         CombineArgs cb{};
-        cb.seqs = d_seqs;
         cb.heads = d_heads;
         cb.Hq = c.n_q_heads;
         cb.Hkv = c.n_kv_heads;
@@ -724,12 +771,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     a.vocab = c.vocab;
     a.part_val = k->lm_val;
     a.part_idx = k->lm_idx;
-    a.n_part = k->n_part_lm;
     if (hvd_status st = gemm(EPI_LM, a, c.vocab, D); st != HVD_OK) return st;
     AcceptArgs ac{};
     ac.part_val = k->lm_val;
     ac.part_idx = k->lm_idx;
-    ac.n_part = k->n_part_lm;
+    ac.n_part = lm_parts;
     ac.M = M;
     ac.g = k->g;
     ac.seqs = d_seqs;

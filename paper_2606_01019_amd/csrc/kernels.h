@@ -6,7 +6,8 @@
 
 namespace hvd {
 
-constexpr int kPage = 16;  // tokens per KV page
+constexpr int kPage = 16;        // tokens per KV page
+constexpr int kAttnChunk = 256;  // most KV positions one attention workgroup stages in LDS
 
 // Row metadata of one forward: token, sequence slot, absolute position.
 struct RowMeta {
@@ -17,17 +18,22 @@ struct RowMeta {
 struct SeqMeta {
   int32_t slot, ctx, k, cu;
 };
-// One attention work item: sequence entry b, kv head g, KV chunk c of nch,
-// the row group rg (rows [rg*128, rg*128+128) of the (k+1)*group rows) and,
-// for multi-chunk items, the partial slot `part`.
+// One attention work item, self-contained so a workgroup needs one scalar
+// load: sequence slot, cached length ctx, draft length k, first row cu; kv
+// head g; KV chunk c of nch covering positions [p_begin, p_end); the row
+// group rg (rows [rg*128, rg*128+128) of the (k+1)*group query rows); and,
+// for multi-chunk items, the partial slot `part` (combine heads: first slot).
 struct AttnItem {
-  int32_t b, g, c, nch, rg, part, pad0, pad1;
+  int32_t slot, ctx, k, cu;
+  int32_t g, c, nch, rg;
+  int32_t part, p_begin, p_end, pad0;
+  int32_t pad1, pad2, pad3, pad4;
 };
 
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_LM = 3 };
 
 struct GemmArgs {
-  const uint4* W;    // packed weights, fragment (nt, kt) at (nt*KT + kt)*64 lanes
+  const uint4* W;    // packed weights: strip s, K step kt at ((s/4*KT + kt)*4 + s%4)*64 lanes
   const uint4* Ahi;  // packed activations (hi part), fragment (kt, mt) at (kt*MTtot + mt)*64
   const uint4* Alo;  // packed activations (lo part)
   int KT, NT, MTtot, M;
@@ -60,6 +66,8 @@ struct GemmArgs {
   float* part_val;     // [M][n_part]
   int32_t* part_idx;
   int n_part;
+  // K split across workgroups: partial tiles [mblocks][NT/ns][splits][64*4*... rows][cols]
+  float* part;
 };
 
 struct AttnArgs {
@@ -69,9 +77,7 @@ struct AttnArgs {
   int Hq, Hkv, dh, group;
   const int32_t* pt;
   int pt_stride;
-  const SeqMeta* seqs;
   const AttnItem* items;
-  int chunk;           // positions per KV chunk (multiple of 32)
   float scale_log2;    // log2(e) / sqrt(dh)
   uint16_t* Ohi;       // O GEMM A operand (K = Hq*dh)
   uint16_t* Olo;
@@ -81,7 +87,6 @@ struct AttnArgs {
 };
 
 struct CombineArgs {
-  const SeqMeta* seqs;
   const AttnItem* heads;  // one entry per (b, g, rg) whose nch > 1; part = first slot
   int Hq, Hkv, dh, group;
   const float* part_o;
@@ -125,12 +130,14 @@ struct AcceptArgs {
 hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst, int N, int K,
                        hipStream_t s);
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
-hipError_t launch_gemm(int epi, const GemmArgs& a, int mblocks, int mt_block, hipStream_t s);
+// ns: 16-column strips per workgroup (1, 2, 4; >= 2 for EPI_SILU); grid.x = NT / ns.
+// splits > 1 splits K across workgroups and adds the gemm_finish pass.
+hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int n_items, hipStream_t s);
+hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
-// Strips (16 output columns) handled by one GEMM workgroup for an epilogue.
-int gemm_strips_per_block(int epi);
+constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
 
 }  // namespace hvd

@@ -6,16 +6,21 @@
 
 namespace hvd {
 
-// dst fragment (s, kt), lane l, half j = src[rowmap[16 s + l%16]][32 kt + 8 (l/16) + j]
+// dst fragment (strip s, K step kt), lane l, half j =
+//   src[rowmap[16 s + l%16]][32 kt + 8 (l/16) + j]
+// stored at ((s/4 * KT + kt) * 4 + s%4) * 512 halves: the 4 strips of a
+// 64-column block are contiguous for each K step.
 __global__ void pack_weight(const uint16_t* __restrict__ src, const int32_t* __restrict__ rowmap,
                             uint16_t* __restrict__ dst, int N, int K) {
   const int KT = K >> 5;
   const size_t total = (size_t)(N >> 4) * KT * 64;
   for (size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (size_t)gridDim.x * blockDim.x) {
     const int l = (int)(t & 63);
-    const size_t frag = t >> 6;
-    const int kt = (int)(frag % KT);
-    const int s = (int)(frag / KT);
+    const size_t frag = t >> 6;           // in destination order
+    const int ns = (int)(frag & 3);
+    const int kt = (int)((frag >> 2) % KT);
+    const int cb = (int)((frag >> 2) / KT);
+    const int s = cb * 4 + ns;
     const int srow = rowmap[s * 16 + (l & 15)];
     const uint4 v = *(const uint4*)(src + (size_t)srow * K + kt * 32 + (l >> 4) * 8);
     *(uint4*)(dst + t * 8) = v;

@@ -155,9 +155,13 @@ class KVCache:
         if nbytes == 0:
             raise HvdError(HVD_ERR_ARG, "bad max_seqs / n_pages")
         self.buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        torch.cuda.current_stream().synchronize()  # buffer allocated before the library's stream uses it
+        # The library's work runs on its own (default-priority) stream: the
+        # null stream adds cross-stream synchronization to every launch.
+        self.stream = stream if stream is not None else torch.cuda.Stream()
         h = ctypes.c_void_p()
         _check(self.lib.hvd_kv_alloc(model.handle, max_seqs, n_pages, ctypes.c_void_p(self.buf.data_ptr()), nbytes,
-                                     _stream(stream), ctypes.byref(h)))
+                                     _stream(self.stream), ctypes.byref(h)))
         self.handle = h
         self.max_seqs = max_seqs
 
