@@ -33,7 +33,8 @@ hvd_status set_err(hvd_status s, const std::string& m) {
 
 constexpr size_t kAlign = 256;
 constexpr int kPrefillRows = 128;  // rows per prefill chunk
-constexpr int kGemmMinBlocks = 256;          // GEMM workgroups wanted per launch (one per CU)
+constexpr int kGemmMinBlocks = 192;          // GEMM workgroups below which the shape changes
+constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (one per CU)
 constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
 constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
@@ -345,13 +346,16 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   const size_t Mp = (size_t)k->MTmax * 16;
   k->X = cv.take<float>(Mp * D);
   k->ss = cv.take<float>(Mp * (D / 16));
-  k->Nhi = cv.take<uint16_t>(Mp * D);
-  k->Nlo = cv.take<uint16_t>(Mp * D);
+  // GEMM operands carry kGemmMaxMT extra fragments: a workgroup always reads
+  // a full block of row tiles and drops the rows past the last tile
+  const size_t pad = (size_t)kGemmMaxMT * 512;
+  k->Nhi = cv.take<uint16_t>(Mp * D + pad);
+  k->Nlo = cv.take<uint16_t>(Mp * D + pad);
   k->Q = cv.take<_Float16>(Mp * qd);
-  k->Ohi = cv.take<uint16_t>(Mp * qd);
-  k->Olo = cv.take<uint16_t>(Mp * qd);
-  k->Ahi = cv.take<uint16_t>(Mp * F);
-  k->Alo = cv.take<uint16_t>(Mp * F);
+  k->Ohi = cv.take<uint16_t>(Mp * qd + pad);
+  k->Olo = cv.take<uint16_t>(Mp * qd + pad);
+  k->Ahi = cv.take<uint16_t>(Mp * F + pad);
+  k->Alo = cv.take<uint16_t>(Mp * F + pad);
   k->n_part_lm = c.vocab / 16;  // LM-head partials per row (upper bound: one per strip)
   k->lm_val = cv.take<float>(Mp * k->n_part_lm);
   k->lm_idx = cv.take<int32_t>(Mp * k->n_part_lm);
@@ -621,10 +625,9 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
 
   const int mt_block = std::min(MT, kGemmMaxMT);
   const int mblocks = (MT + mt_block - 1) / mt_block;
-  // Workgroup shape per GEMM: 64-column blocks (each activation fragment
-  // feeds 4 weight fragments) when there are enough of them; otherwise a K
-  // split across workgroups for long-K GEMMs (partial tiles + a finish pass),
-  // else 16-column blocks (more workgroups, more activation re-reads).
+  // Workgroup shape per GEMM (measured on the 8B verify shapes): 4 strips
+  // per workgroup when that alone gives enough workgroups; for long-K GEMMs
+  // 4 strips plus a K split; otherwise 2 strips, K-split if still too few.
   int lm_parts = 0;
   auto gemm = [&](int epi, GemmArgs& a, int N, int K) -> hvd_status {
     a.KT = K / 32;
@@ -632,18 +635,21 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     a.MTtot = MT;
     a.M = M;
     a.part = k->gemm_part;
+    const int want = k->gemm_min_blocks;
+    const int nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
     int ns = 4, splits = 1;
-    const int nb4 = N / 64 * mblocks;
-    if (nb4 < k->gemm_min_blocks) {
-      if (a.KT >= kGemmLongK) {
-        splits = std::min((k->gemm_min_blocks + nb4 - 1) / nb4, a.KT / 64);
-        while (splits > 1 && (size_t)nb4 * splits * mt_block * 16 * 64 * 4 > kGemmPartBytes) --splits;
-      } else if (epi != EPI_SILU) {
-        ns = (N / 32 * mblocks >= k->gemm_min_blocks) ? 2 : 1;
-      } else {
-        ns = 2;
-      }
+    if (nb4 >= want) {
+      ns = 4;
+    } else if (a.KT >= kGemmLongK) {
+      ns = 4;
+      splits = std::max(1, std::min((kGemmSplitTarget + nb4 - 1) / nb4, a.KT / 64));
+    } else if (nb2 >= want) {
+      ns = 2;
+    } else {
+      ns = 2;
+      splits = std::max(1, std::min((kGemmSplitTarget + nb2 - 1) / nb2, a.KT / 64));
     }
+    while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > kGemmPartBytes) --splits;
     if (epi == EPI_LM) {
       lm_parts = a.NT / ns;
       a.n_part = lm_parts;

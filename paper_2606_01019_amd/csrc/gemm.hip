@@ -13,12 +13,14 @@
 // 64-column group are contiguous after packing) and reuses each activation
 // fragment for all NS strips, with a prefetch queue of depth U (weights and
 // activations issued together so the in-order vmcnt waits never stall on a
-// younger load).  Partial sums are reduced through LDS in a fixed order.
-// When the column blocks alone are too few to keep enough weight bytes in
-// flight, K is also split across workgroups (gridDim.y): each publishes its
-// partial tile and a second kernel sums the splits in order (deterministic;
-// a kernel boundary is cheaper here than device-scope release fences).  The
-// fused epilogue:
+// younger load).  The epilogue's own inputs (row sums of squares, residual
+// tile, rotary factors, KV page ids) are fetched into LDS right after the
+// first weight loads, so no dependent memory round trip is left for the end.
+// Partial sums are reduced through LDS in a fixed order.  When the column
+// blocks alone are too few to keep enough weight bytes in flight, K is also
+// split across workgroups (gridDim.y): each publishes its partial tile and a
+// second kernel sums the splits in order (deterministic; a kernel boundary is
+// cheaper here than device-scope release fences).  Fused epilogues:
 //   EPI_QKV   inverse-RMS row scale, rotary embedding on q and k (pairs are
 //             adjacent columns after the load-time permutation), q -> Q
 //             buffer, k/v -> paged fp16 KV cache;
@@ -43,51 +45,138 @@ constexpr int gemm_depth(int MT, int NS) {
   return d < 1 ? 1 : (d > 8 ? 8 : d);
 }
 
-constexpr int kKG = 8;      // waves per workgroup, each a contiguous K range
+constexpr int kKG = 8;  // waves per workgroup, each a contiguous K range
+
+// Epilogue inputs staged in LDS before the main loop.
+template <int MT, int NS, int EPI>
+struct EpiPre {
+  static constexpr int ROWS = MT * 16, COLS = NS * 16;
+  float inv_rms[ROWS];
+  float x[EPI == EPI_RESID ? ROWS : 1][EPI == EPI_RESID ? COLS : 1];
+  float gain[EPI == EPI_RESID ? COLS : 1];
+  float2 rope[EPI == EPI_QKV ? ROWS : 1][EPI == EPI_QKV ? COLS / 2 : 1];
+  int page[EPI == EPI_QKV ? ROWS : 1];
+  int pos[EPI == EPI_QKV ? ROWS : 1];
+};
+
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void gemm_prefetch(const GemmArgs& a, EpiPre<MT, NS, EPI>& p, int cb, int mt0,
+                                              int mcount) {
+  constexpr int ROWS = MT * 16, COLS = NS * 16;
+  const int tid = threadIdx.x;
+  const int row0 = mt0 * 16, col0 = cb * COLS, rows_here = mcount * 16;
+  // inverse RMS of the block's rows from per-16-column sums of squares,
+  // summed in a fixed order (rows past the last tile get 1/sqrt(eps))
+  if (a.ss != nullptr) {
+    // TPR threads per row, each summing float4 groups q = j, j+TPR, ... of
+    // the row's ss_n entries, four loads in flight per round
+    constexpr int TPR = (512 / ROWS) >= 32 ? 32 : (512 / ROWS) >= 16 ? 16 : (512 / ROWS) >= 8 ? 8 : 4;
+    const int r = tid / TPR, j = tid % TPR;
+    if (r < ROWS) {
+      float sacc = 0.f;
+      if (r < rows_here) {
+        const float4* srow = (const float4*)(a.ss + (size_t)(row0 + r) * a.ss_n);
+        const int nq = a.ss_n >> 2;
+        for (int q0 = j; q0 < nq; q0 += 4 * TPR) {
+          float4 v[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            v[q] = (q0 + q * TPR < nq) ? srow[q0 + q * TPR] : float4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sacc += (v[q].x + v[q].y) + (v[q].z + v[q].w);
+        }
+      }
+#pragma unroll
+      for (int o = TPR / 2; o > 0; o >>= 1) sacc += __shfl_xor(sacc, o);
+      if (j == 0) p.inv_rms[r] = rsqrtf(sacc * a.inv_dim + a.eps);
+    }
+  } else if (tid < ROWS) {
+    p.inv_rms[tid] = 1.f;
+  }
+  if constexpr (EPI == EPI_RESID) {
+    for (int e = tid; e < rows_here * (COLS / 4); e += 512) {
+      const int r = e / (COLS / 4), c4 = (e % (COLS / 4)) * 4;
+      const float4 v = *(const float4*)(a.X + (size_t)(row0 + r) * a.D + col0 + c4);
+      p.x[r][c4] = v.x;
+      p.x[r][c4 + 1] = v.y;
+      p.x[r][c4 + 2] = v.z;
+      p.x[r][c4 + 3] = v.w;
+    }
+    if (tid < COLS) p.gain[tid] = a.gain_next[col0 + tid];
+  }
+  if constexpr (EPI == EPI_QKV) {
+    const bool rotated = col0 < a.q_cols + a.kv_cols;  // block holds q or k columns
+    const bool cached = col0 + COLS > a.q_cols;        // block holds k or v columns
+    const int half = a.dh >> 1;
+    for (int e = tid; e < rows_here; e += 512) {
+      const int R = row0 + e;
+      int pos = 0, page = 0;
+      if (R < a.M) {
+        const RowMeta rm = a.rows[R];
+        pos = rm.pos;
+        if (cached) page = a.pt[(size_t)rm.slot * a.pt_stride + (rm.pos >> 4)];
+      }
+      p.pos[e] = pos;
+      p.page[e] = page;
+    }
+    if (rotated) {
+      for (int e = tid; e < rows_here * (COLS / 2); e += 512) {
+        const int r = e / (COLS / 2), cp = e % (COLS / 2);
+        const int R = row0 + r;
+        const int C = col0 + 2 * cp;
+        const int base = C < a.q_cols ? 0 : a.q_cols;
+        const int j = ((C - base) % a.dh) >> 1;
+        p.rope[r][cp] = R < a.M ? a.rope[(size_t)a.rows[R].pos * half + j] : float2{1.f, 0.f};
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ uint4 pack8(const uint16_t* v) {
+  return uint4{v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
+               v[6] | ((uint32_t)v[7] << 16)};
+}
 
 // Fused epilogue on the reduced [rows][cols] tile of one workgroup.
-template <int MT, int kNS, int EPI>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[kNS * 16 + 1], const float* inv_rms,
-                                              int cb, int mt0, int mcount) {
-  constexpr int COLS = kNS * 16;
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[NS * 16 + 1],
+                                              const EpiPre<MT, NS, EPI>& p, int cb, int mt0, int mcount) {
+  constexpr int COLS = NS * 16;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int rows_here = mcount * 16;
   const int row0 = mt0 * 16;
   const int col0 = cb * COLS;
+
   if constexpr (EPI == EPI_QKV) {
-    const int half = a.dh >> 1;
     for (int e = tid; e < rows_here * (COLS / 2); e += 512) {
-      int r = e / (COLS / 2), cp = (e % (COLS / 2)) * 2;
-      int R = row0 + r;
+      const int r = e / (COLS / 2), cp = e % (COLS / 2);
+      const int R = row0 + r;
       if (R >= a.M) continue;
-      float v0 = tile[r][cp] * inv_rms[r];
-      float v1 = tile[r][cp + 1] * inv_rms[r];
-      int C = col0 + cp;
-      RowMeta rm = a.rows[R];
+      const float v0 = tile[r][2 * cp] * p.inv_rms[r];
+      const float v1 = tile[r][2 * cp + 1] * p.inv_rms[r];
+      const int C = col0 + 2 * cp;
       if (C < a.q_cols + a.kv_cols) {
-        int base = C < a.q_cols ? 0 : a.q_cols;
-        int dp = (C - base) % a.dh;  // even: pair (dp, dp+1) = (j, j + dh/2) in the original order
-        int j = dp >> 1;
-        float2 cs = a.rope[(size_t)rm.pos * half + j];
-        float o0 = v0 * cs.x - v1 * cs.y;
-        float o1 = v1 * cs.x + v0 * cs.y;
+        const int base = C < a.q_cols ? 0 : a.q_cols;
+        const int dp = (C - base) % a.dh;  // even: pair (dp, dp+1) = (j, j + dh/2) in the original order
+        const float2 cs = p.rope[r][cp];
+        const float o0 = v0 * cs.x - v1 * cs.y;
+        const float o1 = v1 * cs.x + v0 * cs.y;
         if (C < a.q_cols) {
           a.Q[(size_t)R * a.q_cols + C] = (_Float16)o0;
           a.Q[(size_t)R * a.q_cols + C + 1] = (_Float16)o1;
         } else {
-          int g = (C - base) / a.dh;
-          int page = a.pt[(size_t)rm.slot * a.pt_stride + (rm.pos >> 4)];
-          _Float16* kp = a.kv + (size_t)page * a.page_stride + ((size_t)g * kPage + (rm.pos & 15)) * a.dh + dp;
+          const int g = (C - base) / a.dh;
+          _Float16* kp =
+              a.kv + (size_t)p.page[r] * a.page_stride + ((size_t)g * kPage + (p.pos[r] & 15)) * a.dh + dp;
           kp[0] = (_Float16)o0;
           kp[1] = (_Float16)o1;
         }
       } else {
-        int cv = C - a.q_cols - a.kv_cols;
-        int g = cv / a.dh, d = cv % a.dh;
-        int page = a.pt[(size_t)rm.slot * a.pt_stride + (rm.pos >> 4)];
-        _Float16* vp = a.kv + (size_t)page * a.page_stride + (size_t)a.Hkv * kPage * a.dh +
-                       ((size_t)g * a.dh + d) * kPage + (rm.pos & 15);
+        const int cv = C - a.q_cols - a.kv_cols;
+        const int g = cv / a.dh, d = cv % a.dh;
+        _Float16* vp = a.kv + (size_t)p.page[r] * a.page_stride + (size_t)a.Hkv * kPage * a.dh +
+                       ((size_t)g * a.dh + d) * kPage + (p.pos[r] & 15);
         vp[0] = (_Float16)v0;
         vp[kPage] = (_Float16)v1;
       }
@@ -96,78 +185,73 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[k
     // octets of 8 consecutive columns of one row: 16-byte fragment stores
     constexpr int OCT = COLS / 8;
     for (int base = 0; base < rows_here * OCT; base += 512) {
-      int e = base + tid;
-      bool ok = e < rows_here * OCT;
-      int r = ok ? e / OCT : 0, o = ok ? e % OCT : 0;
-      int R = row0 + r, C = col0 + o * 8;
+      const int e = base + tid;
+      const bool ok = e < rows_here * OCT;
+      const int r = ok ? e / OCT : 0, o = ok ? e % OCT : 0;
+      const int R = row0 + r, C = col0 + o * 8;
       float sq = 0.f;
       if (ok) {
-        float* xp = a.X + (size_t)R * a.D + C;
-        float4 x0 = *(float4*)xp, x1 = *(float4*)(xp + 4);
-        float xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        float xv[8];
         uint16_t hi[8], lo[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          xv[i] += tile[r][o * 8 + i];
+          xv[i] = p.x[r][o * 8 + i] + tile[r][o * 8 + i];
           sq += xv[i] * xv[i];
-          split_bf16(xv[i] * a.gain_next[C + i], hi[i], lo[i]);
+          split_bf16(xv[i] * p.gain[o * 8 + i], hi[i], lo[i]);
         }
+        float* xp = a.X + (size_t)R * a.D + C;
         *(float4*)xp = float4{xv[0], xv[1], xv[2], xv[3]};
         *(float4*)(xp + 4) = float4{xv[4], xv[5], xv[6], xv[7]};
-        size_t off = afrag_off(R, C, a.MTtot);
-        uint4 h, l;
-        h.x = hi[0] | ((uint32_t)hi[1] << 16); h.y = hi[2] | ((uint32_t)hi[3] << 16);
-        h.z = hi[4] | ((uint32_t)hi[5] << 16); h.w = hi[6] | ((uint32_t)hi[7] << 16);
-        l.x = lo[0] | ((uint32_t)lo[1] << 16); l.y = lo[2] | ((uint32_t)lo[3] << 16);
-        l.z = lo[4] | ((uint32_t)lo[5] << 16); l.w = lo[6] | ((uint32_t)lo[7] << 16);
-        *(uint4*)(a.Nhi + off) = h;
-        *(uint4*)(a.Nlo + off) = l;
+        const size_t off = afrag_off(R, C, a.MTtot);
+        *(uint4*)(a.Nhi + off) = pack8(hi);
+        *(uint4*)(a.Nlo + off) = pack8(lo);
       }
-      float other = __shfl_xor(sq, 1);
+      const float other = __shfl_xor(sq, 1);
       if (ok && (o & 1) == 0) a.ss_out[(size_t)R * (a.D >> 4) + (C >> 4)] = sq + other;
     }
   } else if constexpr (EPI == EPI_SILU) {
-    // strip pairs (2s = gate, 2s+1 = up) -> act columns (cb*2 + s)*16 + c
+    // strip pairs (2s = gate, 2s+1 = up) -> act columns (cb*NS/2 + s)*16 + c
     constexpr int OCT = COLS / 16;  // act octets per row
     for (int e = tid; e < rows_here * OCT; e += 512) {
-      int r = e / OCT, o = e % OCT;
-      int s_ = o >> 1, c8 = (o & 1) * 8;
-      int R = row0 + r;
-      int F = (cb * (kNS / 2) + s_) * 16 + c8;
+      const int r = e / OCT, o = e % OCT;
+      const int s_ = o >> 1, c8 = (o & 1) * 8;
+      const int R = row0 + r;
+      const int F = (cb * (NS / 2) + s_) * 16 + c8;
       uint16_t hi[8], lo[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        float g = tile[r][s_ * 32 + c8 + i] * inv_rms[r];
-        float u = tile[r][s_ * 32 + 16 + c8 + i] * inv_rms[r];
-        float act = g / (1.f + __expf(-g)) * u;
+        const float g = tile[r][s_ * 32 + c8 + i] * p.inv_rms[r];
+        const float u = tile[r][s_ * 32 + 16 + c8 + i] * p.inv_rms[r];
+        const float act = g / (1.f + __expf(-g)) * u;
         split_bf16(act, hi[i], lo[i]);
       }
-      size_t off = afrag_off(R, F, a.MTtot);
-      uint4 h, l;
-      h.x = hi[0] | ((uint32_t)hi[1] << 16); h.y = hi[2] | ((uint32_t)hi[3] << 16);
-      h.z = hi[4] | ((uint32_t)hi[5] << 16); h.w = hi[6] | ((uint32_t)hi[7] << 16);
-      l.x = lo[0] | ((uint32_t)lo[1] << 16); l.y = lo[2] | ((uint32_t)lo[3] << 16);
-      l.z = lo[4] | ((uint32_t)lo[5] << 16); l.w = lo[6] | ((uint32_t)lo[7] << 16);
-      *(uint4*)(a.act_hi + off) = h;
-      *(uint4*)(a.act_lo + off) = l;
+      const size_t off = afrag_off(R, F, a.MTtot);
+      *(uint4*)(a.act_hi + off) = pack8(hi);
+      *(uint4*)(a.act_lo + off) = pack8(lo);
     }
   } else {  // EPI_LM
     // one wave per row (loop): logits, then max / lowest argmax over COLS columns
     for (int r = wave; r < rows_here; r += 8) {
-      int R = row0 + r;
+      const int R = row0 + r;
       if (R >= a.M) break;
       float best = -INFINITY;
       int bidx = 0x7fffffff;
       for (int c = lane; c < COLS; c += 64) {
-        float v = tile[r][c] * inv_rms[r];
+        const float v = tile[r][c] * p.inv_rms[r];
         if (a.logits) a.logits[(size_t)R * a.vocab + col0 + c] = v;
-        if (v > best) { best = v; bidx = col0 + c; }
+        if (v > best) {
+          best = v;
+          bidx = col0 + c;
+        }
       }
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) {
-        float ov = __shfl_xor(best, o);
-        int oi = __shfl_xor(bidx, o);
-        if (ov > best || (ov == best && oi < bidx)) { best = ov; bidx = oi; }
+        const float ov = __shfl_xor(best, o);
+        const int oi = __shfl_xor(bidx, o);
+        if (ov > best || (ov == best && oi < bidx)) {
+          best = ov;
+          bidx = oi;
+        }
       }
       if (lane == 0) {
         a.part_val[(size_t)R * a.n_part + blockIdx.x] = best;
@@ -177,45 +261,25 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[k
   }
 }
 
-// Inverse RMS of the workgroup's rows from per-16-column sums of squares,
-// summed in a fixed order (rows past the last tile get 1/sqrt(eps)).
-template <int MT>
-__device__ __forceinline__ void gemm_inv_rms(const GemmArgs& a, float* inv_rms, int mt0, int mcount) {
-  constexpr int ROWS = MT * 16;
-  const int tid = threadIdx.x;
-  if (a.ss != nullptr) {
-    constexpr int TPR = (512 / ROWS) >= 32 ? 32 : (512 / ROWS) >= 16 ? 16 : (512 / ROWS) >= 8 ? 8 : 4;
-    const int r = tid / TPR, j = tid % TPR;
-    if (r < ROWS) {
-      float sacc = 0.f;
-      if (r < mcount * 16) {
-        const float* srow = a.ss + (size_t)(mt0 * 16 + r) * a.ss_n;
-        for (int i = j; i < a.ss_n; i += TPR) sacc += srow[i];
-      }
-#pragma unroll
-      for (int o = TPR / 2; o > 0; o >>= 1) sacc += __shfl_xor(sacc, o);
-      if (j == 0) inv_rms[r] = rsqrtf(sacc * a.inv_dim + a.eps);
-    }
-  } else if (tid < ROWS) {
-    inv_rms[tid] = 1.f;
-  }
-}
-
-template <int MT, int kNS, int EPI>
+template <int MT, int NS, int EPI>
 __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs a) {
-  constexpr int U = gemm_depth(MT, kNS);
+  constexpr int U = gemm_depth(MT, NS);
   constexpr int ROWS = MT * 16;
-  constexpr int COLS = kNS * 16;
+  constexpr int COLS = NS * 16;
 
-  __shared__ float red[4][kNS][MT][256];
+  __shared__ float red[4][NS][MT][256];
   __shared__ float tile[ROWS][COLS + 1];
-  __shared__ float inv_rms[ROWS];
+  __shared__ EpiPre<MT, NS, EPI> pre;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  // wave index made wave-uniform so K ranges and fragment bases stay in
+  // scalar registers (one VGPR per lane of addressing, no register reuse
+  // that would force the prefetch queue to drain)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int cb = blockIdx.x;
   const int mt0 = blockIdx.z * MT;
   const int mcount = min(MT, a.MTtot - mt0);
+  const bool split = gridDim.y > 1;
 
   // K range of this wave: the workgroup's share of K (split gridDim.y ways)
   // divided kKG ways
@@ -225,65 +289,76 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   const int k0 = wk0 + wave * per;
   const int k1 = min(wk1, k0 + per);
 
-  f32x4 acc[MT][kNS];
+  f32x4 acc[MT][NS];
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
-    for (int n = 0; n < kNS; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int n = 0; n < NS; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // strip s, K step kt at ((s/4*KT + kt)*4 + s%4)*64: strip n of this
   // block at wp[n] + kt*256
-  const u32x4* wp[kNS];
+  const u32x4* wp[NS];
 #pragma unroll
-  for (int n = 0; n < kNS; ++n) {
-    const int st = cb * kNS + n;
-    wp[n] = (const u32x4*)a.W + ((size_t)(st >> 2) * a.KT * 4 + (st & 3)) * 64 + lane;
+  for (int n = 0; n < NS; ++n) {
+    const int st = cb * NS + n;
+    wp[n] = (const u32x4*)a.W + ((size_t)(st >> 2) * a.KT * 4 + (st & 3)) * 64;
   }
   const size_t astride = (size_t)a.MTtot * 64;
-  const u32x4* hp = (const u32x4*)a.Ahi + (size_t)mt0 * 64 + lane;
-  const u32x4* lp = (const u32x4*)a.Alo + (size_t)mt0 * 64 + lane;
+  const u32x4* hp = (const u32x4*)a.Ahi + (size_t)mt0 * 64;
+  const u32x4* lp = (const u32x4*)a.Alo + (size_t)mt0 * 64;
 
-  u32x4 qb[U][kNS], qh[U][MT], ql[U][MT];
+  // Stage u of the prefetch queue holds the fragments of one K step.  Row
+  // tiles past this block's last are read from the operand's padding and
+  // computed, then dropped (no per-tile branches in the loop).
+  u32x4 qb[U][NS], qh[U][MT], ql[U][MT];
+  auto load = [&](int u, int kt) __attribute__((always_inline)) {
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int kt = k0 + u;
-    if (kt < k1) {
+    for (int n = 0; n < NS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)kt * 256 + lane);
 #pragma unroll
-      for (int n = 0; n < kNS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)kt * 256);
-#pragma unroll
-      for (int m = 0; m < MT; ++m)
-        if (m < mcount) {
-          qh[u][m] = hp[kt * astride + m * 64];
-          ql[u][m] = lp[kt * astride + m * 64];
-        }
+    for (int m = 0; m < MT; ++m) {
+      qh[u][m] = hp[kt * astride + m * 64 + lane];
+      ql[u][m] = lp[kt * astride + m * 64 + lane];
     }
-  }
-  for (int kb = k0; kb < k1; kb += U) {
+  };
+  auto consume = [&](int u) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        acc[m][n] = mfma_bf16(qh[u][m], qb[u][n], acc[m][n]);
+        acc[m][n] = mfma_bf16(ql[u][m], qb[u][n], acc[m][n]);
+      }
+  };
+
+  const int nsteps = k1 - k0;  // wave-uniform
+  if (nsteps >= U) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) load(u, k0 + u);
+    if (!split) gemm_prefetch<MT, NS, EPI>(a, pre, cb, mt0, mcount);
+    int kt = k0;
+    // steady state: every stage is consumed and refilled, no branches
+    for (; kt + 2 * U <= k1; kt += U) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        consume(u);
+        load(u, kt + u + U);
+      }
+    }
+    // tail: the U stages in flight hold kt..kt+U-1; fewer than U steps remain after them
+    const int rem = k1 - (kt + U);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kt = kb + u;
-      if (kt < k1) {
+      consume(u);
+      if (u < rem) load(u, kt + U + u);
+    }
 #pragma unroll
-        for (int m = 0; m < MT; ++m)
-          if (m < mcount) {
-#pragma unroll
-            for (int n = 0; n < kNS; ++n) {
-              acc[m][n] = mfma_bf16(qh[u][m], qb[u][n], acc[m][n]);
-              acc[m][n] = mfma_bf16(ql[u][m], qb[u][n], acc[m][n]);
-            }
-          }
-        const int nk = kt + U;
-        if (nk < k1) {
-#pragma unroll
-          for (int n = 0; n < kNS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)nk * 256);
-#pragma unroll
-          for (int m = 0; m < MT; ++m)
-            if (m < mcount) {
-              qh[u][m] = hp[nk * astride + m * 64];
-              ql[u][m] = lp[nk * astride + m * 64];
-            }
-        }
-      }
+    for (int u = 0; u < U; ++u)
+      if (u < rem) consume(u);
+  } else {
+    if (!split) gemm_prefetch<MT, NS, EPI>(a, pre, cb, mt0, mcount);
+    for (int kt = k0; kt < k1; ++kt) {
+      load(0, kt);
+      consume(0);
     }
   }
 
@@ -292,7 +367,7 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
-      for (int n = 0; n < kNS; ++n)
+      for (int n = 0; n < NS; ++n)
 #pragma unroll
         for (int i = 0; i < 4; ++i) red[wave - 4][n][m][lane * 4 + i] = acc[m][n][i];
   }
@@ -301,38 +376,38 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
-      for (int n = 0; n < kNS; ++n)
+      for (int n = 0; n < NS; ++n)
 #pragma unroll
         for (int i = 0; i < 4; ++i) red[wave][n][m][lane * 4 + i] += acc[m][n][i];
   }
   __syncthreads();
-  for (int e = tid; e < kNS * MT * 256; e += 512) {
+  for (int e = tid; e < NS * MT * 256; e += 512) {
     const int n = e / (MT * 256), rem = e % (MT * 256);
     const int m = rem / 256, li = rem % 256;
     const int ln = li >> 2, i = li & 3;
     const float v = (red[0][n][m][li] + red[1][n][m][li]) + (red[2][n][m][li] + red[3][n][m][li]);
     tile[m * 16 + (ln >> 4) * 4 + i][n * 16 + (ln & 15)] = v;
   }
-  if (gridDim.y > 1) {
+  __syncthreads();
+
+  if (split) {
     // K split across workgroups: publish the partial tile; gemm_finish sums
     // the splits in order and runs the epilogue.
     float* dst = a.part + ((size_t)(blockIdx.z * gridDim.x + cb) * gridDim.y + blockIdx.y) * ROWS * COLS;
     for (int e = tid; e < mcount * 16 * COLS; e += 512) dst[e] = tile[e / COLS][e % COLS];
     return;
   }
-  gemm_inv_rms<MT>(a, inv_rms, mt0, mcount);
-  __syncthreads();
-  gemm_epilogue<MT, kNS, EPI>(a, tile, inv_rms, cb, mt0, mcount);
+  gemm_epilogue<MT, NS, EPI>(a, tile, pre, cb, mt0, mcount);
 }
 
 // Second pass of a K-split GEMM: one workgroup per (column block, row block)
 // sums the splits' partial tiles in split order, then runs the epilogue.
-template <int MT, int kNS, int EPI>
+template <int MT, int NS, int EPI>
 __global__ __launch_bounds__(512) void gemm_finish(GemmArgs a, int splits) {
   constexpr int ROWS = MT * 16;
-  constexpr int COLS = kNS * 16;
+  constexpr int COLS = NS * 16;
   __shared__ float tile[ROWS][COLS + 1];
-  __shared__ float inv_rms[ROWS];
+  __shared__ EpiPre<MT, NS, EPI> pre;
   const int cb = blockIdx.x;
   const int mt0 = blockIdx.z * MT;
   const int mcount = min(MT, a.MTtot - mt0);
@@ -342,9 +417,9 @@ __global__ __launch_bounds__(512) void gemm_finish(GemmArgs a, int splits) {
     for (int q = 0; q < splits; ++q) v += src[(size_t)q * ROWS * COLS + e];
     tile[e / COLS][e % COLS] = v;
   }
-  gemm_inv_rms<MT>(a, inv_rms, mt0, mcount);
+  gemm_prefetch<MT, NS, EPI>(a, pre, cb, mt0, mcount);
   __syncthreads();
-  gemm_epilogue<MT, kNS, EPI>(a, tile, inv_rms, cb, mt0, mcount);
+  gemm_epilogue<MT, NS, EPI>(a, tile, pre, cb, mt0, mcount);
 }
 
 template <int NS, int EPI>
