@@ -152,10 +152,12 @@ int32_t hvd_kv_free_pages(hvd_kv kv);
 
 /* Per-kernel timing: while enabled, every launch of a kernel family is
  * bracketed by HIP events on the handle's stream and its algorithmic HBM bytes
- * (weights streamed, KV read) are accumulated.  family: 0 = weight-streaming
- * GEMMs, 1 = verify attention, 2 = everything else.  hvd_profile_read returns
- * the summed event time (ms), launch count and algorithmic bytes since the
- * last enable. */
+ * (weights streamed, KV read) are accumulated.  family: 0 = QKV GEMM,
+ * 1 = O GEMM, 2 = gate/up GEMM, 3 = down GEMM, 4 = LM-head GEMM (a GEMM launch
+ * includes its split-K finish pass when it has one), 5 = verify attention,
+ * 6 = attention combine, 7 = everything else.  hvd_profile_read returns the
+ * summed event time (ms), launch count and algorithmic bytes since the last
+ * enable.  The events add a little time to every bracketed launch. */
 hvd_status hvd_profile_enable(hvd_kv kv, int32_t enable);
 hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* launches, double* bytes);
 

@@ -40,6 +40,9 @@ constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GE
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
 constexpr int kAttnRows = 128;     // query rows per attention work item
 constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items)
+// profiling families: GEMM by role, attention, combine, everything else
+enum { PF_QKV = 0, PF_O = 1, PF_GATEUP = 2, PF_DOWN = 3, PF_LM = 4, PF_ATTN = 5, PF_COMBINE = 6, PF_OTHER = 7,
+       kProfFamilies = 8 };
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -316,8 +319,8 @@ struct hvd_kv_s {
   bool prof = false;
   std::vector<ProfRec> prof_pending;
   std::vector<hipEvent_t> ev_pool;
-  double prof_ms[3] = {0, 0, 0}, prof_bytes[3] = {0, 0, 0};
-  int64_t prof_n[3] = {0, 0, 0};
+  double prof_ms[kProfFamilies] = {}, prof_bytes[kProfFamilies] = {};
+  int64_t prof_n[kProfFamilies] = {};
 };
 
 namespace {
@@ -619,7 +622,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     e.n_upd = (int)last.size();
     e.pt = k->pt;
     e.pt_stride = k->pt_stride;
-    ProfScope ps(k, 2, 0.0);
+    ProfScope ps(k, PF_OTHER, 0.0);
     HIP_TRY(launch_embed(e, s));
   }
 
@@ -629,7 +632,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   // per workgroup when that alone gives enough workgroups; for long-K GEMMs
   // 4 strips plus a K split; otherwise 2 strips, K-split if still too few.
   int lm_parts = 0;
-  auto gemm = [&](int epi, GemmArgs& a, int N, int K) -> hvd_status {
+  auto gemm = [&](int epi, GemmArgs& a, int N, int K, int family) -> hvd_status {
     a.KT = K / 32;
     a.NT = N / 16;
     a.MTtot = MT;
@@ -654,7 +657,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       lm_parts = a.NT / ns;
       a.n_part = lm_parts;
     }
-    ProfScope ps(k, 0, (double)N * K * 2.0);
+    ProfScope ps(k, family, (double)N * K * 2.0);
     HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, s));
     return HVD_OK;
   };
@@ -684,7 +687,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.pt_stride = k->pt_stride;
       a.rows = d_rows;
       a.rope = m->rope;
-      if (hvd_status st = gemm(EPI_QKV, a, qd + 2 * kvd, D); st != HVD_OK) return st;
+      if (hvd_status st = gemm(EPI_QKV, a, qd + 2 * kvd, D, PF_QKV); st != HVD_OK) return st;
     }
     {
       AttnArgs a{};
@@ -705,7 +708,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.part_o = k->part_o;
       a.part_ml = k->part_ml;
       {
-        ProfScope ps(k, 1, kv_bytes);
+        ProfScope ps(k, PF_ATTN, kv_bytes);
         HIP_TRY(launch_attn(a, (int)plan.items.size(), s));
       }
       if (!plan.heads.empty()) {
@@ -720,7 +723,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
         cb.Ohi = k->Ohi;
         cb.Olo = k->Olo;
         cb.MTtot = MT;
-        ProfScope ps(k, 2, 0.0);
+        ProfScope ps(k, PF_COMBINE, 0.0);
         HIP_TRY(launch_combine(cb, (int)plan.heads.size(), s));
       }
     }
@@ -735,7 +738,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.Nhi = k->Nhi;
       a.Nlo = k->Nlo;
       a.ss_out = k->ss;
-      if (hvd_status st = gemm(EPI_RESID, a, D, qd); st != HVD_OK) return st;
+      if (hvd_status st = gemm(EPI_RESID, a, D, qd, PF_O); st != HVD_OK) return st;
     }
     {
       GemmArgs a{};
@@ -748,7 +751,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.eps = c.rms_eps;
       a.act_hi = k->Ahi;
       a.act_lo = k->Alo;
-      if (hvd_status st = gemm(EPI_SILU, a, 2 * F, D); st != HVD_OK) return st;
+      if (hvd_status st = gemm(EPI_SILU, a, 2 * F, D, PF_GATEUP); st != HVD_OK) return st;
     }
     {
       GemmArgs a{};
@@ -761,7 +764,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.Nhi = k->Nhi;
       a.Nlo = k->Nlo;
       a.ss_out = k->ss;
-      if (hvd_status st = gemm(EPI_RESID, a, D, F); st != HVD_OK) return st;
+      if (hvd_status st = gemm(EPI_RESID, a, D, F, PF_DOWN); st != HVD_OK) return st;
     }
   }
   if (lm_head) {
@@ -777,7 +780,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     a.vocab = c.vocab;
     a.part_val = k->lm_val;
     a.part_idx = k->lm_idx;
-    if (hvd_status st = gemm(EPI_LM, a, c.vocab, D); st != HVD_OK) return st;
+    if (hvd_status st = gemm(EPI_LM, a, c.vocab, D, PF_LM); st != HVD_OK) return st;
     AcceptArgs ac{};
     ac.part_val = k->lm_val;
     ac.part_idx = k->lm_idx;
@@ -790,7 +793,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     ac.out = k->out;
     ac.counter = k->counter;
     {
-      ProfScope ps(k, 2, 0.0);
+      ProfScope ps(k, PF_OTHER, 0.0);
       HIP_TRY(launch_accept(ac, s));
     }
     HIP_TRY(hipMemcpyAsync(k->out_host, k->out, 2 * (size_t)B * 4, hipMemcpyDeviceToHost, s));
@@ -891,7 +894,7 @@ extern "C" int32_t hvd_kv_free_pages(hvd_kv k) { return k ? k->hs->free_pages() 
 extern "C" hvd_status hvd_profile_enable(hvd_kv k, int32_t enable) {
   if (!k) return set_err(HVD_ERR_ARG, "null handle");
   k->prof = enable != 0;
-  for (int i = 0; i < 3; ++i) {
+  for (int i = 0; i < kProfFamilies; ++i) {
     k->prof_ms[i] = 0;
     k->prof_bytes[i] = 0;
     k->prof_n[i] = 0;
@@ -900,7 +903,7 @@ extern "C" hvd_status hvd_profile_enable(hvd_kv k, int32_t enable) {
 }
 
 extern "C" hvd_status hvd_profile_read(hvd_kv k, int32_t family, double* ms, int64_t* launches, double* bytes) {
-  if (!k || family < 0 || family > 2) return set_err(HVD_ERR_ARG, "bad handle or family");
+  if (!k || family < 0 || family >= kProfFamilies) return set_err(HVD_ERR_ARG, "bad handle or family");
   if (ms) *ms = k->prof_ms[family];
   if (launches) *launches = k->prof_n[family];
   if (bytes) *bytes = k->prof_bytes[family];

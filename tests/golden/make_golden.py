@@ -99,8 +99,36 @@ def case_cfg2():
             "oracle_dtype": "float32"}
 
 
+def case_cfg3():
+    cfg = SHAPE_8B
+    log("cfg3: weights")
+    m = fp32_model(cfg)
+    ctx = wt.segment_context(wt.rng_for("context", 3), 16384, cfg.vocab)
+    log("cfg3: prefill")
+    st = oracle.prefill(m, ctx)
+    ids = sample_ids(cfg.vocab)
+    arng = wt.rng_for("accept", 30)
+    ks = [32, 48, 64]
+    plans = [wt.bimodal_accept(arng, k) for k in ks]
+    log(f"cfg3: greedy continuation for plans {plans}")
+    g = greedy(m, st, max(a + 1 for a in plans) + 1)
+    drng = wt.rng_for("draft", 30)
+    steps = []
+    for k, a in zip(ks, plans):
+        d = wt.plant_cache_draft(drng, ctx, g, a, k, cfg.vocab)
+        res = oracle.verify(m, st, d)
+        log(f"cfg3: k={k} planted={a} accepted={res.accepted}")
+        steps.append(record(res, ids))
+    return {"config": "8B shape, batch 1, context 16384 built from 64-token segments (16 base segments, 20% "
+                      "per-token mutation), cache drafts k in 32,48,64 planted bimodal from the oracle's greedy "
+                      "continuation, tail copied from an earlier context span",
+            "model": cfg.as_dict(), "context_seed": ["context", 3], "context_len": 16384,
+            "context_kind": "segments", "sample_ids": [int(i) for i in ids], "steps": steps,
+            "oracle_dtype": "float32"}
+
+
 def main():
-    cases = {"cfg2": case_cfg2}
+    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3}
     for name in sys.argv[1:]:
         t0 = time.time()
         out = cases[name]()
