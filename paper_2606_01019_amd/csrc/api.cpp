@@ -8,6 +8,7 @@
 #include <cstring>
 #include <map>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "../../include/hvd.h"
@@ -40,6 +41,7 @@ constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GE
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
 constexpr int kAttnRows = 128;     // query rows per attention work item
 constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items)
+constexpr size_t kMaxGraphs = 64;  // cached step graphs per KV handle
 // profiling families: GEMM by role, attention, combine, everything else
 enum { PF_QKV = 0, PF_O = 1, PF_GATEUP = 2, PF_DOWN = 3, PF_LM = 4, PF_ATTN = 5, PF_COMBINE = 6, PF_OTHER = 7,
        kProfFamilies = 8 };
@@ -275,6 +277,15 @@ extern "C" void hvd_model_free(hvd_model m) {
 
 // ------------------------------------------------------------------ KV handle
 
+struct GraphKey {
+  int M, B, n_items, n_heads, lm_head;
+  float* logits;
+  bool operator<(const GraphKey& o) const {
+    return std::tie(M, B, n_items, n_heads, lm_head, logits) <
+           std::tie(o.M, o.B, o.n_items, o.n_heads, o.lm_head, o.logits);
+  }
+};
+
 struct ProfRec {
   hipEvent_t a, b;
   int family;
@@ -304,6 +315,8 @@ struct hvd_kv_s {
   int32_t* lm_idx = nullptr;
   int n_part_lm = 0;
   int gemm_min_blocks = kGemmMinBlocks;
+  bool use_graphs = false;
+  std::map<GraphKey, hipGraphExec_t> graphs;
   int attn_min_items = kAttnMinItems;
   float* gemm_part = nullptr;
   int32_t* g = nullptr;
@@ -424,6 +437,7 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   k->hs = new HostState(max_seqs, n_pages, kPage, c.max_pos, c.max_draft, c.vocab);
   if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
+  if (const char* e = getenv("HVD_GRAPHS")) k->use_graphs = atoi(e) != 0;
   if (hipError_t e = attn_set_lds_limit(); e != hipSuccess) {
     hvd_kv_free(k);
     return set_err(HVD_ERR_DEVICE, std::string("attention LDS limit: ") + hipGetErrorString(e));
@@ -434,6 +448,7 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
 
 extern "C" void hvd_kv_free(hvd_kv k) {
   if (!k) return;
+  for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
   for (auto e : k->ev_pool) (void)hipEventDestroy(e);
   for (auto& r : k->prof_pending) {
     (void)hipEventDestroy(r.a);
@@ -573,25 +588,38 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   std::map<std::pair<int, int>, int> last;
   for (auto& u : upd_raw) last[{u.slot, u.index}] = u.page;
 
-  // pack metadata: rows | seqs | items | heads | updates
+  // Pad the attention grids to buckets (no-op items have k = -1) so the
+  // launch sequence depends only on (rows, sequences, buckets): one cached
+  // HIP graph per such shape.
+  const size_t n_items = (plan.items.size() + 63) / 64 * 64;
+  const size_t n_heads = (plan.heads.size() + 15) / 16 * 16;
+  {
+    AttnItem none{};
+    none.k = -1;
+    plan.items.resize(n_items, none);
+    plan.heads.resize(n_heads, none);
+  }
+
+  // pack metadata: header | rows | seqs | items | heads | updates
   int32_t* h = k->meta_host;
   size_t off = 0;
   auto put = [&](const void* src, size_t ints) {
-    std::memcpy(h + off, src, ints * 4);
+    if (ints) std::memcpy(h + off, src, ints * 4);
     size_t o = off;
     off += (ints + 3) / 4 * 4;
     return o;
   };
-  const size_t need_ints = 4 * (size_t)M + 4 * (size_t)B + 16 * (plan.items.size() + plan.heads.size()) +
-                           3 * last.size() + 32;
+  const size_t need_ints = 16 + 4 * (size_t)M + 4 * (size_t)B + 16 * (n_items + n_heads) + 3 * last.size() + 32;
   if (need_ints > k->meta_ints) {
     k->hs->take_updates();
     return set_err(HVD_ERR_OOM, "metadata buffer too small");
   }
+  int32_t header[16] = {(int32_t)last.size()};
+  put(header, 16);
   const size_t o_rows = put(rows.data(), 4 * (size_t)M);
   const size_t o_seqs = put(seqs.data(), 4 * (size_t)B);
-  const size_t o_items = put(plan.items.data(), 16 * plan.items.size());
-  const size_t o_heads = put(plan.heads.data(), 16 * plan.heads.size());
+  const size_t o_items = put(plan.items.data(), 16 * n_items);
+  const size_t o_heads = put(plan.heads.data(), 16 * n_heads);
   std::vector<int32_t> upd;
   for (auto& kv : last) {
     upd.push_back(kv.first.first);
@@ -605,6 +633,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   const AttnItem* d_items = (const AttnItem*)(k->meta_dev + o_items);
   const AttnItem* d_heads = (const AttnItem*)(k->meta_dev + o_heads);
 
+  // ---------------------------------------------------------------- launches
+  // Everything below only enqueues kernels whose arguments are fixed by
+  // (M, B, n_items, n_heads, lm_head, logits): captured once per shape into
+  // a HIP graph and replayed (eager while profiling or with graphs off).
+  auto launch_all = [&]() -> hvd_status {
   {
     EmbedArgs e{};
     e.E = m->embed;
@@ -619,7 +652,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     e.ss_out = k->ss;
     e.MTtot = MT;
     e.upd = k->meta_dev + o_upd;
-    e.n_upd = (int)last.size();
+    e.n_upd = k->meta_dev;  // header[0]
     e.pt = k->pt;
     e.pt_stride = k->pt_stride;
     ProfScope ps(k, PF_OTHER, 0.0);
@@ -796,8 +829,38 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       ProfScope ps(k, PF_OTHER, 0.0);
       HIP_TRY(launch_accept(ac, s));
     }
-    HIP_TRY(hipMemcpyAsync(k->out_host, k->out, 2 * (size_t)B * 4, hipMemcpyDeviceToHost, s));
   }
+  return HVD_OK;
+  };  // launch_all
+
+  if (k->prof || !k->use_graphs) {
+    if (hvd_status st = launch_all(); st != HVD_OK) return st;
+  } else {
+    const GraphKey key{M, B, (int)n_items, (int)n_heads, lm_head ? 1 : 0, logits};
+    auto it = k->graphs.find(key);
+    if (it == k->graphs.end()) {
+      if (k->graphs.size() >= kMaxGraphs) {
+        for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+        k->graphs.clear();
+      }
+      hipGraph_t g = nullptr;
+      HIP_TRY(hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
+      const hvd_status st = launch_all();
+      const hipError_t ec = hipStreamEndCapture(s, &g);
+      if (st != HVD_OK) {
+        if (g) (void)hipGraphDestroy(g);
+        return st;
+      }
+      if (ec != hipSuccess) return set_err(HVD_ERR_DEVICE, std::string("graph capture: ") + hipGetErrorString(ec));
+      hipGraphExec_t ge = nullptr;
+      const hipError_t ei = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(g);
+      if (ei != hipSuccess) return set_err(HVD_ERR_DEVICE, std::string("graph instantiate: ") + hipGetErrorString(ei));
+      it = k->graphs.emplace(key, ge).first;
+    }
+    HIP_TRY(hipGraphLaunch(it->second, s));
+  }
+  if (lm_head) HIP_TRY(hipMemcpyAsync(k->out_host, k->out, 2 * (size_t)B * 4, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (k->prof) prof_collect(k);
   return HVD_OK;
@@ -908,6 +971,20 @@ extern "C" hvd_status hvd_profile_read(hvd_kv k, int32_t family, double* ms, int
   if (launches) *launches = k->prof_n[family];
   if (bytes) *bytes = k->prof_bytes[family];
   return HVD_OK;
+}
+
+extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value) {
+  if (!k) return set_err(HVD_ERR_ARG, "null handle");
+  switch (option) {
+    case HVD_OPT_GRAPHS:
+      k->use_graphs = value != 0;
+      if (!k->use_graphs) {
+        for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+        k->graphs.clear();
+      }
+      return HVD_OK;
+  }
+  return set_err(HVD_ERR_ARG, "unknown option");
 }
 
 extern "C" const char* hvd_last_error(void) { return g_err.c_str(); }

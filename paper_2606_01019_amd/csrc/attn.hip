@@ -37,6 +37,7 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
 
   __shared__ int spg[kAttnChunk / kPage];  // page ids of the current sub-chunk
   const AttnItem it = a.items[blockIdx.x];
+  if (it.k < 0) return;  // grid padding
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int G = a.group;
   const int R = (it.k + 1) * G;
@@ -238,6 +239,7 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   constexpr int OCT = DH / 8;
   constexpr int RPB = 256 / OCT;  // rows per block
   const AttnItem hd = a.heads[blockIdx.x / (128 / RPB)];
+  if (hd.k < 0) return;  // grid padding
   const int slice = blockIdx.x % (128 / RPB);
   const int G = a.group;
   const int R = (hd.k + 1) * G;

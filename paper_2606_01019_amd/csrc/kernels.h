@@ -107,8 +107,8 @@ struct EmbedArgs {
   float* ss_out;
   int MTtot;
   // page-table updates applied before any KV write of this step
-  const int32_t* upd;  // [n_upd][3]: slot, index, page
-  int n_upd;
+  const int32_t* upd;    // [n_upd][3]: slot, index, page
+  const int32_t* n_upd;  // device count (metadata header) so the launch is shape-only
   int32_t* pt;
   int pt_stride;
 };

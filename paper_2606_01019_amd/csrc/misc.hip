@@ -40,7 +40,7 @@ hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst
 // applies this step's page-table updates.
 __global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
   if (blockIdx.x == 0)
-    for (int u = threadIdx.x; u < a.n_upd; u += blockDim.x)
+    for (int u = threadIdx.x, n = *a.n_upd; u < n; u += blockDim.x)
       a.pt[(size_t)a.upd[u * 3] * a.pt_stride + a.upd[u * 3 + 1]] = a.upd[u * 3 + 2];
   const int R = blockIdx.x;
   const bool valid = R < a.M;

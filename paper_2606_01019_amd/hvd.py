@@ -19,7 +19,8 @@ _STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM
 
 EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
            "hvd_prefill", "hvd_verify", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
-           "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_last_error")
+           "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error")
+HVD_OPT_GRAPHS = 1
 
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
@@ -79,6 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hvd_profile_enable": (I32, [P, I32]),
         "hvd_profile_read": (I32, [P, I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
                                    ctypes.POINTER(ctypes.c_double)]),
+        "hvd_kv_set_option": (I32, [P, I32, I32]),
         "hvd_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -205,6 +207,10 @@ class KVCache:
         a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
         _check(self.lib.hvd_seq_info(self.handle, seq_id, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
         return a.value, b.value, bool(c.value)
+
+    def set_graphs(self, on: bool):
+        """Replay step kernels from cached HIP graphs, or launch eagerly (default)."""
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_GRAPHS, 1 if on else 0))
 
     def free_pages(self):
         return self.lib.hvd_kv_free_pages(self.handle)
