@@ -345,7 +345,10 @@ size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int p
   const size_t rg_verify = ((size_t)(c.max_draft + 1) * G + kAttnRows - 1) / kAttnRows;
   const size_t rg_prefill = ((size_t)kPrefillRows * G + kAttnRows - 1) / kAttnRows;
   const size_t units = std::max((size_t)max_seqs * rg_verify, rg_prefill) * c.n_kv_heads;
-  return 4 * (size_t)max_rows + 4 * (size_t)max_seqs + 16 * (2 * units + kPartSlots) +
+  // items <= units + kPartSlots and heads <= units, each padded up (to 64
+  // and 16 entries); header and per-section alignment fit in the last term
+  const size_t item_ints = sizeof(AttnItem) / 4;
+  return 4 * (size_t)max_rows + 4 * (size_t)max_seqs + item_ints * (2 * units + kPartSlots + 64 + 16) +
          3 * (size_t)max_seqs * pt_stride + 64;
 }
 
@@ -516,7 +519,8 @@ struct Plan {
 
 // Split every (sequence, kv head, row group) into KV chunks of `chunk`
 // positions, chosen so the launch has enough workgroups to fill the GPU.
-bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, int min_items, Plan& p) {
+bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<SeqMeta>& seqs, int min_items,
+                    Plan& p) {
   const int G = c.n_q_heads / c.n_kv_heads;
   struct Unit { int b, g, rg, keys; };
   auto item = [&](const Unit& u, int c, int nch, int part, int chunk) {
@@ -526,6 +530,14 @@ bool plan_attention(const hvd_config& c, const std::vector<SeqMeta>& seqs, int m
     it.g = u.g; it.c = c; it.nch = nch; it.rg = u.rg; it.part = part;
     it.p_begin = c * chunk;
     it.p_end = std::min(s.ctx + s.k + 1, (c + 1) * chunk);
+    // pages of the first kAttnChunk positions; entries past the chunk's end
+    // repeat its first page (the kernel loads them unconditionally)
+    const std::vector<int32_t>& pg = hs.seq(s.slot).pages;
+    const int first = it.p_begin / kPage;
+    for (int j = 0; j < kItemPages; ++j) {
+      const bool in = it.p_begin + j * kPage < it.p_end;
+      it.pages[j] = pg[(size_t)(in ? first + j : first)];
+    }
     return it;
   };
   std::vector<Unit> units;
@@ -582,7 +594,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   const int G = c.n_q_heads / c.n_kv_heads;
 
   Plan plan;
-  if (!plan_attention(c, seqs, k->attn_min_items, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
+  if (!plan_attention(c, *k->hs, seqs, k->attn_min_items, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
   std::vector<PageUpdate> upd_raw = k->hs->take_updates();
   // keep the last update of each (slot, index): they are applied in parallel
   std::map<std::pair<int, int>, int> last;
@@ -609,7 +621,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
     off += (ints + 3) / 4 * 4;
     return o;
   };
-  const size_t need_ints = 16 + 4 * (size_t)M + 4 * (size_t)B + 16 * (n_items + n_heads) + 3 * last.size() + 32;
+  const size_t need_ints = 16 + 4 * (size_t)M + 4 * (size_t)B + 32 * (n_items + n_heads) + 3 * last.size() + 32;
   if (need_ints > k->meta_ints) {
     k->hs->take_updates();
     return set_err(HVD_ERR_OOM, "metadata buffer too small");
@@ -618,8 +630,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   put(header, 16);
   const size_t o_rows = put(rows.data(), 4 * (size_t)M);
   const size_t o_seqs = put(seqs.data(), 4 * (size_t)B);
-  const size_t o_items = put(plan.items.data(), 16 * n_items);
-  const size_t o_heads = put(plan.heads.data(), 16 * n_heads);
+  const size_t o_items = put(plan.items.data(), sizeof(AttnItem) / 4 * n_items);
+  const size_t o_heads = put(plan.heads.data(), sizeof(AttnItem) / 4 * n_heads);
   std::vector<int32_t> upd;
   for (auto& kv : last) {
     upd.push_back(kv.first.first);
@@ -742,7 +754,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
       a.part_ml = k->part_ml;
       {
         ProfScope ps(k, PF_ATTN, kv_bytes);
-        HIP_TRY(launch_attn(a, (int)plan.items.size(), s));
+        HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, s));
       }
       if (!plan.heads.empty()) {
         CombineArgs cb{};

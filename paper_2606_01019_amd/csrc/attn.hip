@@ -27,24 +27,40 @@
 
 namespace hvd {
 
-template <int DH>
-__global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
-  constexpr int CH = kAttnChunk;
-  constexpr int KSEG = DH / 8;          // 16-byte segments per K row
-  extern __shared__ __align__(16) unsigned char smem[];
-  _Float16* sK = (_Float16*)smem;                       // [CH][DH], segment-swizzled
-  _Float16* sV = (_Float16*)(smem + CH * DH * 2);       // [DH][CH], 8-byte-unit-swizzled
+// Item and page-table reads go through the constant address space: both
+// are read-only while attention runs, and uniform addresses there become
+// scalar loads whose results (page ids included) sit in SGPRs.
+typedef const __attribute__((address_space(4))) AttnItem ConstItem;
+typedef const __attribute__((address_space(4))) int32_t ConstI32;
 
-  __shared__ int spg[kAttnChunk / kPage];  // page ids of the current sub-chunk
-  const AttnItem it = a.items[blockIdx.x];
-  if (it.k < 0) return;  // grid padding
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+// NP = pages staged per sub-chunk (the launch picks it from the chunk
+// length), so short decode chunks issue only the loads they need.
+template <int DH, int NP>
+__global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
+  constexpr int CH = NP * kPage;        // positions per sub-chunk
+  constexpr int KSEG = DH / 8;          // 16-byte segments per K row
+  constexpr int VU = CH / 4;            // 8-byte units per V row in LDS
+  constexpr int VM = VU < 16 ? VU : 16; // V swizzle span (units)
+  constexpr int LPP = DH / 64;          // 16-byte loads per thread per page
+  static_assert(NP >= 2 && NP <= kItemPages && (NP & (NP - 1)) == 0, "pages per sub-chunk");
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16* sK = (_Float16*)smem;                  // [CH][DH], segment-swizzled
+  _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], 8-byte-unit-swizzled
+
+  ConstItem* ip = (ConstItem*)a.items + blockIdx.x;
+  const int kdr = ip->k;
+  if (kdr < 0) return;  // grid padding
+  const int slot = ip->slot, ctx = ip->ctx, cu = ip->cu, g = ip->g;
+  const int nch = ip->nch, rg = ip->rg, part = ip->part;
+  const int p_begin = ip->p_begin, p_end = ip->p_end;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.group;
-  const int R = (it.k + 1) * G;
-  const int p_begin = it.p_begin;
-  const int p_end = it.p_end;
+  const int R = (kdr + 1) * G;
   const int lg = lane >> 4;
   const size_t vhalf = (size_t)a.Hkv * kPage * DH;
+  const _Float16* kvg = a.kv + (size_t)g * kPage * DH;  // this kv head's K block in a page
+  ConstI32* ptrow = (ConstI32*)a.pt + (size_t)slot * a.pt_stride;
 
   // per-wave state of its (up to) two 16-row tiles, kept across sub-chunks
   int tile_row[2];
@@ -54,18 +70,9 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
   f32x4 o[2][DH / 16];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const int row_base = it.rg * 128 + (wave + 4 * q) * 16;
+    const int row_base = rg * 128 + (wave + 4 * q) * 16;
     tile_on[q] = row_base < R;
     tile_row[q] = row_base + (lane & 15);
-    const int r = tile_row[q];
-    const bool rvalid = r < R;
-    const int i = rvalid ? r / G : it.k;
-    const int h = it.g * G + (rvalid ? r % G : 0);
-#pragma unroll
-    for (int kd = 0; kd < DH / 32; ++kd)
-      qf[q][kd] = (tile_on[q] && rvalid)
-                      ? *(const f16x8*)(a.Q + ((size_t)(it.cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8)
-                      : f16x8{0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int d = 0; d < DH / 16; ++d) o[q][d] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -73,66 +80,78 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
   for (int sub = p_begin; sub < p_end; sub += CH) {
     const int n_pos = min(CH, p_end - sub);
     const int n_pages = (n_pos + kPage - 1) / kPage;
-    if (sub != p_begin) __syncthreads();  // previous sub-chunk fully consumed
-    if (tid < n_pages) spg[tid] = a.pt[(size_t)it.slot * a.pt_stride + (sub >> 4) + tid];
-    __syncthreads();
-    // ---- stage K and V of the sub-chunk into LDS (all loads issued before any use)
-    {
-      constexpr int K_UNITS = CH * KSEG;              // 16-byte units of K
-      constexpr int V_UNITS = CH / kPage * DH * 2;    // 16-byte units of V (2 per d row per page)
-      constexpr int PER = (K_UNITS + V_UNITS) / 256;
-      uint4 buf[PER];
+    // pool page of each staged page; pages past the sub-chunk's end repeat
+    // its first page (in-bounds, cached; their V is zeroed below)
+    int pgid[NP];
+    if (sub == p_begin) {
 #pragma unroll
-      for (int j = 0; j < PER; ++j) {
+      for (int p = 0; p < NP; ++p) pgid[p] = ip->pages[p];
+    } else {
+#pragma unroll
+      for (int p = 0; p < NP; ++p) pgid[p] = ptrow[(sub >> 4) + (p < n_pages ? p : 0)];
+      __syncthreads();  // previous sub-chunk fully consumed
+    }
+    // ---- all K/V loads of the sub-chunk in flight at once (page-major:
+    // per page, units [0, 2DH) are K rows, [2DH, 4DH) V rows of the head)
+    u32x4 buf[NP][LPP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int j = 0; j < LPP; ++j) {
         const int u = j * 256 + tid;
-        const bool isk = u < K_UNITS;
-        const int v = u - K_UNITS;
-        const int page_i = isk ? u / (kPage * KSEG) : v / (DH * 2);
-        const int off = isk ? u % (kPage * KSEG) : v % (DH * 2);  // K: t*KSEG + s; V: d*2 + half
-        buf[j] = uint4{0, 0, 0, 0};
-        if (page_i < n_pages) {
-          const int pg = spg[page_i];
-          const _Float16* base = a.kv + (size_t)pg * a.page_stride +
-                                 (isk ? (size_t)it.g * kPage * DH : vhalf + (size_t)it.g * DH * kPage);
-          buf[j] = *(const uint4*)(base + (size_t)off * 8);
-        }
+        const size_t off = u < 2 * DH ? (size_t)u * 8 : vhalf + (size_t)(u - 2 * DH) * 8;
+        buf[p][j] = *(const u32x4*)(kvg + (size_t)pgid[p] * a.page_stride + off);
       }
+    if (sub == p_begin) {
+      // query fragments (rows past R read a valid row; their results are dropped)
 #pragma unroll
-      for (int j = 0; j < PER; ++j) {
+      for (int q = 0; q < 2; ++q) {
+        const int r = tile_row[q];
+        const int i = r < R ? r / G : kdr;
+        const int h = g * G + (r < R ? r % G : 0);
+#pragma unroll
+        for (int kd = 0; kd < DH / 32; ++kd)
+          qf[q][kd] = *(const f16x8*)(a.Q + ((size_t)(cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int j = 0; j < LPP; ++j) {
         const int u = j * 256 + tid;
-        if (u < K_UNITS) {
-          const int page_i = u / (kPage * KSEG), off = u % (kPage * KSEG);
-          const int t = off / KSEG, sgm = off % KSEG;
-          const int p = page_i * kPage + t;
-          *(uint4*)(sK + p * DH + ((sgm ^ (p & 15)) & (KSEG - 1)) * 8) = buf[j];
+        u32x4 x = buf[p][j];
+        if (u < 2 * DH) {
+          const int t = u / KSEG, sgm = u % KSEG;
+          const int pos = p * kPage + t;
+          *(u32x4*)(sK + pos * DH + ((sgm ^ (pos & 15)) & (KSEG - 1)) * 8) = x;
         } else {
-          const int v = u - K_UNITS;
-          const int page_i = v / (DH * 2), off = v % (DH * 2);
-          const int d = off >> 1, hh = off & 1;
-          // 8 positions page_i*16 + hh*8 .. +7 of row d; zero positions past the end
-          uint4 x = buf[j];
-          const int pp = page_i * kPage + hh * 8;
-          if (pp + 8 > n_pos) {
-            uint16_t* e = (uint16_t*)&x;
+          const int v = u - 2 * DH;
+          const int d = v >> 1, hh = v & 1;
+          // 8 positions pp .. pp+7 of row d; zero positions past the end
+          const int pp = p * kPage + hh * 8;
+          if (pp >= n_pos) {
+            x = u32x4{0u, 0u, 0u, 0u};
+          } else if (pp + 8 > n_pos) {
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-              if (pp + q >= n_pos) e[q] = 0;
+            for (int e = 0; e < 4; ++e) {
+              const uint32_t keep = (pp + 2 * e + 1 < n_pos) ? 0xffffffffu : (pp + 2 * e < n_pos ? 0xffffu : 0u);
+              x[e] &= keep;
+            }
           }
           const int u0 = pp >> 2;  // 8-byte units (4 positions)
           uint2* row = (uint2*)(sV + (size_t)d * CH);
-          row[(u0 & ~15) | ((u0 & 15) ^ (d & 15))] = uint2{x.x, x.y};
-          row[((u0 + 1) & ~15) | (((u0 + 1) & 15) ^ (d & 15))] = uint2{x.z, x.w};
+          row[(u0 & ~(VM - 1)) | ((u0 & (VM - 1)) ^ (d & (VM - 1)))] = uint2{x[0], x[1]};
+          row[((u0 + 1) & ~(VM - 1)) | (((u0 + 1) & (VM - 1)) ^ (d & (VM - 1)))] = uint2{x[2], x[3]};
         }
       }
-    }
     __syncthreads();
 
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       if (!tile_on[q]) continue;
       const int r = tile_row[q];
-      const int i = r < R ? r / G : it.k;
-      const int lim = it.ctx + i - sub;  // last visible position, sub-chunk-relative
+      const int i = r < R ? r / G : kdr;
+      const int lim = ctx + i - sub;  // last visible position, sub-chunk-relative
       for (int p0 = 0; p0 < n_pos; p0 += 32) {
         const bool has1 = p0 + 16 < n_pos;
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -186,8 +205,8 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
           o[q][dt] *= alpha;
           const int d = dt * 16 + (lane & 15);
           const uint2* row = (const uint2*)(sV + (size_t)d * CH);
-          const uint2 va = row[(ua & ~15) | ((ua & 15) ^ (d & 15))];
-          const uint2 vb = has1 ? row[(ub & ~15) | ((ub & 15) ^ (d & 15))] : uint2{0, 0};
+          const uint2 va = row[(ua & ~(VM - 1)) | ((ua & (VM - 1)) ^ (d & (VM - 1)))];
+          const uint2 vb = has1 ? row[(ub & ~(VM - 1)) | ((ub & (VM - 1)) ^ (d & (VM - 1)))] : uint2{0, 0};
           const u32x4 vv = {va.x, va.y, vb.x, vb.y};
           o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf, o[q][dt]);
         }
@@ -203,11 +222,11 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
     l += __shfl_xor(l, 32);
     const int r = tile_row[q];
     const bool rvalid = r < R;
-    if (it.nch == 1) {
+    if (nch == 1) {
       if (rvalid) {
-        const int i = r / G, h = it.g * G + r % G;
+        const int i = r / G, h = g * G + r % G;
         const float inv = l > 0.f ? 1.f / l : 0.f;
-        const int row = it.cu + i;
+        const int row = cu + i;
 #pragma unroll
         for (int dt = 0; dt < DH / 16; ++dt) {
           const int col = h * DH + dt * 16 + lg * 4;
@@ -221,23 +240,26 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
       }
     } else {
       const int lr = (wave + 4 * q) * 16 + (lane & 15);
-      const size_t slot = (size_t)it.part * 128 + lr;
+      const size_t ps = (size_t)part * 128 + lr;
 #pragma unroll
       for (int dt = 0; dt < DH / 16; ++dt)
-        *(float4*)(a.part_o + slot * DH + dt * 16 + lg * 4) =
+        *(float4*)(a.part_o + ps * DH + dt * 16 + lg * 4) =
             float4{o[q][dt][0], o[q][dt][1], o[q][dt][2], o[q][dt][3]};
-      if (lg == 0) *(float2*)(a.part_ml + slot * 2) = float2{m[q], l};
+      if (lg == 0) *(float2*)(a.part_ml + ps * 2) = float2{m[q], l};
     }
   }
 }
 
 // Merge the chunk partials of one (sequence, kv head, row group) in chunk
-// order: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c.  One block per
-// (head entry, 16-row slice); one thread per (row, 8 output dims).
+// order: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, as a running
+// (M, L, acc) merge over batches of 8 chunks whose loads are all issued
+// before any is used (the merge is latency-bound).  One block per (head
+// entry, 16-row slice); one thread per (row, 8 output dims).
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   constexpr int OCT = DH / 8;
   constexpr int RPB = 256 / OCT;  // rows per block
+  constexpr int NB = 8;           // chunks per batch
   const AttnItem hd = a.heads[blockIdx.x / (128 / RPB)];
   if (hd.k < 0) return;  // grid padding
   const int slice = blockIdx.x % (128 / RPB);
@@ -249,18 +271,37 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   const float* ml = a.part_ml + ((size_t)hd.part * 128 + lr) * 2;
   const float* po = a.part_o + ((size_t)hd.part * 128 + lr) * DH + o8;
   const size_t cstride_ml = (size_t)128 * 2, cstride_o = (size_t)128 * DH;
-  float M = -INFINITY;
-  for (int c = 0; c < hd.nch; ++c) M = fmaxf(M, ml[c * cstride_ml]);
-  float L = 0.f, acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll 4
-  for (int c = 0; c < hd.nch; ++c) {
-    const float mc = ml[c * cstride_ml], lc = ml[c * cstride_ml + 1];
-    const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - M);
-    L += w * lc;
-    const float4 x0 = *(const float4*)(po + c * cstride_o);
-    const float4 x1 = *(const float4*)(po + c * cstride_o + 4);
-    acc[0] += w * x0.x; acc[1] += w * x0.y; acc[2] += w * x0.z; acc[3] += w * x0.w;
-    acc[4] += w * x1.x; acc[5] += w * x1.y; acc[6] += w * x1.z; acc[7] += w * x1.w;
+  float M = -INFINITY, L = 0.f;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int c0 = 0; c0 < hd.nch; c0 += NB) {
+    float2 mlc[NB];
+    float4 x0[NB], x1[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int c = c0 + j;
+      mlc[j] = float2{-INFINITY, 0.f};
+      x0[j] = x1[j] = float4{0.f, 0.f, 0.f, 0.f};
+      if (c < hd.nch) {
+        mlc[j] = *(const float2*)(ml + c * cstride_ml);
+        x0[j] = *(const float4*)(po + c * cstride_o);
+        x1[j] = *(const float4*)(po + c * cstride_o + 4);
+      }
+    }
+    float Mn = M;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) Mn = fmaxf(Mn, mlc[j].x);
+    const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mn);
+    L *= sc;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] *= sc;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float w = (mlc[j].x == -INFINITY) ? 0.f : exp2f(mlc[j].x - Mn);
+      L += w * mlc[j].y;
+      acc[0] += w * x0[j].x; acc[1] += w * x0[j].y; acc[2] += w * x0[j].z; acc[3] += w * x0[j].w;
+      acc[4] += w * x1[j].x; acc[5] += w * x1[j].y; acc[6] += w * x1[j].z; acc[7] += w * x1[j].w;
+    }
+    M = Mn;
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
   const int i = r / G, h = hd.g * G + r % G;
@@ -274,18 +315,33 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
                                  lo[4] | ((uint32_t)lo[5] << 16), lo[6] | ((uint32_t)lo[7] << 16)};
 }
 
-size_t attn_lds_bytes(int dh) { return (size_t)kAttnChunk * dh * 2 * 2; }
+int attn_pages_per_sub(int chunk) {
+  int np = 2;
+  while (np < kItemPages && np * kPage < chunk) np *= 2;
+  return np;
+}
 
-hipError_t launch_attn(const AttnArgs& a, int n_items, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  const size_t lds = attn_lds_bytes(a.dh);
-  if (a.dh == 128)
-    hipLaunchKernelGGL(verify_attn<128>, dim3(n_items), dim3(256), lds, s, a);
-  else if (a.dh == 64)
-    hipLaunchKernelGGL(verify_attn<64>, dim3(n_items), dim3(256), lds, s, a);
-  else
-    return hipErrorInvalidValue;
+size_t attn_lds_bytes(int dh, int np) { return (size_t)np * kPage * dh * 2 * 2; }
+
+template <int DH>
+static hipError_t launch_attn_dh(const AttnArgs& a, int n_items, int np, hipStream_t s) {
+  const size_t lds = attn_lds_bytes(DH, np);
+  switch (np) {
+    case 2: hipLaunchKernelGGL((verify_attn<DH, 2>), dim3(n_items), dim3(256), lds, s, a); break;
+    case 4: hipLaunchKernelGGL((verify_attn<DH, 4>), dim3(n_items), dim3(256), lds, s, a); break;
+    case 8: hipLaunchKernelGGL((verify_attn<DH, 8>), dim3(n_items), dim3(256), lds, s, a); break;
+    case 16: hipLaunchKernelGGL((verify_attn<DH, 16>), dim3(n_items), dim3(256), lds, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
+}
+
+hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  const int np = attn_pages_per_sub(chunk);
+  if (a.dh == 128) return launch_attn_dh<128>(a, n_items, np, s);
+  if (a.dh == 64) return launch_attn_dh<64>(a, n_items, np, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s) {
@@ -299,12 +355,23 @@ hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int DH, int NP>
+static hipError_t set_lds(void) {
+  return hipFuncSetAttribute((const void*)verify_attn<DH, NP>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)attn_lds_bytes(DH, NP));
+}
+
 hipError_t attn_set_lds_limit() {
-  hipError_t e = hipFuncSetAttribute((const void*)verify_attn<128>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)attn_lds_bytes(128));
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)verify_attn<64>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)attn_lds_bytes(64));
+  hipError_t e = hipSuccess;
+  if (e == hipSuccess) e = set_lds<128, 2>();
+  if (e == hipSuccess) e = set_lds<128, 4>();
+  if (e == hipSuccess) e = set_lds<128, 8>();
+  if (e == hipSuccess) e = set_lds<128, 16>();
+  if (e == hipSuccess) e = set_lds<64, 2>();
+  if (e == hipSuccess) e = set_lds<64, 4>();
+  if (e == hipSuccess) e = set_lds<64, 8>();
+  if (e == hipSuccess) e = set_lds<64, 16>();
+  return e;
 }
 
 }  // namespace hvd

@@ -18,17 +18,22 @@ struct RowMeta {
 struct SeqMeta {
   int32_t slot, ctx, k, cu;
 };
-// One attention work item, self-contained so a workgroup needs one scalar
-// load: sequence slot, cached length ctx, draft length k, first row cu; kv
-// head g; KV chunk c of nch covering positions [p_begin, p_end); the row
-// group rg (rows [rg*128, rg*128+128) of the (k+1)*group query rows); and,
-// for multi-chunk items, the partial slot `part` (combine heads: first slot).
+// One attention work item, self-contained so a workgroup needs no other
+// metadata: sequence slot, cached length ctx, draft length k, first row cu;
+// kv head g; KV chunk c of nch covering positions [p_begin, p_end); the row
+// group rg (rows [rg*128, rg*128+128) of the (k+1)*group query rows); for
+// multi-chunk items, the partial slot `part` (combine heads: first slot); and
+// the pool pages holding the first kAttnChunk positions of the chunk, so the
+// KV loads need not wait for a page-table read.
+constexpr int kItemPages = 16;  // kAttnChunk / kPage
 struct AttnItem {
   int32_t slot, ctx, k, cu;
   int32_t g, c, nch, rg;
   int32_t part, p_begin, p_end, pad0;
   int32_t pad1, pad2, pad3, pad4;
+  int32_t pages[kItemPages];
 };
+static_assert(kItemPages * kPage == kAttnChunk, "item page list covers one LDS sub-chunk");
 
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_LM = 3 };
 
@@ -133,7 +138,8 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 // ns: 16-column strips per workgroup (1, 2, 4; >= 2 for EPI_SILU); grid.x = NT / ns.
 // splits > 1 splits K across workgroups and adds the gemm_finish pass.
 hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, hipStream_t s);
-hipError_t launch_attn(const AttnArgs& a, int n_items, hipStream_t s);
+// chunk: the plan's KV chunk length (picks the pages staged per sub-chunk)
+hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, hipStream_t s);
 hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
