@@ -581,8 +581,10 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   return true;
 }
 
-hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vector<RowMeta>& rows, bool lm_head,
+hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<RowMeta> rows, bool lm_head,
                    float* logits) {
+  // each row's K/V page (the QKV epilogue writes K/V there)
+  for (RowMeta& r : rows) r.page = k->hs->seq(r.slot).pages[(size_t)(r.pos / kPage)];
   hvd_model_s* m = k->m;
   const hvd_config& c = m->cfg;
   hipStream_t s = k->stream;
@@ -674,19 +676,25 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, const std::vec
   const int mt_block = std::min(MT, kGemmMaxMT);
   const int mblocks = (MT + mt_block - 1) / mt_block;
   // Workgroup shape per GEMM (measured on the 8B verify shapes): 4 strips
-  // per workgroup when that alone gives enough workgroups; for long-K GEMMs
-  // 4 strips plus a K split; otherwise 2 strips, K-split if still too few.
+  // per workgroup when that alone gives enough workgroups (8 for two row
+  // tiles, which halves the activation fragments per weight byte); for
+  // long-K GEMMs 4 strips plus a K split; otherwise 2 strips, K-split if
+  // still too few.
   int lm_parts = 0;
   auto gemm = [&](int epi, GemmArgs& a, int N, int K, int family) -> hvd_status {
     a.KT = K / 32;
     a.NT = N / 16;
+    a.wg = (size_t)a.KT * 256;  // pack_weight's layout: 4-strip groups, K steps contiguous
+    a.wk = 256;
     a.MTtot = MT;
     a.M = M;
     a.part = k->gemm_part;
     const int want = k->gemm_min_blocks;
-    const int nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
+    const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
     int ns = 4, splits = 1;
-    if (nb4 >= want) {
+    if (mt_block == 2 && N % 128 == 0 && nb8 >= want) {
+      ns = 8;
+    } else if (nb4 >= want) {
       ns = 4;
     } else if (a.KT >= kGemmLongK) {
       ns = 4;

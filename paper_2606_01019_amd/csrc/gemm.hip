@@ -38,6 +38,8 @@ namespace hvd {
 // Prefetch depth: K steps in flight per wave.  A stage holds NS weight and
 // 2*MT activation fragments (4 VGPRs each); up to 2 row tiles the kernel is
 // sized for 4 waves per SIMD (two 8-wave workgroups per CU), beyond that 2.
+// (A one-workgroup-per-CU variant with a 16-stage queue measured no faster:
+// these launches are not limited by weight bytes in flight.)
 constexpr int gemm_occupancy(int MT) { return MT <= 2 ? 4 : 2; }
 constexpr int gemm_depth(int MT, int NS) {
   const int budget = gemm_occupancy(MT) == 4 ? 80 : 160;
@@ -47,7 +49,7 @@ constexpr int gemm_depth(int MT, int NS) {
 
 constexpr int kKG = 8;  // waves per workgroup, each a contiguous K range
 
-// Epilogue inputs staged in LDS before the main loop.
+// Epilogue inputs staged in LDS for the epilogue.
 template <int MT, int NS, int EPI>
 struct EpiPre {
   static constexpr int ROWS = MT * 16, COLS = NS * 16;
@@ -59,74 +61,178 @@ struct EpiPre {
   int pos[EPI == EPI_QKV ? ROWS : 1];
 };
 
+// The same inputs on their way in, held in registers.  epi_issue() requests
+// them before the first weight stage (memory returns in order, so a wait for
+// them never waits for a weight stage), epi_commit() writes them to LDS
+// while the first stages are still in flight.  Rotary factors depend on the
+// row positions: epi_issue_rope() requests them after the first stages and
+// epi_commit_rope() stores them after the main loop.  Every load reads a
+// valid address (indices past the block are clamped and their values
+// dropped), so no load sits under a branch.
 template <int MT, int NS, int EPI>
-__device__ __forceinline__ void gemm_prefetch(const GemmArgs& a, EpiPre<MT, NS, EPI>& p, int cb, int mt0,
-                                              int mcount) {
-  constexpr int ROWS = MT * 16, COLS = NS * 16;
+struct EpiRegs {
+  static constexpr int ROWS = MT * 16, COLS = NS * 16;
+  static constexpr bool NORM = EPI != EPI_RESID;  // GEMM input is RMS-normalised
+  static constexpr int TPR = ROWS <= 16 ? 32 : ROWS <= 32 ? 16 : 8;  // threads per row of sums of squares
+  static constexpr int SSQ = 4;  // float4 of sums of squares per thread held here (more: read late)
+  static constexpr int XQ = EPI == EPI_RESID ? (ROWS * COLS / 4 + 511) / 512 : 1;
+  static constexpr int RQ = EPI == EPI_QKV ? (ROWS * COLS / 2 + 511) / 512 : 1;
+  // rotary factors ride along the main loop only for small row blocks
+  // (larger ones are short of registers: they request them after it)
+  static constexpr bool EARLY_ROPE = MT <= 2;
+  float4 ss[NORM ? SSQ : 1];
+  float4 x[XQ];
+  float gain;
+  RowMeta rm;
+  int rpos[RQ];
+  float2 rope[RQ];
+};
+
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void epi_issue(const GemmArgs& a, EpiRegs<MT, NS, EPI>& e, int cb, int mt0, int mcount) {
+  using E = EpiRegs<MT, NS, EPI>;
+  constexpr int COLS = E::COLS;
   const int tid = threadIdx.x;
   const int row0 = mt0 * 16, col0 = cb * COLS, rows_here = mcount * 16;
-  // inverse RMS of the block's rows from per-16-column sums of squares,
-  // summed in a fixed order (rows past the last tile get 1/sqrt(eps))
-  if (a.ss != nullptr) {
-    // TPR threads per row, each summing float4 groups q = j, j+TPR, ... of
-    // the row's ss_n entries, four loads in flight per round
-    constexpr int TPR = (512 / ROWS) >= 32 ? 32 : (512 / ROWS) >= 16 ? 16 : (512 / ROWS) >= 8 ? 8 : 4;
-    const int r = tid / TPR, j = tid % TPR;
-    if (r < ROWS) {
-      float sacc = 0.f;
-      if (r < rows_here) {
-        const float4* srow = (const float4*)(a.ss + (size_t)(row0 + r) * a.ss_n);
-        const int nq = a.ss_n >> 2;
-        for (int q0 = j; q0 < nq; q0 += 4 * TPR) {
-          float4 v[4];
+  if constexpr (E::NORM) {
+    const int r = tid / E::TPR, j = tid % E::TPR;
+    const float4* srow = (const float4*)(a.ss + (size_t)(row0 + (r < rows_here ? r : 0)) * a.ss_n);
+    const int nq = a.ss_n >> 2;
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            v[q] = (q0 + q * TPR < nq) ? srow[q0 + q * TPR] : float4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int q = 0; q < 4; ++q) sacc += (v[q].x + v[q].y) + (v[q].z + v[q].w);
-        }
-      }
-#pragma unroll
-      for (int o = TPR / 2; o > 0; o >>= 1) sacc += __shfl_xor(sacc, o);
-      if (j == 0) p.inv_rms[r] = rsqrtf(sacc * a.inv_dim + a.eps);
+    for (int i = 0; i < E::SSQ; ++i) {
+      const int q = j + i * E::TPR;
+      e.ss[i] = srow[q < nq ? q : 0];
     }
+  }
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int i = 0; i < E::XQ; ++i) {
+      int el = tid + i * 512;
+      if (el >= rows_here * (COLS / 4)) el = 0;
+      const int r = el / (COLS / 4), c4 = (el % (COLS / 4)) * 4;
+      e.x[i] = *(const float4*)(a.X + (size_t)(row0 + r) * a.D + col0 + c4);
+    }
+    e.gain = a.gain_next[col0 + (tid < COLS ? tid : 0)];
+  }
+  if constexpr (EPI == EPI_QKV) {
+    const int last = a.M - 1;
+    e.rm = a.rows[min(row0 + min(tid, rows_here - 1), last)];
+#pragma unroll
+    for (int i = 0; i < E::RQ; ++i) {
+      int el = tid + i * 512;
+      if (el >= rows_here * (COLS / 2)) el = 0;
+      e.rpos[i] = a.rows[min(row0 + el / (COLS / 2), last)].pos;
+    }
+  }
+}
+
+// Marks the point from which the epilogue inputs may be used: the compiler
+// sees new values here, so it can neither fold them into work placed
+// before the weight stream nor wait for them earlier.
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void epi_settle(EpiRegs<MT, NS, EPI>& e) {
+  using E = EpiRegs<MT, NS, EPI>;
+  if constexpr (E::NORM) {
+#pragma unroll
+    for (int i = 0; i < E::SSQ; ++i) asm volatile("" : "+v"(e.ss[i].x), "+v"(e.ss[i].y), "+v"(e.ss[i].z), "+v"(e.ss[i].w));
+  }
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int i = 0; i < E::XQ; ++i) asm volatile("" : "+v"(e.x[i].x), "+v"(e.x[i].y), "+v"(e.x[i].z), "+v"(e.x[i].w));
+    asm volatile("" : "+v"(e.gain));
+  }
+  if constexpr (EPI == EPI_QKV) {
+    asm volatile("" : "+v"(e.rm.pos), "+v"(e.rm.page));
+#pragma unroll
+    for (int i = 0; i < E::RQ; ++i) asm volatile("" : "+v"(e.rpos[i]));
+  }
+}
+
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void epi_issue_rope(const GemmArgs& a, EpiRegs<MT, NS, EPI>& e, int cb) {
+  if constexpr (EPI == EPI_QKV) {
+    using E = EpiRegs<MT, NS, EPI>;
+    constexpr int COLS = E::COLS;
+    const int col0 = cb * COLS;
+    const bool rotated = col0 < a.q_cols + a.kv_cols;  // block holds q or k columns
+    const int half = a.dh >> 1;
+#pragma unroll
+    for (int i = 0; i < E::RQ; ++i) {
+      const int cp = (threadIdx.x + i * 512) % (COLS / 2);
+      const int C = col0 + 2 * cp;
+      const int base = C < a.q_cols ? 0 : a.q_cols;
+      const int j = rotated ? ((C - base) % a.dh) >> 1 : 0;
+      e.rope[i] = a.rope[(size_t)e.rpos[i] * half + j];
+    }
+  }
+}
+
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void epi_commit(const GemmArgs& a, const EpiRegs<MT, NS, EPI>& e,
+                                           EpiPre<MT, NS, EPI>& p, int cb, int mt0, int mcount) {
+  using E = EpiRegs<MT, NS, EPI>;
+  constexpr int ROWS = E::ROWS, COLS = E::COLS;
+  const int tid = threadIdx.x;
+  const int row0 = mt0 * 16, rows_here = mcount * 16;
+  if constexpr (E::NORM) {
+    // inverse RMS from per-16-column sums of squares, summed in a fixed order
+    const int r = tid / E::TPR, j = tid % E::TPR;
+    const int nq = a.ss_n >> 2;
+    float sacc = 0.f;
+#pragma unroll
+    for (int i = 0; i < E::SSQ; ++i) {
+      const float4 v = e.ss[i];
+      if (j + i * E::TPR < nq) sacc += (v.x + v.y) + (v.z + v.w);
+    }
+    if (nq > E::SSQ * E::TPR) {  // wide rows: the rest is read here
+      const float4* srow = (const float4*)(a.ss + (size_t)(row0 + (r < rows_here ? r : 0)) * a.ss_n);
+      for (int q = j + E::SSQ * E::TPR; q < nq; q += E::TPR) {
+        const float4 v = srow[q];
+        sacc += (v.x + v.y) + (v.z + v.w);
+      }
+    }
+#pragma unroll
+    for (int o = E::TPR / 2; o > 0; o >>= 1) sacc += __shfl_xor(sacc, o);
+    if (j == 0 && r < ROWS) p.inv_rms[r] = r < rows_here ? rsqrtf(sacc * a.inv_dim + a.eps) : 1.f;
   } else if (tid < ROWS) {
     p.inv_rms[tid] = 1.f;
   }
   if constexpr (EPI == EPI_RESID) {
-    for (int e = tid; e < rows_here * (COLS / 4); e += 512) {
-      const int r = e / (COLS / 4), c4 = (e % (COLS / 4)) * 4;
-      const float4 v = *(const float4*)(a.X + (size_t)(row0 + r) * a.D + col0 + c4);
-      p.x[r][c4] = v.x;
-      p.x[r][c4 + 1] = v.y;
-      p.x[r][c4 + 2] = v.z;
-      p.x[r][c4 + 3] = v.w;
+#pragma unroll
+    for (int i = 0; i < E::XQ; ++i) {
+      const int el = tid + i * 512;
+      if (el < rows_here * (COLS / 4)) {
+        const int r = el / (COLS / 4), c4 = (el % (COLS / 4)) * 4;
+        p.x[r][c4] = e.x[i].x;
+        p.x[r][c4 + 1] = e.x[i].y;
+        p.x[r][c4 + 2] = e.x[i].z;
+        p.x[r][c4 + 3] = e.x[i].w;
+      }
     }
-    if (tid < COLS) p.gain[tid] = a.gain_next[col0 + tid];
+    if (tid < COLS) p.gain[tid] = e.gain;
   }
   if constexpr (EPI == EPI_QKV) {
-    const bool rotated = col0 < a.q_cols + a.kv_cols;  // block holds q or k columns
-    const bool cached = col0 + COLS > a.q_cols;        // block holds k or v columns
-    const int half = a.dh >> 1;
-    for (int e = tid; e < rows_here; e += 512) {
-      const int R = row0 + e;
-      int pos = 0, page = 0;
-      if (R < a.M) {
-        const RowMeta rm = a.rows[R];
-        pos = rm.pos;
-        if (cached) page = a.pt[(size_t)rm.slot * a.pt_stride + (rm.pos >> 4)];
-      }
-      p.pos[e] = pos;
-      p.page[e] = page;
+    if (tid < rows_here) {
+      const bool ok = row0 + tid < a.M;
+      p.pos[tid] = ok ? e.rm.pos : 0;
+      p.page[tid] = ok ? e.rm.page : 0;
     }
-    if (rotated) {
-      for (int e = tid; e < rows_here * (COLS / 2); e += 512) {
-        const int r = e / (COLS / 2), cp = e % (COLS / 2);
-        const int R = row0 + r;
-        const int C = col0 + 2 * cp;
-        const int base = C < a.q_cols ? 0 : a.q_cols;
-        const int j = ((C - base) % a.dh) >> 1;
-        p.rope[r][cp] = R < a.M ? a.rope[(size_t)a.rows[R].pos * half + j] : float2{1.f, 0.f};
+  }
+}
+
+template <int MT, int NS, int EPI>
+__device__ __forceinline__ void epi_commit_rope(const GemmArgs& a, const EpiRegs<MT, NS, EPI>& e,
+                                                EpiPre<MT, NS, EPI>& p, int mt0, int mcount) {
+  if constexpr (EPI == EPI_QKV) {
+    using E = EpiRegs<MT, NS, EPI>;
+    constexpr int COLS = E::COLS;
+    const int rows_here = mcount * 16;
+#pragma unroll
+    for (int i = 0; i < E::RQ; ++i) {
+      const int el = threadIdx.x + i * 512;
+      if (el < rows_here * (COLS / 2)) {
+        const int r = el / (COLS / 2), cp = el % (COLS / 2);
+        p.rope[r][cp] = mt0 * 16 + r < a.M ? e.rope[i] : float2{1.f, 0.f};
       }
     }
   }
@@ -281,13 +387,14 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   const int mcount = min(MT, a.MTtot - mt0);
   const bool split = gridDim.y > 1;
 
-  // K range of this wave: the workgroup's share of K (split gridDim.y ways)
-  // divided kKG ways
+  // K steps of this wave: the workgroup's share of K (split gridDim.y ways),
+  // dealt round-robin to its kKG waves, so at any moment the workgroup reads
+  // one contiguous window of weights (kKG adjacent K steps) rather than kKG
+  // distant streams
   const int kts = (a.KT + gridDim.y - 1) / gridDim.y;
   const int wk0 = blockIdx.y * kts, wk1 = min(a.KT, wk0 + kts);
-  const int per = (wk1 - wk0 + kKG - 1) / kKG;
-  const int k0 = wk0 + wave * per;
-  const int k1 = min(wk1, k0 + per);
+  const int kb = wk0 + wave;
+  const int nsteps = kb < wk1 ? (wk1 - kb + kKG - 1) / kKG : 0;  // wave-uniform
 
   f32x4 acc[MT][NS];
 #pragma unroll
@@ -295,13 +402,12 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
 #pragma unroll
     for (int n = 0; n < NS; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // strip s, K step kt at ((s/4*KT + kt)*4 + s%4)*64: strip n of this
-  // block at wp[n] + kt*256
+  // strip n of this block, K step kt, at wp[n] + kt*wk
   const u32x4* wp[NS];
 #pragma unroll
   for (int n = 0; n < NS; ++n) {
     const int st = cb * NS + n;
-    wp[n] = (const u32x4*)a.W + ((size_t)(st >> 2) * a.KT * 4 + (st & 3)) * 64;
+    wp[n] = (const u32x4*)a.W + (size_t)(st >> 2) * a.wg + (size_t)(st & 3) * 64;
   }
   const size_t astride = (size_t)a.MTtot * 64;
   const u32x4* hp = (const u32x4*)a.Ahi + (size_t)mt0 * 64;
@@ -311,9 +417,10 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   // tiles past this block's last are read from the operand's padding and
   // computed, then dropped (no per-tile branches in the loop).
   u32x4 qb[U][NS], qh[U][MT], ql[U][MT];
-  auto load = [&](int u, int kt) __attribute__((always_inline)) {
+  auto load = [&](int u, int j) __attribute__((always_inline)) {
+    const int kt = kb + j * kKG;
 #pragma unroll
-    for (int n = 0; n < NS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)kt * 256 + lane);
+    for (int n = 0; n < NS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)kt * a.wk + lane);
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       qh[u][m] = hp[kt * astride + m * 64 + lane];
@@ -330,37 +437,44 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
       }
   };
 
-  const int nsteps = k1 - k0;  // wave-uniform
+  EpiRegs<MT, NS, EPI> er;
+  epi_issue<MT, NS, EPI>(a, er, cb, mt0, mcount);  // (a split block's copy goes unused)
   if (nsteps >= U) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) load(u, k0 + u);
-    if (!split) gemm_prefetch<MT, NS, EPI>(a, pre, cb, mt0, mcount);
-    int kt = k0;
+    for (int u = 0; u < U; ++u) load(u, u);
+    epi_settle<MT, NS, EPI>(er);
+    if constexpr (EpiRegs<MT, NS, EPI>::EARLY_ROPE) epi_issue_rope<MT, NS, EPI>(a, er, cb);
+    epi_commit<MT, NS, EPI>(a, er, pre, cb, mt0, mcount);
+    int j = 0;
     // steady state: every stage is consumed and refilled, no branches
-    for (; kt + 2 * U <= k1; kt += U) {
+    for (; j + 2 * U <= nsteps; j += U) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         consume(u);
-        load(u, kt + u + U);
+        load(u, j + u + U);
       }
     }
-    // tail: the U stages in flight hold kt..kt+U-1; fewer than U steps remain after them
-    const int rem = k1 - (kt + U);
+    // tail: the U stages in flight hold steps j..j+U-1; fewer than U remain after them
+    const int rem = nsteps - (j + U);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       consume(u);
-      if (u < rem) load(u, kt + U + u);
+      if (u < rem) load(u, j + U + u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
       if (u < rem) consume(u);
   } else {
-    if (!split) gemm_prefetch<MT, NS, EPI>(a, pre, cb, mt0, mcount);
-    for (int kt = k0; kt < k1; ++kt) {
-      load(0, kt);
+    epi_settle<MT, NS, EPI>(er);
+    if constexpr (EpiRegs<MT, NS, EPI>::EARLY_ROPE) epi_issue_rope<MT, NS, EPI>(a, er, cb);
+    epi_commit<MT, NS, EPI>(a, er, pre, cb, mt0, mcount);
+    for (int j = 0; j < nsteps; ++j) {
+      load(0, j);
       consume(0);
     }
   }
+  if constexpr (!EpiRegs<MT, NS, EPI>::EARLY_ROPE) epi_issue_rope<MT, NS, EPI>(a, er, cb);
+  epi_commit_rope<MT, NS, EPI>(a, er, pre, mt0, mcount);
 
   // ---- reduce the 8 K ranges through LDS in two rounds (fixed order)
   if (wave >= 4) {
@@ -402,22 +516,51 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
 
 // Second pass of a K-split GEMM: one workgroup per (column block, row block)
 // sums the splits' partial tiles in split order, then runs the epilogue.
+// All loads (epilogue inputs, then the partials, 8 splits per batch) are
+// requested before any is used.
 template <int MT, int NS, int EPI>
 __global__ __launch_bounds__(512) void gemm_finish(GemmArgs a, int splits) {
   constexpr int ROWS = MT * 16;
   constexpr int COLS = NS * 16;
+  constexpr int EPT = (ROWS * COLS + 511) / 512;  // tile entries per thread
+  constexpr int SB = 8;                           // splits per batch
   __shared__ float tile[ROWS][COLS + 1];
   __shared__ EpiPre<MT, NS, EPI> pre;
+  const int tid = threadIdx.x;
   const int cb = blockIdx.x;
   const int mt0 = blockIdx.z * MT;
   const int mcount = min(MT, a.MTtot - mt0);
+  const int n_el = mcount * 16 * COLS;
   const float* src = a.part + (size_t)(blockIdx.z * gridDim.x + cb) * splits * ROWS * COLS;
-  for (int e = threadIdx.x; e < mcount * 16 * COLS; e += 512) {
-    float v = 0.f;
-    for (int q = 0; q < splits; ++q) v += src[(size_t)q * ROWS * COLS + e];
-    tile[e / COLS][e % COLS] = v;
+  EpiRegs<MT, NS, EPI> er;
+  epi_issue<MT, NS, EPI>(a, er, cb, mt0, mcount);
+  float v[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) v[i] = 0.f;
+  for (int q0 = 0; q0 < splits; q0 += SB) {
+    float t[EPT][SB];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+#pragma unroll
+      for (int q = 0; q < SB; ++q) {
+        const int el = tid + i * 512;
+        t[i][q] = src[(size_t)(q0 + q < splits ? q0 + q : 0) * ROWS * COLS + (el < n_el ? el : 0)];
+      }
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+#pragma unroll
+      for (int q = 0; q < SB; ++q)
+        if (q0 + q < splits) v[i] += t[i][q];
   }
-  gemm_prefetch<MT, NS, EPI>(a, pre, cb, mt0, mcount);
+  epi_settle<MT, NS, EPI>(er);
+  epi_issue_rope<MT, NS, EPI>(a, er, cb);
+  epi_commit<MT, NS, EPI>(a, er, pre, cb, mt0, mcount);
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int el = tid + i * 512;
+    if (el < n_el) tile[el / COLS][el % COLS] = v[i];
+  }
+  epi_commit_rope<MT, NS, EPI>(a, er, pre, mt0, mcount);
   __syncthreads();
   gemm_epilogue<MT, NS, EPI>(a, tile, pre, cb, mt0, mcount);
 }
@@ -427,11 +570,16 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
   dim3 grid(a.NT / NS, splits, mblocks);
   dim3 fgrid(a.NT / NS, 1, mblocks);
   switch (mt) {
-#define HVD_CASE(X)                                                                                   \
-  case X:                                                                                             \
-    hipLaunchKernelGGL((gemm_skinny<X, NS, EPI>), grid, dim3(512), 0, s, a);                          \
-    if (splits > 1) hipLaunchKernelGGL((gemm_finish<X, NS, EPI>), fgrid, dim3(512), 0, s, a, splits); \
-    break;
+// (8-strip blocks only up to 2 row tiles: LDS)
+#define HVD_CASE(X)                                                                                     \
+  case X:                                                                                               \
+    if constexpr (NS * X <= 16) {                                                                       \
+      hipLaunchKernelGGL((gemm_skinny<X, NS, EPI>), grid, dim3(512), 0, s, a);                          \
+      if (splits > 1) hipLaunchKernelGGL((gemm_finish<X, NS, EPI>), fgrid, dim3(512), 0, s, a, splits); \
+      break;                                                                                            \
+    } else {                                                                                            \
+      return hipErrorInvalidValue;                                                                      \
+    }
     HVD_CASE(1) HVD_CASE(2) HVD_CASE(3) HVD_CASE(4)
 #undef HVD_CASE
     default: return hipErrorInvalidValue;
@@ -447,6 +595,7 @@ static hipError_t launch_epi(const GemmArgs& a, int ns, int splits, int mblocks,
       return hipErrorInvalidValue;
     case 2: return launch_ns<2, EPI>(a, splits, mblocks, mt, s);
     case 4: return launch_ns<4, EPI>(a, splits, mblocks, mt, s);
+    case 8: return launch_ns<8, EPI>(a, splits, mblocks, mt, s);
   }
   return hipErrorInvalidValue;
 }

@@ -9,9 +9,10 @@ namespace hvd {
 constexpr int kPage = 16;        // tokens per KV page
 constexpr int kAttnChunk = 256;  // most KV positions one attention workgroup stages in LDS
 
-// Row metadata of one forward: token, sequence slot, absolute position.
+// Row metadata of one forward: token, sequence slot, absolute position, and
+// the pool page holding that position's K/V.
 struct RowMeta {
-  int32_t tok, slot, pos, pad;
+  int32_t tok, slot, pos, page;
 };
 // Sequence metadata of one forward: slot, cached length, draft length k,
 // first row (rows cu .. cu+k).
@@ -38,7 +39,9 @@ static_assert(kItemPages * kPage == kAttnChunk, "item page list covers one LDS s
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_LM = 3 };
 
 struct GemmArgs {
-  const uint4* W;    // packed weights: strip s, K step kt at ((s/4*KT + kt)*4 + s%4)*64 lanes
+  const uint4* W;    // packed weights: 1 KB fragment of strip s, K step kt at
+                     // (s/4)*wg + (s%4)*64 + kt*wk (16-byte units)
+  size_t wg, wk;     // group and K-step strides of the packing (see pack_weight)
   const uint4* Ahi;  // packed activations (hi part), fragment (kt, mt) at (kt*MTtot + mt)*64
   const uint4* Alo;  // packed activations (lo part)
   int KT, NT, MTtot, M;
