@@ -86,7 +86,10 @@ size_t hvd_model_bytes(const hvd_config* cfg);
  *     wv [Hkv*dh, D], wo [D, Hq*dh], mlp_norm [D], wg [F, D], wu [F, D],
  *     wd [D, F];
  *   final_norm [D], lm_head [V, D].
- * Count = 3 + 9 * n_layers.  dev_buf (nullable) must hold hvd_model_bytes.
+ * Count = 3 + 9 * n_layers.  Matrices are stored on the device as fp16
+ * (exact for every bf16 value of magnitude >= 2^-17; smaller ones round with
+ * an error below 2^-25), the embedding and gains as given.
+ * dev_buf (nullable) must hold hvd_model_bytes.
  * stream is a hipStream_t (NULL = default stream).  Temporary staging memory
  * is allocated and freed inside the call. */
 hvd_status hvd_model_load(const hvd_config* cfg, const uint16_t* const* tensors, void* dev_buf,

@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
           const int col = h * DH + dt * 16 + lg * 4;
           uint16_t hi[4], lo[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) split_bf16(o[q][dt][j] * inv, hi[j], lo[j]);
+          for (int j = 0; j < 4; ++j) split_f16(o[q][dt][j] * inv, hi[j], lo[j]);
           const size_t off = afrag_off(row, col, a.MTtot);
           *(uint2*)(a.Ohi + off) = uint2{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16)};
           *(uint2*)(a.Olo + off) = uint2{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16)};
@@ -307,7 +307,7 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   const int i = r / G, h = hd.g * G + r % G;
   uint16_t hi[8], lo[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) split_bf16(acc[j] * inv, hi[j], lo[j]);
+  for (int j = 0; j < 8; ++j) split_f16(acc[j] * inv, hi[j], lo[j]);
   const size_t off = afrag_off(hd.cu + i, h * DH + o8, a.MTtot);
   *(uint4*)(a.Ohi + off) = uint4{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16),
                                  hi[4] | ((uint32_t)hi[5] << 16), hi[6] | ((uint32_t)hi[7] << 16)};

@@ -23,11 +23,16 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 }
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
-// Split v into hi + lo bf16 parts: hi = bf16(v), lo = bf16(v - hi).  hi + lo
-// carries about 16 significant bits of v.
-__device__ __forceinline__ void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
-  hi = f2bf(v);
-  lo = f2bf(v - bf2f(hi));
+// fp16 bits of v (round to nearest even) and back.
+__device__ __forceinline__ uint16_t f2h(float v) { return __builtin_bit_cast(uint16_t, (_Float16)v); }
+__device__ __forceinline__ float h2f(uint16_t b) { return (float)__builtin_bit_cast(_Float16, b); }
+
+// Split v into hi + lo fp16 parts: hi = fp16(v), lo = fp16(v - hi).  hi + lo
+// carries about 22 significant bits of v (fewer when lo is subnormal, where
+// its absolute error is below 3e-8).
+__device__ __forceinline__ void split_f16(float v, uint16_t& hi, uint16_t& lo) {
+  hi = f2h(v);
+  lo = f2h(v - h2f(hi));
 }
 
 // Offset (in halves) of element (row, col) inside a fragment-packed operand
@@ -39,9 +44,9 @@ __device__ __forceinline__ size_t afrag_off(int row, int col, int mtiles) {
   return ((size_t)(kt * mtiles + mt) * 64 + lane) * 8 + (col & 7);
 }
 
-__device__ __forceinline__ f32x4 mfma_bf16(const u32x4& a, const u32x4& b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+__device__ __forceinline__ f32x4 mfma_f16(const u32x4& a, const u32x4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 __device__ __forceinline__ f32x4 mfma_f16(const f16x8& a, const f16x8& b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);

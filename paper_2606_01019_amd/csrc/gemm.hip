@@ -1,14 +1,16 @@
-// Weight-streaming GEMMs of the verify forward (gfx950, MFMA 16x16x32 bf16).
+// Weight-streaming GEMMs of the verify forward (gfx950, MFMA 16x16x32 f16).
 //
-// Y[m, n] = sum_k A[m, k] * W[n, k] with W the bf16 weight in torch Linear
-// layout, pre-packed so that one 16x32 B-operand fragment is 1 KB contiguous
-// (one 16-byte load per lane), and A the activation carried as a hi + lo pair
-// of bf16 fragments (two MFMAs per tile: hi*W + lo*W keeps ~16 significant
-// bits of the fp32 activation; the MFMA pipe is idle in this HBM-bound regime).
+// Y[m, n] = sum_k A[m, k] * W[n, k] with W the weight in torch Linear layout
+// (bf16 values, stored as fp16: the conversion is exact but for magnitudes
+// below 2^-17), pre-packed so that one 16x32 B-operand fragment is 1 KB
+// contiguous (one 16-byte load per lane), and A the activation carried as a
+// hi + lo pair of fp16 fragments (two MFMAs per tile: hi*W + lo*W keeps ~22
+// significant bits of the fp32 activation; the MFMA pipe is idle in this
+// HBM-bound regime).
 //
 // Work split: a workgroup of 8 waves owns NS strips of 16 output columns
-// (NS = 1, 2 or 4, chosen per GEMM so the launch has enough workgroups) and
-// up to 64 rows; its waves split K into 8 contiguous pieces.  Each wave
+// (NS = 1, 2, 4 or 8, chosen per GEMM so the launch has enough workgroups)
+// and up to 64 rows; its waves take the K steps round-robin.  Each wave
 // streams the NS strips' weight fragments of a K step (the 4 strips of a
 // 64-column group are contiguous after packing) and reuses each activation
 // fragment for all NS strips, with a prefetch queue of depth U (weights and
@@ -303,7 +305,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[N
         for (int i = 0; i < 8; ++i) {
           xv[i] = p.x[r][o * 8 + i] + tile[r][o * 8 + i];
           sq += xv[i] * xv[i];
-          split_bf16(xv[i] * p.gain[o * 8 + i], hi[i], lo[i]);
+          split_f16(xv[i] * p.gain[o * 8 + i], hi[i], lo[i]);
         }
         float* xp = a.X + (size_t)R * a.D + C;
         *(float4*)xp = float4{xv[0], xv[1], xv[2], xv[3]};
@@ -329,7 +331,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[N
         const float g = tile[r][s_ * 32 + c8 + i] * p.inv_rms[r];
         const float u = tile[r][s_ * 32 + 16 + c8 + i] * p.inv_rms[r];
         const float act = g / (1.f + __expf(-g)) * u;
-        split_bf16(act, hi[i], lo[i]);
+        split_f16(act, hi[i], lo[i]);
       }
       const size_t off = afrag_off(R, F, a.MTtot);
       *(uint4*)(a.act_hi + off) = pack8(hi);
@@ -432,8 +434,8 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int n = 0; n < NS; ++n) {
-        acc[m][n] = mfma_bf16(qh[u][m], qb[u][n], acc[m][n]);
-        acc[m][n] = mfma_bf16(ql[u][m], qb[u][n], acc[m][n]);
+        acc[m][n] = mfma_f16(qh[u][m], qb[u][n], acc[m][n]);
+        acc[m][n] = mfma_f16(ql[u][m], qb[u][n], acc[m][n]);
       }
   };
 

@@ -7,7 +7,7 @@
 namespace hvd {
 
 // dst fragment (strip s, K step kt), lane l, half j =
-//   src[rowmap[16 s + l%16]][32 kt + 8 (l/16) + j]
+//   fp16(src[rowmap[16 s + l%16]][32 kt + 8 (l/16) + j])   (src bf16)
 // stored at ((s/4 * KT + kt) * 4 + s%4) * 512 halves: the 4 strips of a
 // 64-column block are contiguous for each K step.
 __global__ void pack_weight(const uint16_t* __restrict__ src, const int32_t* __restrict__ rowmap,
@@ -22,8 +22,15 @@ __global__ void pack_weight(const uint16_t* __restrict__ src, const int32_t* __r
     const int cb = (int)((frag >> 2) / KT);
     const int s = cb * 4 + ns;
     const int srow = rowmap[s * 16 + (l & 15)];
+    // bf16 -> fp16: exact except magnitudes below 2^-17 (fp16 subnormals),
+    // whose rounding error is below 2^-25
     const uint4 v = *(const uint4*)(src + (size_t)srow * K + kt * 32 + (l >> 4) * 8);
-    *(uint4*)(dst + t * 8) = v;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t h[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      h[j] = (uint32_t)f2h(bf2f((uint16_t)(w[j] & 0xFFFFu))) | ((uint32_t)f2h(bf2f((uint16_t)(w[j] >> 16))) << 16);
+    *(uint4*)(dst + t * 8) = uint4{h[0], h[1], h[2], h[3]};
   }
 }
 
@@ -36,7 +43,7 @@ hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst
 }
 
 // One block per (padded) row: X = fp32(E[tok]), the first norm's operand
-// bf16 split of X * gain, per-16-column sums of squares.  Block 0 first
+// fp16 hi/lo split of X * gain, per-16-column sums of squares.  Block 0 first
 // applies this step's page-table updates.
 __global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
   if (blockIdx.x == 0)
@@ -69,7 +76,7 @@ __global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         sq += x[j] * x[j];
-        split_bf16(x[j] * a.gain[C + j], hi[j], lo[j]);
+        split_f16(x[j] * a.gain[C + j], hi[j], lo[j]);
       }
       const size_t off = afrag_off(R, C, a.MTtot);
       *(uint4*)(a.Nhi + off) = uint4{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16),
