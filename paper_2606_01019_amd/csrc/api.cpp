@@ -319,6 +319,8 @@ struct hvd_kv_s {
   std::map<GraphKey, hipGraphExec_t> graphs;
   int attn_min_items = kAttnMinItems;
   float* gemm_part = nullptr;
+  float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
+  bool mlp_single = false;   // large-batch MLP GEMMs on the hi activation part only
   int32_t* g = nullptr;
   int32_t* out = nullptr;
   uint32_t* counter = nullptr;
@@ -379,6 +381,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->lm_val = cv.take<float>(Mp * k->n_part_lm);
   k->lm_idx = cv.take<int32_t>(Mp * k->n_part_lm);
   k->gemm_part = cv.take<float>(kGemmPartBytes / 4);
+  k->inv_rms = cv.take<float>(Mp);
   k->g = cv.take<int32_t>(Mp);
   k->out = cv.take<int32_t>(2 * (size_t)max_seqs);
   k->counter = cv.take<uint32_t>(64);
@@ -690,6 +693,25 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.M = M;
     a.part = k->gemm_part;
     const int want = k->gemm_min_blocks;
+    if (MT > kGemmMaxMT && N % 128 == 0) {
+      // many rows: MFMA-tiled kernel, 128-row tiles, weights read once per
+      // XCD; 256-column tiles when they alone fill the chip, else 128, and a
+      // K split when even those are too few
+      const int RB = (MT * 16 + 127) / 128;
+      const int wn = (N % 256 == 0 && N / 256 * RB >= want) ? 4 : 2;
+      const int nblk = N / (64 * wn) * RB;
+      int splits = 1;
+      if (nblk < want) splits = std::max(1, std::min({4, (kGemmSplitTarget + nblk - 1) / nblk, a.KT / 32}));
+      while (splits > 1 && (size_t)splits * RB * 128 * N * 4 > kGemmPartBytes) --splits;
+      const bool mlp = epi == EPI_SILU || family == PF_DOWN;
+      if (epi == EPI_LM) {
+        lm_parts = N / (64 * wn);
+        a.n_part = lm_parts;
+      }
+      ProfScope ps(k, family, (double)N * K * 2.0);
+      HIP_TRY(launch_gemm_tiled(epi, a, wn, !(mlp && k->mlp_single), splits, k->inv_rms, s));
+      return HVD_OK;
+    }
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
     int ns = 4, splits = 1;
     if (mt_block == 2 && N % 128 == 0 && nb8 >= want) {

@@ -1,0 +1,407 @@
+// Large-batch GEMMs of the verify forward (gfx950, MFMA 32x32x16 f16): many
+// verify rows at once (batched sequences, long drafts) and prefill chunks,
+// where the weight-streaming kernel would re-read the weights per 64 rows.
+//
+// Y[m, n] = sum_k A[m, k] W[n, k] over the same packed operands as the
+// streaming kernel: 1 KB fragments of 16 rows (or weight columns) x 32 K.
+// A workgroup of 4 waves (2 x 2) owns a 128-row x BN-column tile (BN = 64 WN)
+// and walks its K range in 32-wide steps: every step's A and W fragments are
+// copied into one of two LDS buffers (register-staged two steps ahead, so the
+// copy of step k+1 overlaps the MFMAs of step k), and each wave multiplies
+// its 64 x 32WN sub-tile with 2 x WN MFMA tiles of 32 x 32.  HI_LO chooses
+// the activation precision: the fp16 hi + lo pair (two MFMAs per tile, ~22
+// bits) or the hi part alone (one MFMA, 11 bits).
+//
+// Workgroups are numbered so that each XCD receives a contiguous run of
+// tiles with the row blocks of a column block adjacent: the weight tile is
+// fetched from HBM once into that XCD's L2 and re-read from there by the
+// other row blocks.  A K split (gridDim covers S splits) writes fp32 partial
+// tiles that gemm_tiled_finish sums in split order before the epilogue.
+//
+// The epilogue works on the accumulator registers: MFMA 32x32 output element
+// (row 8*(r/4) + 4*(lane/32) + r%4, column lane%32) of register r.  Partner
+// columns (rotary pairs, gate/up strips) are exchanged with lane shuffles.
+#include "common.h"
+#include "kernels.h"
+
+namespace hvd {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f32x16 mfma32_f16(const u32x4& a, const u32x4& b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                0, 0);
+}
+
+// Workgroup -> (split, column block, row block): XCD x (= id % 8 under the
+// round-robin dispatch) gets logical tiles [start_x, start_x + n_x), row
+// blocks fastest.
+struct TileCoord {
+  int split, cb, rb;
+};
+__device__ __forceinline__ TileCoord tile_coord(int id, int total, int RB, int CB) {
+  const int x = id & 7, local = id >> 3;
+  const int q = total >> 3, rem = total & 7;
+  const int logical = x * q + min(x, rem) + local;
+  TileCoord t;
+  t.rb = logical % RB;
+  t.cb = (logical / RB) % CB;
+  t.split = logical / (RB * CB);
+  return t;
+}
+
+// Epilogue on the accumulators of one wave.  rows/cols are global indices of
+// the wave's sub-tile origin.  inv_rms: per-row inverse RMS (NORM GEMMs).
+template <int WN, int EPI>
+__device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (&acc)[2][WN], int row_w, int col_w,
+                                               const float* inv_rms, float2* lm_best, int* lm_idx, int cb) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int lhi = lane >> 5, lc = lane & 31;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int R = row_w + 32 * i + 8 * (r >> 2) + 4 * lhi + (r & 3);
+      const bool rok = R < a.M;
+      const float ir = (EPI != EPI_RESID && rok) ? inv_rms[R] : 1.f;
+      if constexpr (EPI == EPI_QKV) {
+        RowMeta rm{0, 0, 0, 0};
+        if (rok) rm = a.rows[R];
+        const int half = a.dh >> 1;
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const int C = col_w + 32 * j + lc;
+          const float v = acc[i][j][r] * ir;
+          const float pv = __shfl_xor(v, 1);  // rotary partner (adjacent column)
+          if (!rok) continue;
+          if (C < a.q_cols + a.kv_cols) {
+            if ((C & 1) == 0) {
+              const int base = C < a.q_cols ? 0 : a.q_cols;
+              const int dp = (C - base) % a.dh;
+              const float2 cs = a.rope[(size_t)rm.pos * half + (dp >> 1)];
+              const float o0 = v * cs.x - pv * cs.y;
+              const float o1 = pv * cs.x + v * cs.y;
+              const uint32_t packed = (uint32_t)f2h(o0) | ((uint32_t)f2h(o1) << 16);
+              if (C < a.q_cols) {
+                *(uint32_t*)(a.Q + (size_t)R * a.q_cols + C) = packed;
+              } else {
+                const int g = (C - base) / a.dh;
+                *(uint32_t*)(a.kv + (size_t)rm.page * a.page_stride + ((size_t)g * kPage + (rm.pos & 15)) * a.dh +
+                             dp) = packed;
+              }
+            }
+          } else {
+            const int cv = C - a.q_cols - a.kv_cols;
+            const int g = cv / a.dh, d = cv % a.dh;
+            a.kv[(size_t)rm.page * a.page_stride + (size_t)a.Hkv * kPage * a.dh + ((size_t)g * a.dh + d) * kPage +
+                 (rm.pos & 15)] = (_Float16)v;
+          }
+        }
+      } else if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const int C = col_w + 32 * j + lc;
+          float x = 0.f;
+          if (rok) {
+            float* xp = a.X + (size_t)R * a.D + C;
+            x = *xp + acc[i][j][r];
+            *xp = x;
+            uint16_t hi, lo;
+            split_f16(x * a.gain_next[C], hi, lo);
+            const size_t off = afrag_off(R, C, a.MTtot);
+            a.Nhi[off] = hi;
+            a.Nlo[off] = lo;
+          }
+          // sum of squares over the 16 columns of this lane's strip
+          float sq = x * x;
+          sq += __shfl_xor(sq, 1);
+          sq += __shfl_xor(sq, 2);
+          sq += __shfl_xor(sq, 4);
+          sq += __shfl_xor(sq, 8);
+          if (rok && (lc & 15) == 0) a.ss_out[(size_t)R * (a.D >> 4) + (C >> 4)] = sq;
+        }
+      } else if constexpr (EPI == EPI_SILU) {
+        // a 32-column tile is one (gate strip, up strip) pair
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const int C = col_w + 32 * j + lc;
+          const float v = acc[i][j][r] * ir;
+          const float pv = __shfl_xor(v, 16);
+          if (rok && lc < 16) {
+            const float act = v / (1.f + __expf(-v)) * pv;
+            const int F = (C >> 5) * 16 + lc;
+            uint16_t hi, lo;
+            split_f16(act, hi, lo);
+            const size_t off = afrag_off(R, F, a.MTtot);
+            a.act_hi[off] = hi;
+            a.act_lo[off] = lo;
+          }
+        }
+      } else {  // EPI_LM: per-row max / lowest argmax over this wave's columns
+        float best = -INFINITY;
+        int bidx = 0x7fffffff;
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const int C = col_w + 32 * j + lc;
+          const float v = acc[i][j][r] * ir;
+          if (rok && a.logits) a.logits[(size_t)R * a.vocab + C] = v;
+          if (v > best) {  // columns ascend with j: ties keep the lower one
+            best = v;
+            bidx = C;
+          }
+        }
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) {
+          const float ov = __shfl_xor(best, o);
+          const int oi = __shfl_xor(bidx, o);
+          if (ov > best || (ov == best && oi < bidx)) {
+            best = ov;
+            bidx = oi;
+          }
+        }
+        if (lc == 0) {
+          const int lr = R - (row_w - (wave >> 1) * 64);  // row within the workgroup tile
+          lm_best[(wave & 1) * 128 + lr] = float2{best, 0.f};
+          lm_idx[(wave & 1) * 128 + lr] = bidx;
+        }
+      }
+    }
+  }
+  if constexpr (EPI == EPI_LM) {
+    __syncthreads();
+    // merge the two column halves (lower columns first) and publish
+    if (threadIdx.x < 128) {
+      const int lr = threadIdx.x;
+      const int R = (row_w - (wave >> 1) * 64) + lr;  // wave 0/1: row_w is the tile origin
+      float b = lm_best[lr].x;
+      int bi = lm_idx[lr];
+      const float b2 = lm_best[128 + lr].x;
+      const int bi2 = lm_idx[128 + lr];
+      if (b2 > b || (b2 == b && bi2 < bi)) {
+        b = b2;
+        bi = bi2;
+      }
+      if (R < a.M) {
+        a.part_val[(size_t)R * a.n_part + cb] = b;
+        a.part_idx[(size_t)R * a.n_part + cb] = bi;
+      }
+    }
+  }
+}
+
+template <int WN, int EPI, bool HI_LO>
+__global__ __launch_bounds__(256, 2) void gemm_tiled(GemmArgs a, const float* __restrict__ inv_rms, int RB, int CB,
+                                                     int S) {
+  constexpr int BN = 64 * WN;
+  constexpr int AF = 8;                    // A fragments per K step (128 rows)
+  constexpr int NA = HI_LO ? 2 * AF : AF;  // with the lo part
+  constexpr int WF = BN / 16;              // weight fragments per K step
+  constexpr int NF = NA + WF;
+  constexpr int LPT = NF / 4;  // 16-byte loads per thread per K step (NF*64 / 256)
+  static_assert(NF % 4 == 0, "fragments per step");
+  __shared__ u32x4 sbuf[2][NF][64];
+  __shared__ float2 lm_best[EPI == EPI_LM ? 256 : 1];
+  __shared__ int lm_idx[EPI == EPI_LM ? 256 : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wy = wave >> 1, wx = wave & 1;
+  const TileCoord tc = tile_coord(blockIdx.x, gridDim.x, RB, CB);
+  const int mt0 = tc.rb * 8;
+  const int kts = (a.KT + S - 1) / S;
+  const int kb = tc.split * kts, ke = min(a.KT, kb + kts);
+
+  // this thread's share of a K step: unit u = q*256 + tid is fragment u/64
+  // (q*4 + wave: wave-uniform), lane u%64
+  const u32x4* src[LPT];
+  size_t kstride[LPT];
+#pragma unroll
+  for (int q = 0; q < LPT; ++q) {
+    const int f = q * 4 + wave;
+    if (f < NA) {
+      const int mt = min(mt0 + (f % AF), a.MTtot - 1);  // rows past the operand: any valid tile
+      src[q] = (const u32x4*)(f < AF ? a.Ahi : a.Alo) + (size_t)mt * 64 + lane;
+      kstride[q] = (size_t)a.MTtot * 64;
+    } else {
+      const int st = tc.cb * WF + (f - NA);
+      src[q] = (const u32x4*)a.W + (size_t)(st >> 2) * a.wg + (size_t)(st & 3) * 64 + lane;
+      kstride[q] = a.wk;
+    }
+  }
+  u32x4 ra[LPT], rb[LPT];
+  auto load = [&](u32x4 (&r)[LPT], int kt) __attribute__((always_inline)) {
+    kt = min(kt, ke - 1);  // steps past the range re-read the last one (dropped)
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) r[q] = __builtin_nontemporal_load(src[q] + (size_t)kt * kstride[q]);
+  };
+  auto store = [&](const u32x4 (&r)[LPT], int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) sbuf[buf][q * 4 + wave][lane] = r[q];
+  };
+
+  f32x16 acc[2][WN];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < WN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // operand fragment of 32 rows (or columns) starting at fragment f0, K
+  // sub-step s (16 of the 32): lane l takes row l%32, K 16s + 8(l/32)..+8
+  const int fl = (lane & 15) + 16 * (lane >> 5);  // lane within the fragment, s = 0
+  const int fo = (lane >> 4) & 1;                 // second fragment for lanes 16-31 / 48-63
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      u32x4 ah[2], al[2], bw[WN];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        ah[i] = sbuf[buf][wy * 4 + 2 * i + fo][fl + 32 * s];
+        if constexpr (HI_LO) al[i] = sbuf[buf][AF + wy * 4 + 2 * i + fo][fl + 32 * s];
+      }
+#pragma unroll
+      for (int j = 0; j < WN; ++j) bw[j] = sbuf[buf][NA + wx * 2 * WN + 2 * j + fo][fl + 32 * s];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          acc[i][j] = mfma32_f16(ah[i], bw[j], acc[i][j]);
+          if constexpr (HI_LO) acc[i][j] = mfma32_f16(al[i], bw[j], acc[i][j]);
+        }
+    }
+  };
+
+  if (kb < ke) {
+    load(ra, kb);
+    load(rb, kb + 1);
+    store(ra, 0);
+    __syncthreads();
+    load(ra, kb + 2);
+    for (int kk = kb; kk < ke; kk += 2) {
+      // buffer 0 holds step kk; rb holds kk+1, ra holds kk+2 (in flight)
+      compute(0);
+      store(rb, 1);
+      __syncthreads();
+      load(rb, kk + 3);
+      if (kk + 1 < ke) compute(1);
+      store(ra, 0);
+      __syncthreads();
+      load(ra, kk + 4);
+    }
+  }
+
+  const int row_w = mt0 * 16 + wy * 64;
+  const int col_w = tc.cb * BN + wx * 32 * WN;
+  if (S > 1) {
+    // partial tile of this split, lane-native order: float4 group g of lane l
+    // at ((tile*4 + wave)*8*WN + g)*64 + l
+    const size_t tile = ((size_t)tc.split * RB + tc.rb) * CB + tc.cb;
+    float4* dst = (float4*)a.part + (tile * 4 + wave) * (8 * WN) * 64 + lane;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          dst[((i * WN + j) * 4 + g) * 64] =
+              float4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+    return;
+  }
+  tiled_epilogue<WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
+}
+
+// Sum of the S partial tiles (in split order), then the epilogue.  One
+// workgroup per (column block, row block), same numbering as gemm_tiled.
+template <int WN, int EPI>
+__global__ __launch_bounds__(256) void gemm_tiled_finish(GemmArgs a, const float* __restrict__ inv_rms, int RB,
+                                                         int CB, int S) {
+  constexpr int BN = 64 * WN;
+  __shared__ float2 lm_best[EPI == EPI_LM ? 256 : 1];
+  __shared__ int lm_idx[EPI == EPI_LM ? 256 : 1];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wy = wave >> 1, wx = wave & 1;
+  const TileCoord tc = tile_coord(blockIdx.x, gridDim.x, RB, CB);
+  f32x16 acc[2][WN];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < WN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  for (int sp = 0; sp < S; ++sp) {
+    const size_t tile = ((size_t)sp * RB + tc.rb) * CB + tc.cb;
+    const float4* p = (const float4*)a.part + (tile * 4 + wave) * (8 * WN) * 64 + lane;
+    float4 v[2][WN][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) v[i][j][g] = p[((i * WN + j) * 4 + g) * 64];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          acc[i][j][4 * g] += v[i][j][g].x;
+          acc[i][j][4 * g + 1] += v[i][j][g].y;
+          acc[i][j][4 * g + 2] += v[i][j][g].z;
+          acc[i][j][4 * g + 3] += v[i][j][g].w;
+        }
+  }
+  const int row_w = tc.rb * 128 + wy * 64;
+  const int col_w = tc.cb * BN + wx * 32 * WN;
+  tiled_epilogue<WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
+}
+
+// Inverse RMS of each row from its per-16-column sums of squares (one wave
+// per row, fixed summation order).
+__global__ __launch_bounds__(256) void row_inv_rms(const float* __restrict__ ss, int ss_n, int M, float inv_dim,
+                                                   float eps, float* __restrict__ out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= M) return;
+  float s = 0.f;
+  for (int q = lane; q < ss_n; q += 64) s += ss[(size_t)row * ss_n + q];
+  s = wave_sum(s);
+  if (lane == 0) out[row] = rsqrtf(s * inv_dim + eps);
+}
+
+template <int WN, int EPI, bool HI_LO>
+static hipError_t launch_t(const GemmArgs& a, const float* inv_rms, int splits, hipStream_t s) {
+  const int BN = 64 * WN;
+  const int CB = a.NT * 16 / BN, RB = (a.MTtot * 16 + 127) / 128;
+  const int total = CB * RB * splits;
+  hipLaunchKernelGGL((gemm_tiled<WN, EPI, HI_LO>), dim3(total), dim3(256), 0, s, a, inv_rms, RB, CB, splits);
+  if (splits > 1)
+    hipLaunchKernelGGL((gemm_tiled_finish<WN, EPI>), dim3(CB * RB), dim3(256), 0, s, a, inv_rms, RB, CB, splits);
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_te(const GemmArgs& a, const float* inv_rms, int wn, bool hi_lo, int splits, hipStream_t s) {
+  if (wn == 2) return hi_lo ? launch_t<2, EPI, true>(a, inv_rms, splits, s) : launch_t<2, EPI, false>(a, inv_rms, splits, s);
+  if (wn == 4) return hi_lo ? launch_t<4, EPI, true>(a, inv_rms, splits, s) : launch_t<4, EPI, false>(a, inv_rms, splits, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int wn, bool hi_lo, int splits, float* inv_rms,
+                             hipStream_t s) {
+  if (epi != EPI_RESID) {
+    const int rows = a.MTtot * 16;
+    hipLaunchKernelGGL(row_inv_rms, dim3((rows + 3) / 4), dim3(256), 0, s, a.ss, a.ss_n, rows, a.inv_dim, a.eps,
+                       inv_rms);
+  }
+  switch (epi) {
+    case EPI_QKV: return launch_te<EPI_QKV>(a, inv_rms, wn, hi_lo, splits, s);
+    case EPI_RESID: return launch_te<EPI_RESID>(a, inv_rms, wn, hi_lo, splits, s);
+    case EPI_SILU: return launch_te<EPI_SILU>(a, inv_rms, wn, hi_lo, splits, s);
+    case EPI_LM: return launch_te<EPI_LM>(a, inv_rms, wn, hi_lo, splits, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace hvd
