@@ -694,22 +694,28 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.part = k->gemm_part;
     const int want = k->gemm_min_blocks;
     if (MT > kGemmMaxMT && N % 128 == 0) {
-      // many rows: MFMA-tiled kernel, 128-row tiles, weights read once per
-      // XCD; 256-column tiles when they alone fill the chip, else 128, and a
-      // K split when even those are too few
-      const int RB = (MT * 16 + 127) / 128;
-      const int wn = (N % 256 == 0 && N / 256 * RB >= want) ? 4 : 2;
-      const int nblk = N / (64 * wn) * RB;
+      // many rows: MFMA-tiled kernel, weights read once per XCD.  The
+      // largest tile (256 x 256, 128 x 256, 128 x 128) that still gives
+      // enough workgroups, and a K split when even the smallest is too few
+      static const int tile_bm[3] = {128, 128, 256}, tile_bn[3] = {128, 256, 256};
+      int tile = 0;
+      for (int t = 2; t >= 1; --t)
+        if (N % tile_bn[t] == 0 && N / tile_bn[t] * ((MT * 16 + tile_bm[t] - 1) / tile_bm[t]) >= want) {
+          tile = t;
+          break;
+        }
+      const int RB = (MT * 16 + tile_bm[tile] - 1) / tile_bm[tile];
+      const int nblk = N / tile_bn[tile] * RB;
       int splits = 1;
       if (nblk < want) splits = std::max(1, std::min({4, (kGemmSplitTarget + nblk - 1) / nblk, a.KT / 32}));
-      while (splits > 1 && (size_t)splits * RB * 128 * N * 4 > kGemmPartBytes) --splits;
+      while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > kGemmPartBytes) --splits;
       const bool mlp = epi == EPI_SILU || family == PF_DOWN;
       if (epi == EPI_LM) {
-        lm_parts = N / (64 * wn);
+        lm_parts = N / tile_bn[tile];
         a.n_part = lm_parts;
       }
       ProfScope ps(k, family, (double)N * K * 2.0);
-      HIP_TRY(launch_gemm_tiled(epi, a, wn, !(mlp && k->mlp_single), splits, k->inv_rms, s));
+      HIP_TRY(launch_gemm_tiled(epi, a, tile, !(mlp && k->mlp_single), splits, k->inv_rms, s));
       return HVD_OK;
     }
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;

@@ -4,13 +4,15 @@
 //
 // Y[m, n] = sum_k A[m, k] W[n, k] over the same packed operands as the
 // streaming kernel: 1 KB fragments of 16 rows (or weight columns) x 32 K.
-// A workgroup of 4 waves (2 x 2) owns a 128-row x BN-column tile (BN = 64 WN)
-// and walks its K range in 32-wide steps: every step's A and W fragments are
-// copied into one of two LDS buffers (register-staged two steps ahead, so the
-// copy of step k+1 overlaps the MFMAs of step k), and each wave multiplies
-// its 64 x 32WN sub-tile with 2 x WN MFMA tiles of 32 x 32.  HI_LO chooses
-// the activation precision: the fp16 hi + lo pair (two MFMAs per tile, ~22
-// bits) or the hi part alone (one MFMA, 11 bits).
+// A workgroup of WY x WX waves owns a BM x BN tile (BM = 32 WM WY, BN =
+// 32 WN WX) and walks its K range in 32-wide steps: every step's A and W
+// fragments are copied into one of two LDS buffers (register-staged two steps
+// ahead, so the copy of step k+1 overlaps the MFMAs of step k), and each wave
+// multiplies its 32WM x 32WN sub-tile with WM x WN MFMA tiles of 32 x 32.
+// The 256 x 256 tile (8 waves) needs about 32 bytes of operand per clock and
+// CU at full MFMA rate; 128-row tiles (4 waves) serve smaller batches.
+// HI_LO chooses the activation precision: the fp16 hi + lo pair (two MFMAs
+// per tile, ~22 bits) or the hi part alone (one MFMA, 11 bits).
 //
 // Workgroups are numbered so that each XCD receives a contiguous run of
 // tiles with the row blocks of a column block adjacent: the weight tile is
@@ -52,14 +54,16 @@ __device__ __forceinline__ TileCoord tile_coord(int id, int total, int RB, int C
 
 // Epilogue on the accumulators of one wave.  rows/cols are global indices of
 // the wave's sub-tile origin.  inv_rms: per-row inverse RMS (NORM GEMMs).
-template <int WN, int EPI>
-__device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (&acc)[2][WN], int row_w, int col_w,
+template <int WY, int WX, int WM, int WN, int EPI>
+__device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (&acc)[WM][WN], int row_w, int col_w,
                                                const float* inv_rms, float2* lm_best, int* lm_idx, int cb) {
+  constexpr int BM = 32 * WM * WY;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int wy = wave / WX, wx = wave % WX;
   const int lhi = lane >> 5, lc = lane & 31;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < WM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int R = row_w + 32 * i + 8 * (r >> 2) + 4 * lhi + (r & 3);
@@ -161,26 +165,28 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
           }
         }
         if (lc == 0) {
-          const int lr = R - (row_w - (wave >> 1) * 64);  // row within the workgroup tile
-          lm_best[(wave & 1) * 128 + lr] = float2{best, 0.f};
-          lm_idx[(wave & 1) * 128 + lr] = bidx;
+          const int lr = R - (row_w - wy * 32 * WM);  // row within the workgroup tile
+          lm_best[wx * BM + lr] = float2{best, 0.f};
+          lm_idx[wx * BM + lr] = bidx;
         }
       }
     }
   }
   if constexpr (EPI == EPI_LM) {
     __syncthreads();
-    // merge the two column halves (lower columns first) and publish
-    if (threadIdx.x < 128) {
-      const int lr = threadIdx.x;
-      const int R = (row_w - (wave >> 1) * 64) + lr;  // wave 0/1: row_w is the tile origin
+    // merge the column parts (lower columns first) and publish
+    for (int lr = threadIdx.x; lr < BM; lr += 64 * WY * WX) {
+      const int R = (row_w - wy * 32 * WM) + lr;  // the tile origin
       float b = lm_best[lr].x;
       int bi = lm_idx[lr];
-      const float b2 = lm_best[128 + lr].x;
-      const int bi2 = lm_idx[128 + lr];
-      if (b2 > b || (b2 == b && bi2 < bi)) {
-        b = b2;
-        bi = bi2;
+#pragma unroll
+      for (int x = 1; x < WX; ++x) {
+        const float b2 = lm_best[x * BM + lr].x;
+        const int bi2 = lm_idx[x * BM + lr];
+        if (b2 > b || (b2 == b && bi2 < bi)) {
+          b = b2;
+          bi = bi2;
+        }
       }
       if (R < a.M) {
         a.part_val[(size_t)R * a.n_part + cb] = b;
@@ -190,35 +196,36 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
   }
 }
 
-template <int WN, int EPI, bool HI_LO>
-__global__ __launch_bounds__(256, 2) void gemm_tiled(GemmArgs a, const float* __restrict__ inv_rms, int RB, int CB,
-                                                     int S) {
-  constexpr int BN = 64 * WN;
-  constexpr int AF = 8;                    // A fragments per K step (128 rows)
+template <int WY, int WX, int WM, int WN, int EPI, bool HI_LO>
+__global__ __launch_bounds__(64 * WY * WX, 2) void gemm_tiled(GemmArgs a, const float* __restrict__ inv_rms, int RB,
+                                                              int CB, int S) {
+  constexpr int NW = WY * WX;
+  constexpr int BM = 32 * WM * WY, BN = 32 * WN * WX;
+  constexpr int AF = BM / 16;              // A fragments per K step
   constexpr int NA = HI_LO ? 2 * AF : AF;  // with the lo part
   constexpr int WF = BN / 16;              // weight fragments per K step
   constexpr int NF = NA + WF;
-  constexpr int LPT = NF / 4;  // 16-byte loads per thread per K step (NF*64 / 256)
-  static_assert(NF % 4 == 0, "fragments per step");
+  constexpr int LPT = NF / NW;  // 16-byte loads per thread per K step (NF*64 / (64*NW))
+  static_assert(NF % NW == 0, "fragments per step");
   __shared__ u32x4 sbuf[2][NF][64];
-  __shared__ float2 lm_best[EPI == EPI_LM ? 256 : 1];
-  __shared__ int lm_idx[EPI == EPI_LM ? 256 : 1];
+  __shared__ float2 lm_best[EPI == EPI_LM ? WX * BM : 1];
+  __shared__ int lm_idx[EPI == EPI_LM ? WX * BM : 1];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wy = wave >> 1, wx = wave & 1;
+  const int wy = wave / WX, wx = wave % WX;
   const TileCoord tc = tile_coord(blockIdx.x, gridDim.x, RB, CB);
-  const int mt0 = tc.rb * 8;
+  const int mt0 = tc.rb * AF;
   const int kts = (a.KT + S - 1) / S;
   const int kb = tc.split * kts, ke = min(a.KT, kb + kts);
 
-  // this thread's share of a K step: unit u = q*256 + tid is fragment u/64
-  // (q*4 + wave: wave-uniform), lane u%64
+  // this thread's share of a K step: unit u = q*64*NW + tid is fragment
+  // q*NW + wave (wave-uniform), lane u%64
   const u32x4* src[LPT];
   size_t kstride[LPT];
 #pragma unroll
   for (int q = 0; q < LPT; ++q) {
-    const int f = q * 4 + wave;
+    const int f = q * NW + wave;
     if (f < NA) {
       const int mt = min(mt0 + (f % AF), a.MTtot - 1);  // rows past the operand: any valid tile
       src[q] = (const u32x4*)(f < AF ? a.Ahi : a.Alo) + (size_t)mt * 64 + lane;
@@ -237,12 +244,12 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled(GemmArgs a, const float* __
   };
   auto store = [&](const u32x4 (&r)[LPT], int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int q = 0; q < LPT; ++q) sbuf[buf][q * 4 + wave][lane] = r[q];
+    for (int q = 0; q < LPT; ++q) sbuf[buf][q * NW + wave][lane] = r[q];
   };
 
-  f32x16 acc[2][WN];
+  f32x16 acc[WM][WN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < WM; ++i)
 #pragma unroll
     for (int j = 0; j < WN; ++j)
 #pragma unroll
@@ -255,16 +262,16 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled(GemmArgs a, const float* __
   auto compute = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      u32x4 ah[2], al[2], bw[WN];
+      u32x4 ah[WM], al[WM], bw[WN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        ah[i] = sbuf[buf][wy * 4 + 2 * i + fo][fl + 32 * s];
-        if constexpr (HI_LO) al[i] = sbuf[buf][AF + wy * 4 + 2 * i + fo][fl + 32 * s];
+      for (int i = 0; i < WM; ++i) {
+        ah[i] = sbuf[buf][wy * 2 * WM + 2 * i + fo][fl + 32 * s];
+        if constexpr (HI_LO) al[i] = sbuf[buf][AF + wy * 2 * WM + 2 * i + fo][fl + 32 * s];
       }
 #pragma unroll
       for (int j = 0; j < WN; ++j) bw[j] = sbuf[buf][NA + wx * 2 * WN + 2 * j + fo][fl + 32 * s];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
           acc[i][j] = mfma32_f16(ah[i], bw[j], acc[i][j]);
@@ -292,15 +299,15 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled(GemmArgs a, const float* __
     }
   }
 
-  const int row_w = mt0 * 16 + wy * 64;
+  const int row_w = tc.rb * BM + wy * 32 * WM;
   const int col_w = tc.cb * BN + wx * 32 * WN;
   if (S > 1) {
     // partial tile of this split, lane-native order: float4 group g of lane l
-    // at ((tile*4 + wave)*8*WN + g)*64 + l
+    // at ((tile*NW + wave)*4*WM*WN + g)*64 + l
     const size_t tile = ((size_t)tc.split * RB + tc.rb) * CB + tc.cb;
-    float4* dst = (float4*)a.part + (tile * 4 + wave) * (8 * WN) * 64 + lane;
+    float4* dst = (float4*)a.part + (tile * NW + wave) * (4 * WM * WN) * 64 + lane;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
       for (int j = 0; j < WN; ++j)
 #pragma unroll
@@ -309,53 +316,51 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled(GemmArgs a, const float* __
               float4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
     return;
   }
-  tiled_epilogue<WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
+  tiled_epilogue<WY, WX, WM, WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
 }
 
 // Sum of the S partial tiles (in split order), then the epilogue.  One
 // workgroup per (column block, row block), same numbering as gemm_tiled.
-template <int WN, int EPI>
-__global__ __launch_bounds__(256) void gemm_tiled_finish(GemmArgs a, const float* __restrict__ inv_rms, int RB,
-                                                         int CB, int S) {
-  constexpr int BN = 64 * WN;
-  __shared__ float2 lm_best[EPI == EPI_LM ? 256 : 1];
-  __shared__ int lm_idx[EPI == EPI_LM ? 256 : 1];
+template <int WY, int WX, int WM, int WN, int EPI>
+__global__ __launch_bounds__(64 * WY * WX) void gemm_tiled_finish(GemmArgs a, const float* __restrict__ inv_rms,
+                                                                  int RB, int CB, int S) {
+  constexpr int NW = WY * WX;
+  constexpr int BM = 32 * WM * WY, BN = 32 * WN * WX;
+  __shared__ float2 lm_best[EPI == EPI_LM ? WX * BM : 1];
+  __shared__ int lm_idx[EPI == EPI_LM ? WX * BM : 1];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wy = wave >> 1, wx = wave & 1;
+  const int wy = wave / WX, wx = wave % WX;
   const TileCoord tc = tile_coord(blockIdx.x, gridDim.x, RB, CB);
-  f32x16 acc[2][WN];
+  f32x16 acc[WM][WN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < WM; ++i)
 #pragma unroll
     for (int j = 0; j < WN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   for (int sp = 0; sp < S; ++sp) {
     const size_t tile = ((size_t)sp * RB + tc.rb) * CB + tc.cb;
-    const float4* p = (const float4*)a.part + (tile * 4 + wave) * (8 * WN) * 64 + lane;
-    float4 v[2][WN][4];
+    const float4* p = (const float4*)a.part + (tile * NW + wave) * (4 * WM * WN) * 64 + lane;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
-      for (int j = 0; j < WN; ++j)
+      for (int j = 0; j < WN; ++j) {
+        float4 v[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) v[i][j][g] = p[((i * WN + j) * 4 + g) * 64];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < WN; ++j)
+        for (int g = 0; g < 4; ++g) v[g] = p[((i * WN + j) * 4 + g) * 64];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          acc[i][j][4 * g] += v[i][j][g].x;
-          acc[i][j][4 * g + 1] += v[i][j][g].y;
-          acc[i][j][4 * g + 2] += v[i][j][g].z;
-          acc[i][j][4 * g + 3] += v[i][j][g].w;
+          acc[i][j][4 * g] += v[g].x;
+          acc[i][j][4 * g + 1] += v[g].y;
+          acc[i][j][4 * g + 2] += v[g].z;
+          acc[i][j][4 * g + 3] += v[g].w;
         }
+      }
   }
-  const int row_w = tc.rb * 128 + wy * 64;
+  const int row_w = tc.rb * BM + wy * 32 * WM;
   const int col_w = tc.cb * BN + wx * 32 * WN;
-  tiled_epilogue<WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
+  tiled_epilogue<WY, WX, WM, WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
 }
 
 // Inverse RMS of each row from its per-16-column sums of squares (one wave
@@ -370,25 +375,35 @@ __global__ __launch_bounds__(256) void row_inv_rms(const float* __restrict__ ss,
   if (lane == 0) out[row] = rsqrtf(s * inv_dim + eps);
 }
 
-template <int WN, int EPI, bool HI_LO>
+template <int WY, int WX, int WM, int WN, int EPI, bool HI_LO>
 static hipError_t launch_t(const GemmArgs& a, const float* inv_rms, int splits, hipStream_t s) {
-  const int BN = 64 * WN;
-  const int CB = a.NT * 16 / BN, RB = (a.MTtot * 16 + 127) / 128;
+  const int BM = 32 * WM * WY, BN = 32 * WN * WX, NT = 64 * WY * WX;
+  const int CB = a.NT * 16 / BN, RB = (a.MTtot * 16 + BM - 1) / BM;
   const int total = CB * RB * splits;
-  hipLaunchKernelGGL((gemm_tiled<WN, EPI, HI_LO>), dim3(total), dim3(256), 0, s, a, inv_rms, RB, CB, splits);
+  hipLaunchKernelGGL((gemm_tiled<WY, WX, WM, WN, EPI, HI_LO>), dim3(total), dim3(NT), 0, s, a, inv_rms, RB, CB,
+                     splits);
   if (splits > 1)
-    hipLaunchKernelGGL((gemm_tiled_finish<WN, EPI>), dim3(CB * RB), dim3(256), 0, s, a, inv_rms, RB, CB, splits);
+    hipLaunchKernelGGL((gemm_tiled_finish<WY, WX, WM, WN, EPI>), dim3(CB * RB), dim3(NT), 0, s, a, inv_rms, RB, CB,
+                       splits);
   return hipGetLastError();
 }
 
-template <int EPI>
-static hipError_t launch_te(const GemmArgs& a, const float* inv_rms, int wn, bool hi_lo, int splits, hipStream_t s) {
-  if (wn == 2) return hi_lo ? launch_t<2, EPI, true>(a, inv_rms, splits, s) : launch_t<2, EPI, false>(a, inv_rms, splits, s);
-  if (wn == 4) return hi_lo ? launch_t<4, EPI, true>(a, inv_rms, splits, s) : launch_t<4, EPI, false>(a, inv_rms, splits, s);
+template <int EPI, bool HI_LO>
+static hipError_t launch_th(const GemmArgs& a, const float* inv_rms, int tile, int splits, hipStream_t s) {
+  switch (tile) {
+    case 0: return launch_t<2, 2, 2, 2, EPI, HI_LO>(a, inv_rms, splits, s);  // 128 x 128, 4 waves
+    case 1: return launch_t<2, 2, 2, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 128 x 256, 4 waves
+    case 2: return launch_t<4, 2, 2, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 256 x 256, 8 waves
+  }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int wn, bool hi_lo, int splits, float* inv_rms,
+template <int EPI>
+static hipError_t launch_te(const GemmArgs& a, const float* inv_rms, int tile, bool hi_lo, int splits, hipStream_t s) {
+  return hi_lo ? launch_th<EPI, true>(a, inv_rms, tile, splits, s) : launch_th<EPI, false>(a, inv_rms, tile, splits, s);
+}
+
+hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, int splits, float* inv_rms,
                              hipStream_t s) {
   if (epi != EPI_RESID) {
     const int rows = a.MTtot * 16;
@@ -396,10 +411,10 @@ hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int wn, bool hi_lo, int
                        inv_rms);
   }
   switch (epi) {
-    case EPI_QKV: return launch_te<EPI_QKV>(a, inv_rms, wn, hi_lo, splits, s);
-    case EPI_RESID: return launch_te<EPI_RESID>(a, inv_rms, wn, hi_lo, splits, s);
-    case EPI_SILU: return launch_te<EPI_SILU>(a, inv_rms, wn, hi_lo, splits, s);
-    case EPI_LM: return launch_te<EPI_LM>(a, inv_rms, wn, hi_lo, splits, s);
+    case EPI_QKV: return launch_te<EPI_QKV>(a, inv_rms, tile, hi_lo, splits, s);
+    case EPI_RESID: return launch_te<EPI_RESID>(a, inv_rms, tile, hi_lo, splits, s);
+    case EPI_SILU: return launch_te<EPI_SILU>(a, inv_rms, tile, hi_lo, splits, s);
+    case EPI_LM: return launch_te<EPI_LM>(a, inv_rms, tile, hi_lo, splits, s);
   }
   return hipErrorInvalidValue;
 }

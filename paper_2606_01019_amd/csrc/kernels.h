@@ -141,10 +141,11 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 // ns: 16-column strips per workgroup (1, 2, 4; >= 2 for EPI_SILU); grid.x = NT / ns.
 // splits > 1 splits K across workgroups and adds the gemm_finish pass.
 hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, hipStream_t s);
-// Large-batch GEMM (gemm_tiled.hip): 128 x 64wn tiles (wn 2 or 4), hi_lo
-// false = the hi activation part alone, K split `splits` ways; inv_rms is a
-// per-row scratch vector (computed here for normalised inputs).
-hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int wn, bool hi_lo, int splits, float* inv_rms,
+// Large-batch GEMM (gemm_tiled.hip): tile 0 = 128 x 128, 1 = 128 x 256,
+// 2 = 256 x 256 (rows x columns); hi_lo false = the hi activation part
+// alone; K split `splits` ways; inv_rms is a per-row scratch vector
+// (computed here for normalised inputs).
+hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, int splits, float* inv_rms,
                              hipStream_t s);
 // chunk: the plan's KV chunk length (picks the pages staged per sub-chunk)
 hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, hipStream_t s);

@@ -87,3 +87,36 @@ def oracle_commit_as(st, res, a_gpu, next_gpu):
          for l, nv in enumerate(res.new_v)]
     toks = list(st.tokens) + [int(t) for t in res.draft[:a_gpu]] + [int(next_gpu)]
     return SeqState(tokens=toks, K=K, V=V)
+
+
+def check_golden(rep: Report, L, rec, sample_ids, a_gpu, next_gpu, tol=LOGIT_TOL):
+    """Compare one sequence's GPU verify (logit rows L [k+1, V]) with a stored
+    oracle record (tests/golden/*.json): logits at the sampled ids and at each
+    row's oracle top ids, per-row argmax except near ties, accepted length
+    and next token unless a near tie lies on the accepted path.
+
+    Returns True when the GPU took another branch at a near tie (the caller
+    stops following the oracle's trajectory for that sequence)."""
+    k = len(rec["draft"])
+    assert L.shape[0] == k + 1
+    ids = np.asarray(sample_ids)
+    err = float(np.abs(L[:, ids] - np.asarray(rec["sample_logits"])).max())
+    top_ids = np.asarray(rec["top_ids"])
+    err_top = max(float(np.abs(L[r, top_ids[r]] - np.asarray(rec["top_logits"][r])).max()) for r in range(k + 1))
+    err = max(err, err_top)
+    rep.max_err = max(rep.max_err, err)
+    assert err <= tol, f"logit error {err:.3e} > {tol}"
+    margin = np.asarray(rec["margin"])
+    tie = margin < TIE_MARGIN
+    rep.rows += k + 1
+    rep.excused += int(tie.sum())
+    g_gpu = L.argmax(axis=1)
+    g_ref = np.asarray(rec["argmax"])
+    bad = (g_gpu != g_ref) & ~tie
+    assert not bad.any(), f"argmax differs at non-tie rows {np.flatnonzero(bad)}"
+    rep.excused_diff += int(((g_gpu != g_ref) & tie).sum())
+    assert a_gpu == accept_from_argmax(g_gpu, rec["draft"]) and next_gpu == int(g_gpu[a_gpu])
+    if not tie[:min(rec["accepted"], a_gpu) + 1].any():
+        assert a_gpu == rec["accepted"] and next_gpu == rec["next"], (a_gpu, rec["accepted"], next_gpu, rec["next"])
+        return False
+    return a_gpu != rec["accepted"] or next_gpu != rec["next"]

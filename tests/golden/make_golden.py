@@ -26,7 +26,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 
 import oracle  # noqa: E402
 from oracle.model import OracleModel  # noqa: E402
-from workloads import SHAPE_8B, SHAPE_32B, make_weights, tokens as wt  # noqa: E402
+from workloads import SHAPE_8B, SHAPE_32B, batches, make_weights, tokens as wt  # noqa: E402
 
 N_SAMPLE = 64
 TOP = 8
@@ -40,10 +40,10 @@ def sample_ids(vocab):
     return np.sort(wt.rng_for("misc", 99).choice(vocab, size=N_SAMPLE, replace=False)).astype(int)
 
 
-def record(res, ids):
+def record(res, ids, top_n=TOP):
     lg = res.logits
     part = np.partition(lg, -2, axis=-1)
-    top = np.argsort(-lg, axis=-1)[:, :TOP]
+    top = np.argsort(-lg, axis=-1)[:, :top_n]
     return {
         "draft": [int(t) for t in res.draft],
         "accepted": int(res.accepted),
@@ -127,8 +127,72 @@ def case_cfg3():
             "oracle_dtype": "float32"}
 
 
+def case_cfg4():
+    """Mixed batch: the oracle verifies the sampled sequences one by one (a
+    batched verify is per-sequence by construction)."""
+    cfg = SHAPE_8B
+    plans = batches.mixed_batch_plan()
+    picks = batches.mixed_batch_sampled(plans)
+    log("cfg4: weights")
+    m = fp32_model(cfg)
+    ids = sample_ids(cfg.vocab)
+    seqs = []
+    for b in picks:
+        p = plans[b]
+        ctx = batches.mixed_batch_context(p, cfg.vocab)
+        log(f"cfg4: seq {b} prefill {p.ctx_len}")
+        st = oracle.prefill(m, ctx)
+        g = greedy(m, st, p.accept + 1)
+        d = batches.mixed_batch_draft(p, ctx, g, cfg.vocab)
+        res = oracle.verify(m, st, d)
+        log(f"cfg4: seq {b} ({p.kind}, k={p.k}) planted={p.accept} accepted={res.accepted}")
+        rec = record(res, ids)
+        rec["seq"] = b
+        seqs.append(rec)
+    return {"config": "8B shape, 32 sequences with contexts uniform in [1024, 8192] (Zipf tokens); sequences "
+                      "0-15 model chains k=8 planted geometric(p=0.4), 16-31 cache drafts k in [16, 64] planted "
+                      "uniform in [0, k]; the oracle checks the shortest and longest context of each kind",
+            "model": cfg.as_dict(), "sample_ids": [int(i) for i in ids], "sampled": picks, "seqs": seqs,
+            "oracle_dtype": "float32"}
+
+
+CFG5_LAYERS = 4
+CFG5_SEQS = (0, 1)
+
+
+def case_cfg5():
+    """32B-shaped widths at reduced depth: two of the eight sequences over the
+    16 verify + commit steps (commit keeps the oracle's accepted prefix)."""
+    cfg = SHAPE_32B.with_layers(CFG5_LAYERS)
+    plans = batches.multistep_plan()
+    log("cfg5: weights")
+    m = fp32_model(cfg)
+    ids = sample_ids(cfg.vocab)[:16]
+    out = []
+    for b in CFG5_SEQS:
+        ctx = batches.multistep_context(b, 8192, cfg.vocab)
+        log(f"cfg5: seq {b} prefill")
+        st = oracle.prefill(m, ctx)
+        steps = []
+        for s_, row in enumerate(plans):
+            p = row[b]
+            g = greedy(m, st, p.accept + 1)
+            d = batches.multistep_draft(b, s_, p.k, p.accept, ctx, g, cfg.vocab)
+            res = oracle.verify(m, st, d)
+            rec = record(res, ids, top_n=4)
+            steps.append(rec)
+            st = oracle.commit(st, res, res.accepted)
+            log(f"cfg5: seq {b} step {s_} k={p.k} planted={p.accept} accepted={res.accepted}")
+        out.append({"seq": b, "steps": steps})
+    return {"config": "32B widths (64 q / 8 kv heads of 128, SwiGLU 27648, vocab 152064) at 4 layers; 8 "
+                      "sequences at context 8192 (Zipf tokens), 16 verify + commit steps with k uniform in "
+                      "{4..64} and cache drafts planted uniform in [0, k]; sequences 0 and 1 checked",
+            "model": cfg.as_dict(), "n_layers": CFG5_LAYERS, "sample_ids": [int(i) for i in ids],
+            "seqs": out, "oracle_dtype": "float32"}
+
+
 def main():
-    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3}
+    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3, "cfg4": case_cfg4, "cfg5": case_cfg5}
     for name in sys.argv[1:]:
         t0 = time.time()
         out = cases[name]()

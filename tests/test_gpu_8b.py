@@ -23,18 +23,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 @pytest.fixture(scope="module")
-def setup8b():
+def setup8b(model8b):
     import torch
-    if not torch.cuda.is_available():
-        pytest.skip("no GPU")
     import paper_2606_01019_amd as hvd
-    from workloads import SHAPE_8B, make_weights, tokens as wt
+    from workloads import SHAPE_8B, tokens as wt
     with open(os.path.join(HERE, "golden", "cfg2.json")) as f:
         gold = json.load(f)
-    print("generating 8B weights", flush=True)
-    w = make_weights(SHAPE_8B, seed=42)
-    model = hvd.Model(SHAPE_8B, w)
-    del w
+    model = model8b
     kv = hvd.KVCache(model, max_seqs=1, n_pages=256)
     ctx = wt.zipf_context(wt.rng_for(*gold["context_seed"]), gold["context_len"], SHAPE_8B.vocab)
     kv.prefill(0, ctx)

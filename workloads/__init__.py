@@ -15,3 +15,4 @@ from .weights import (  # noqa: F401
     f32_to_bf16_bits,
 )
 from . import tokens  # noqa: F401
+from . import batches  # noqa: F401
