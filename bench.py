@@ -27,6 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0  # dense fp16/bf16
 K_CYCLE = (1, 2, 4, 8, 16)
 # profiling families of hvd_profile_read, in order
 FAMILIES = ("qkv", "o", "gateup", "down", "lm_head", "attention", "combine", "other")
@@ -45,6 +46,211 @@ def algorithmic_bytes(cfg, ctx, k):
     weights = 2.0 * (cfg.n_layers * layer + V * D)
     kv = 2.0 * 2 * kd * cfg.n_layers * (ctx + k + 1)
     return weights + kv
+
+
+def layer_params(cfg):
+    D, F = cfg.d_model, cfg.ffn_dim
+    return D * (cfg.q_dim + 2 * cfg.kv_dim) + cfg.q_dim * D + 3 * D * F
+
+
+def batch_bytes(cfg, seqs):
+    """Algorithmic HBM bytes of one verify over seqs = [(ctx, k), ...]:
+    every weight once, the K/V of every attended key once."""
+    weights = 2.0 * (cfg.n_layers * layer_params(cfg) + cfg.vocab * cfg.d_model)
+    kv = sum(2.0 * 2 * cfg.kv_dim * cfg.n_layers * (c + k + 1) for c, k in seqs)
+    return weights + kv
+
+
+def batch_flops(cfg, seqs):
+    """Algorithmic flops: 2 per weight per row, plus QK^T and PV over each
+    row's visible keys (causal inside the draft)."""
+    M = sum(k + 1 for _, k in seqs)
+    gemm = 2.0 * M * (cfg.n_layers * layer_params(cfg) + cfg.vocab * cfg.d_model)
+    attn = 4.0 * cfg.q_dim * cfg.n_layers * sum((k + 1) * (c + (k + 2) / 2.0) for c, k in seqs)
+    return gemm + attn
+
+
+def rooflines(cfg, seqs, t):
+    b, f = batch_bytes(cfg, seqs), batch_flops(cfg, seqs)
+    hbm = b / t / 1e9 / HBM_PEAK_GBS
+    mfma = f / t / 1e12 / MFMA_PEAK_TFLOPS
+    return {"bytes": b, "flops": f, "hbm_frac": hbm, "mfma_frac": mfma,
+            "bound": "mfma" if f / (MFMA_PEAK_TFLOPS * 1e12) > b / (HBM_PEAK_GBS * 1e9) else "hbm",
+            "frac": max(hbm, mfma)}
+
+
+def greedy_batch(kv, ids, need):
+    """Greedy continuations (k = 0 verify + commit) of several sequences,
+    need[b] tokens each; the sequences are restored afterwards."""
+    base = {b: kv.seq_info(b)[:2] for b in ids}
+    out = {b: [] for b in ids}
+    while True:
+        active = [b for b in ids if len(out[b]) < need[b]]
+        if not active:
+            break
+        ctxs = [kv.seq_info(b)[0] for b in active]
+        _, n = kv.verify(active, ctxs, [np.zeros(0, np.int32)] * len(active))
+        kv.commit(active)
+        for b, t in zip(active, n):
+            out[b].append(int(t))
+    for b in ids:
+        kv.truncate(b, *base[b])
+    return out
+
+
+def timed_batch(kv, ids, drafts, reps):
+    """Median wall time of verify + commit over reps repeats, the sequences
+    rolled back after each (hvd_verify returns once its outputs are on the
+    host, so the wall time covers the device work)."""
+    base = {b: kv.seq_info(b)[:2] for b in ids}
+    ctxs = [base[b][0] for b in ids]
+    times, acc = [], None
+    for _ in range(reps):
+        t = time.perf_counter()
+        a, _ = kv.verify(ids, ctxs, drafts)
+        kv.commit(ids)
+        times.append(time.perf_counter() - t)
+        acc = [int(x) for x in a]
+        for b in ids:
+            kv.truncate(b, *base[b])
+    return float(np.median(times)), acc
+
+
+def profiled_families(kv, ids, drafts):
+    """Per-role device time of one verify + commit (HIP events around every
+    launch; the sequences are rolled back afterwards)."""
+    base = {b: kv.seq_info(b)[:2] for b in ids}
+    ctxs = [base[b][0] for b in ids]
+    kv.profile_enable(True)
+    kv.verify(ids, ctxs, drafts)
+    kv.commit(ids)
+    fam = {}
+    for i, name in enumerate(FAMILIES):
+        ms, n, _ = kv.profile_read(i)
+        fam[name] = {"ms": ms, "launches": n}
+    kv.profile_enable(False)
+    for b in ids:
+        kv.truncate(b, *base[b])
+    return fam
+
+
+def leg_long_context(model, reps):
+    """Long agentic context: one sequence at 16384 tokens of mutated 64-token
+    segments; cache drafts k = 32, 48, 64 planted bimodal from the model's own
+    greedy continuation, plus the latency sweep over k = 0 .. 64."""
+    import paper_2606_01019_amd as hvd
+    from workloads import tokens as wt
+    cfg = model.cfg
+    n = 16384
+    ctx = wt.segment_context(wt.rng_for("context", 3), n, cfg.vocab)
+    kv = hvd.KVCache(model, max_seqs=1, n_pages=(n + 80) // 16 + 8)
+    t0 = time.time()
+    kv.prefill(0, ctx)
+    prefill_s = time.time() - t0
+    greedy = greedy_batch(kv, [0], {0: 66})[0]
+    arng, drng = wt.rng_for("accept", 3, 1), wt.rng_for("draft", 3, 1)
+    sweep, cache_legs = {}, []
+    for k in (0, 1, 2, 4, 8, 16, 32, 48, 64):
+        a_plan = wt.bimodal_accept(arng, k) if k >= 32 else (wt.geometric_accept(arng, 0.3, k) if k else 0)
+        d = wt.plant_cache_draft(drng, ctx, greedy, a_plan, k, cfg.vocab) if k else np.zeros(0, np.int32)
+        t, acc = timed_batch(kv, [0], [d], reps)
+        sweep[str(k)] = t * 1e6
+        if k >= 32:
+            r = rooflines(cfg, [(n - 1, k)], t)
+            cache_legs.append({"k": k, "planted": a_plan, "accepted": acc[0], "latency_us": t * 1e6,
+                               "committed_tokens_per_s": (acc[0] + 1) / t, "hbm_frac": r["hbm_frac"],
+                               "mfma_frac": r["mfma_frac"]})
+    kv.close()
+    return {"workload": f"8B shape, batch 1, context {n} (64-token segments, 16 bases, 20% mutation), cache "
+                        f"drafts k = 32/48/64 planted bimodal",
+            "prefill_tokens_per_s": (n - 1) / prefill_s,
+            "latency_us_by_k": sweep, "cache_drafts": cache_legs,
+            "committed_tokens_per_s": sum(c["accepted"] + 1 for c in cache_legs) /
+                                      sum(c["latency_us"] * 1e-6 for c in cache_legs)}
+
+
+def leg_mixed_batch(model, reps):
+    """32 sequences, contexts 1024..8192 over the paged cache, half model
+    chains k = 8 (geometric 0.4), half cache drafts k in 16..64 (uniform)."""
+    import paper_2606_01019_amd as hvd
+    from workloads import batches
+    cfg = model.cfg
+    plans = batches.mixed_batch_plan()
+    pages = sum((p.ctx_len + p.k + 16) // 16 + 1 for p in plans) + 128
+    kv = hvd.KVCache(model, max_seqs=len(plans), n_pages=pages)
+    ctxs = [batches.mixed_batch_context(p, cfg.vocab) for p in plans]
+    t0 = time.time()
+    for p in plans:
+        kv.prefill(p.seq, ctxs[p.seq])
+    prefill_s = time.time() - t0
+    ids = [p.seq for p in plans]
+    greedy = greedy_batch(kv, ids, {p.seq: p.accept + 1 for p in plans})
+    drafts = [batches.mixed_batch_draft(p, ctxs[p.seq], greedy[p.seq], cfg.vocab) for p in plans]
+    t, acc = timed_batch(kv, ids, drafts, reps)
+    fam = profiled_families(kv, ids, drafts)
+    seqs = [(p.ctx_len - 1, p.k) for p in plans]
+    r = rooflines(cfg, seqs, t)
+    kv.close()
+    return {"workload": "8B shape, 32 sequences, contexts uniform 1024..8192, 16 model chains k=8 "
+                        "(geometric 0.4) + 16 cache drafts k in 16..64 (uniform acceptance)",
+            "rows": sum(k + 1 for _, k in seqs), "latency_ms": t * 1e3,
+            "committed_tokens_per_s": sum(a + 1 for a in acc) / t,
+            "accept_mismatch_vs_plant": sum(1 for a, p in zip(acc, plans) if a != p.accept),
+            "prefill_tokens_per_s": sum(p.ctx_len - 1 for p in plans) / prefill_s,
+            "roofline": {"bound": r["bound"], "achieved": r["flops"] / t / 1e12, "peak": MFMA_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": r["mfma_frac"], "hbm_frac": r["hbm_frac"]},
+            "kernel_families_ms": {k: v["ms"] for k, v in fam.items()}}
+
+
+def leg_multistep_32b(reps):
+    """32B shape (64 layers), 8 sequences at context 8192, 16 consecutive
+    verify + commit steps, k uniform 4..64, acceptance uniform in [0, k];
+    every step is timed reps times with a rollback in between."""
+    import torch
+    import paper_2606_01019_amd as hvd
+    from workloads import SHAPE_32B, batches, make_weights
+    cfg = SHAPE_32B
+    t0 = time.time()
+    w = make_weights(cfg, seed=42)
+    log(f"32B weights drawn in {time.time() - t0:.1f}s")
+    model = hvd.Model(cfg, w)
+    del w
+    plans = batches.multistep_plan()
+    n = len(plans[0])
+    kv = hvd.KVCache(model, max_seqs=n, n_pages=n * ((8192 + 16 * 66) // 16 + 4))
+    ctxs = [batches.multistep_context(b, 8192, cfg.vocab) for b in range(n)]
+    t0 = time.time()
+    for b in range(n):
+        kv.prefill(b, ctxs[b])
+    prefill_s = time.time() - t0
+    ids = list(range(n))
+    step_t, committed, rows, flops, bts = [], 0, [], 0.0, 0.0
+    for s, row in enumerate(plans):
+        greedy = greedy_batch(kv, ids, {b: row[b].accept + 1 for b in ids})
+        drafts = [batches.multistep_draft(b, s, row[b].k, row[b].accept, ctxs[b], greedy[b], cfg.vocab) for b in ids]
+        seqs = [(kv.seq_info(b)[0], row[b].k) for b in ids]
+        t, _ = timed_batch(kv, ids, drafts, reps)
+        a, _ = kv.verify(ids, [c for c, _ in seqs], drafts)  # the step itself, kept
+        kv.commit(ids)
+        step_t.append(t)
+        committed += sum(int(x) + 1 for x in a)
+        rows.append(sum(k + 1 for _, k in seqs))
+        flops += batch_flops(cfg, seqs)
+        bts += batch_bytes(cfg, seqs)
+    total = sum(step_t)
+    kv.close()
+    model.close()
+    del kv, model
+    torch.cuda.empty_cache()
+    return {"workload": "32B shape (64 layers), 8 sequences at context 8192, 16 verify + commit steps, k "
+                        "uniform 4..64, acceptance uniform in [0, k], each step re-verified after rollback",
+            "mean_rows": float(np.mean(rows)), "step_latency_ms": [x * 1e3 for x in step_t],
+            "mean_step_ms": total / len(step_t) * 1e3,
+            "committed_tokens_per_s": committed / total,
+            "prefill_tokens_per_s": n * 8191 / prefill_s,
+            "roofline": {"bound": "mfma" if flops / (MFMA_PEAK_TFLOPS * 1e12) > bts / (HBM_PEAK_GBS * 1e9) else "hbm",
+                         "achieved_TFLOPs": flops / total / 1e12, "mfma_frac": flops / total / 1e12 / MFMA_PEAK_TFLOPS,
+                         "achieved_GBs": bts / total / 1e9, "hbm_frac": bts / total / 1e9 / HBM_PEAK_GBS}}
 
 
 def plan_steps(n, seed_key):
@@ -101,6 +307,9 @@ def main():
     ap.add_argument("--ctx", type=int, default=2048)
     ap.add_argument("--layers", type=int, default=0, help="override depth (0 = full 32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workloads", default="long_context,mixed_batch,multistep_32b",
+                    help="extra workloads reported beside the headline (comma list, '' for none)")
+    ap.add_argument("--reps", type=int, default=5, help="repeats per timed step of the extra workloads")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the verify step of one "
@@ -221,6 +430,24 @@ def main():
                      "bytes_per_launch": d_b / max(d_n, 1)},
         "kernel_families": fam,
     }
+    kv.close()
+    legs = [x for x in args.workloads.split(",") if x]
+    extra = {}
+    for leg in legs:
+        t0 = time.time()
+        if leg == "long_context":
+            extra[leg] = leg_long_context(model, args.reps)
+        elif leg == "mixed_batch":
+            extra[leg] = leg_mixed_batch(model, args.reps)
+        elif leg == "multistep_32b":
+            model.close()
+            torch.cuda.empty_cache()
+            extra[leg] = leg_multistep_32b(args.reps)
+        else:
+            raise SystemExit(f"unknown workload {leg}")
+        log(f"{leg} in {time.time() - t0:.1f}s")
+    if extra:
+        out["workloads"] = extra
     if not args.no_cpu_baseline:
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(SHAPE_8B, args.ctx, committed / args.steps, np.mean(ks))

@@ -320,7 +320,7 @@ struct hvd_kv_s {
   int attn_min_items = kAttnMinItems;
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
-  bool mlp_single = false;   // large-batch MLP GEMMs on the hi activation part only
+  bool mlp_single = true;    // large-batch verify MLP GEMMs on the hi activation part only
   int32_t* g = nullptr;
   int32_t* out = nullptr;
   uint32_t* counter = nullptr;
@@ -715,7 +715,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         a.n_part = lm_parts;
       }
       ProfScope ps(k, family, (double)N * K * 2.0);
-      HIP_TRY(launch_gemm_tiled(epi, a, tile, !(mlp && k->mlp_single), splits, k->inv_rms, s));
+      HIP_TRY(launch_gemm_tiled(epi, a, tile, !(mlp && k->mlp_single && lm_head), splits, k->inv_rms, s));
       return HVD_OK;
     }
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
@@ -1030,6 +1030,11 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
         for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
         k->graphs.clear();
       }
+      return HVD_OK;
+    case HVD_OPT_MLP_SINGLE:
+      k->mlp_single = value != 0;
+      for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);  // captured with the old choice
+      k->graphs.clear();
       return HVD_OK;
   }
   return set_err(HVD_ERR_ARG, "unknown option");

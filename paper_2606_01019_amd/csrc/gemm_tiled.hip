@@ -6,9 +6,10 @@
 // streaming kernel: 1 KB fragments of 16 rows (or weight columns) x 32 K.
 // A workgroup of WY x WX waves owns a BM x BN tile (BM = 32 WM WY, BN =
 // 32 WN WX) and walks its K range in 32-wide steps: every step's A and W
-// fragments are copied into one of two LDS buffers (register-staged two steps
-// ahead, so the copy of step k+1 overlaps the MFMAs of step k), and each wave
-// multiplies its 32WM x 32WN sub-tile with WM x WN MFMA tiles of 32 x 32.
+// fragments are copied from global memory straight into a ring of ST LDS
+// slots (global_load_lds: no registers, ST - 1 steps in flight ahead of the
+// MFMAs), and each wave multiplies its 32WM x 32WN sub-tile with WM x WN
+// MFMA tiles of 32 x 32.
 // The 256 x 256 tile (8 waves) needs about 32 bytes of operand per clock and
 // CU at full MFMA rate; 128-row tiles (4 waves) serve smaller batches.
 // HI_LO chooses the activation precision: the fp16 hi + lo pair (two MFMAs
@@ -29,6 +30,24 @@
 namespace hvd {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits
+// 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+// Workgroup barrier without the memory fence of __syncthreads (whose release
+// would wait for every LDS copy in flight); the empty asm statements keep the
+// compiler from moving LDS accesses across it.
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 __device__ __forceinline__ f32x16 mfma32_f16(const u32x4& a, const u32x4& b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
@@ -196,9 +215,12 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
   }
 }
 
+// 128 x 128 wave tiles (256 accumulators) run one wave per SIMD
+constexpr int tiled_occupancy(int WM, int WN) { return WM * WN >= 16 ? 1 : 2; }
+
 template <int WY, int WX, int WM, int WN, int EPI, bool HI_LO>
-__global__ __launch_bounds__(64 * WY * WX, 2) void gemm_tiled(GemmArgs a, const float* __restrict__ inv_rms, int RB,
-                                                              int CB, int S) {
+__global__ __launch_bounds__(64 * WY * WX, tiled_occupancy(WM, WN)) void gemm_tiled(
+    GemmArgs a, const float* __restrict__ inv_rms, int RB, int CB, int S) {
   constexpr int NW = WY * WX;
   constexpr int BM = 32 * WM * WY, BN = 32 * WN * WX;
   constexpr int AF = BM / 16;              // A fragments per K step
@@ -207,7 +229,11 @@ __global__ __launch_bounds__(64 * WY * WX, 2) void gemm_tiled(GemmArgs a, const 
   constexpr int NF = NA + WF;
   constexpr int LPT = NF / NW;  // 16-byte loads per thread per K step (NF*64 / (64*NW))
   static_assert(NF % NW == 0, "fragments per step");
-  __shared__ u32x4 sbuf[2][NF][64];
+  // ring depth: two workgroups per CU for the small tiles, else one
+  constexpr int LDS_BUDGET = (NW == 4 && WM * WN < 16) ? 76 * 1024 : 150 * 1024;
+  constexpr int ST0 = LDS_BUDGET / (NF * 1024);
+  constexpr int ST = ST0 < 3 ? 3 : (ST0 > 6 ? 6 : ST0);
+  __shared__ u32x4 sbuf[ST][NF][64];
   __shared__ float2 lm_best[EPI == EPI_LM ? WX * BM : 1];
   __shared__ int lm_idx[EPI == EPI_LM ? WX * BM : 1];
 
@@ -236,15 +262,15 @@ __global__ __launch_bounds__(64 * WY * WX, 2) void gemm_tiled(GemmArgs a, const 
       kstride[q] = a.wk;
     }
   }
-  u32x4 ra[LPT], rb[LPT];
-  auto load = [&](u32x4 (&r)[LPT], int kt) __attribute__((always_inline)) {
-    kt = min(kt, ke - 1);  // steps past the range re-read the last one (dropped)
+  // copy K step kt into ring slot `slot`: lane l's 16 bytes land at
+  // sbuf[slot][f][l].  Steps past the range re-copy the last one, so every
+  // iteration issues the same number of copies (constant vmcnt targets).
+  auto issue = [&](int slot, int kt) __attribute__((always_inline)) {
+    kt = min(kt, ke - 1);
 #pragma unroll
-    for (int q = 0; q < LPT; ++q) r[q] = __builtin_nontemporal_load(src[q] + (size_t)kt * kstride[q]);
-  };
-  auto store = [&](const u32x4 (&r)[LPT], int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int q = 0; q < LPT; ++q) sbuf[buf][q * NW + wave][lane] = r[q];
+    for (int q = 0; q < LPT; ++q)
+      __builtin_amdgcn_global_load_lds((const void*)(src[q] + (size_t)kt * kstride[q]),
+                                       (lds_void*)&sbuf[slot][q * NW + wave][0], 16, 0, 0);
   };
 
   f32x16 acc[WM][WN];
@@ -259,45 +285,70 @@ __global__ __launch_bounds__(64 * WY * WX, 2) void gemm_tiled(GemmArgs a, const 
   // sub-step s (16 of the 32): lane l takes row l%32, K 16s + 8(l/32)..+8
   const int fl = (lane & 15) + 16 * (lane >> 5);  // lane within the fragment, s = 0
   const int fo = (lane >> 4) & 1;                 // second fragment for lanes 16-31 / 48-63
-  auto compute = [&](int buf) __attribute__((always_inline)) {
+  // the operands of one K step, held in registers: read from LDS one step
+  // ahead so the reads of step i+1 overlap the MFMAs of step i
+  struct Ops {
+    u32x4 ah[2][WM], al[2][HI_LO ? WM : 1], bw[2][WN];
+  };
+  auto read_ops = [&](int buf, Ops& o) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      u32x4 ah[WM], al[WM], bw[WN];
 #pragma unroll
       for (int i = 0; i < WM; ++i) {
-        ah[i] = sbuf[buf][wy * 2 * WM + 2 * i + fo][fl + 32 * s];
-        if constexpr (HI_LO) al[i] = sbuf[buf][AF + wy * 2 * WM + 2 * i + fo][fl + 32 * s];
+        o.ah[s][i] = sbuf[buf][wy * 2 * WM + 2 * i + fo][fl + 32 * s];
+        if constexpr (HI_LO) o.al[s][i] = sbuf[buf][AF + wy * 2 * WM + 2 * i + fo][fl + 32 * s];
       }
 #pragma unroll
-      for (int j = 0; j < WN; ++j) bw[j] = sbuf[buf][NA + wx * 2 * WN + 2 * j + fo][fl + 32 * s];
+      for (int j = 0; j < WN; ++j) o.bw[s][j] = sbuf[buf][NA + wx * 2 * WN + 2 * j + fo][fl + 32 * s];
+    }
+  };
+  // the MFMAs of one step; the first one goes out before `between` (the
+  // next step's LDS reads), so the register wait it needs covers only the
+  // previous step's reads, and the reads then overlap the remaining MFMAs
+  auto mfma_ops = [&](const Ops& o, auto&& between) __attribute__((always_inline)) {
+    acc[0][0] = mfma32_f16(o.ah[0][0], o.bw[0][0], acc[0][0]);
+    __builtin_amdgcn_sched_barrier(0);
+    between();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-          acc[i][j] = mfma32_f16(ah[i], bw[j], acc[i][j]);
-          if constexpr (HI_LO) acc[i][j] = mfma32_f16(al[i], bw[j], acc[i][j]);
+          if (s != 0 || i != 0 || j != 0) acc[i][j] = mfma32_f16(o.ah[s][i], o.bw[s][j], acc[i][j]);
+          if constexpr (HI_LO) acc[i][j] = mfma32_f16(o.al[s][i], o.bw[s][j], acc[i][j]);
         }
-    }
   };
 
-  if (kb < ke) {
-    load(ra, kb);
-    load(rb, kb + 1);
-    store(ra, 0);
-    __syncthreads();
-    load(ra, kb + 2);
-    for (int kk = kb; kk < ke; kk += 2) {
-      // buffer 0 holds step kk; rb holds kk+1, ra holds kk+2 (in flight)
-      compute(0);
-      store(rb, 1);
-      __syncthreads();
-      load(rb, kk + 3);
-      if (kk + 1 < ke) compute(1);
-      store(ra, 0);
-      __syncthreads();
-      load(ra, kk + 4);
+  // Ring schedule: step j lives in slot j % ST.  Iteration i waits until
+  // step i+1 has landed (own copies: vmcnt; everyone's: barrier), refills
+  // the slot of step i-1 with step i+ST-1, reads step i+1's operands and
+  // multiplies step i's (read in the previous iteration).
+  const int nk = ke - kb;
+  if (nk > 0) {
+    Ops o0, o1;
+#pragma unroll
+    for (int st = 0; st < ST - 1; ++st) issue(st, kb + st);
+    vm_wait<LPT * (ST - 2)>();
+    block_barrier();
+    read_ops(0, o0);
+    for (int i = 0; i < nk; i += 2) {
+      vm_wait<LPT * (ST - 3)>();
+      block_barrier();
+      issue((i + ST - 1) % ST, kb + i + ST - 1);
+      mfma_ops(o0, [&]() { read_ops((i + 1) % ST, o1); });
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + 1 < nk) {
+        vm_wait<LPT * (ST - 3)>();
+        block_barrier();
+        issue((i + ST) % ST, kb + i + ST);
+        mfma_ops(o1, [&]() { read_ops((i + 2) % ST, o0); });
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
+  vm_wait<0>();  // no copy may land after the workgroup's LDS is released
 
   const int row_w = tc.rb * BM + wy * 32 * WM;
   const int col_w = tc.cb * BN + wx * 32 * WN;
@@ -394,6 +445,7 @@ static hipError_t launch_th(const GemmArgs& a, const float* inv_rms, int tile, i
     case 0: return launch_t<2, 2, 2, 2, EPI, HI_LO>(a, inv_rms, splits, s);  // 128 x 128, 4 waves
     case 1: return launch_t<2, 2, 2, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 128 x 256, 4 waves
     case 2: return launch_t<4, 2, 2, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 256 x 256, 8 waves
+    case 3: return launch_t<2, 2, 4, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 256 x 256, 4 waves
   }
   return hipErrorInvalidValue;
 }

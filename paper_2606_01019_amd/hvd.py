@@ -21,6 +21,7 @@ EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes"
            "hvd_prefill", "hvd_verify", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
            "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error")
 HVD_OPT_GRAPHS = 1
+HVD_OPT_MLP_SINGLE = 2
 
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
@@ -135,9 +136,12 @@ class Model:
         self.handle = h
 
     def close(self):
+        """Release the handle and the device buffer (no KV cache of this model
+        may be used afterwards)."""
         if getattr(self, "handle", None):
             self.lib.hvd_model_free(self.handle)
             self.handle = None
+        self.buf = None
 
     def __del__(self):
         try:
@@ -208,6 +212,11 @@ class KVCache:
         _check(self.lib.hvd_seq_info(self.handle, seq_id, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
         return a.value, b.value, bool(c.value)
 
+    def set_mlp_single(self, on: bool):
+        """Large-batch verify MLP GEMMs on the fp16 activation alone (default)
+        or on the fp16 hi + lo pair."""
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_MLP_SINGLE, 1 if on else 0))
+
     def set_graphs(self, on: bool):
         """Replay step kernels from cached HIP graphs, or launch eagerly (default)."""
         _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_GRAPHS, 1 if on else 0))
@@ -225,8 +234,10 @@ class KVCache:
 
     def close(self):
         if getattr(self, "handle", None):
+            self.stream.synchronize()
             self.lib.hvd_kv_free(self.handle)
             self.handle = None
+        self.buf = None
 
     def __del__(self):
         try:
