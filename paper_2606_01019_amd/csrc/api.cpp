@@ -277,12 +277,15 @@ extern "C" void hvd_model_free(hvd_model m) {
 
 // ------------------------------------------------------------------ KV handle
 
+// A captured step is valid for every step with the same launch sequence:
+// rows, sequences, attention grid sizes and kernel variants (chunk length,
+// rows per item), LM head on/off and the logits pointer.
 struct GraphKey {
-  int M, B, n_items, n_heads, lm_head;
+  int M, B, n_items, n_heads, chunk, rpi, lm_head;
   float* logits;
   bool operator<(const GraphKey& o) const {
-    return std::tie(M, B, n_items, n_heads, lm_head, logits) <
-           std::tie(o.M, o.B, o.n_items, o.n_heads, o.lm_head, o.logits);
+    return std::tie(M, B, n_items, n_heads, chunk, rpi, lm_head, logits) <
+           std::tie(o.M, o.B, o.n_items, o.n_heads, o.chunk, o.rpi, o.lm_head, o.logits);
   }
 };
 
@@ -523,7 +526,7 @@ struct Plan {
 // Split every (sequence, kv head, row group) into KV chunks of `chunk`
 // positions, chosen so the launch has enough workgroups to fill the GPU.
 bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<SeqMeta>& seqs, int min_items,
-                    Plan& p) {
+                    int rpi, Plan& p) {
   const int G = c.n_q_heads / c.n_kv_heads;
   struct Unit { int b, g, rg, keys; };
   auto item = [&](const Unit& u, int c, int nch, int part, int chunk) {
@@ -548,10 +551,10 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   for (int b = 0; b < (int)seqs.size(); ++b) {
     const SeqMeta& s = seqs[b];
     const int R = (s.k + 1) * G;
-    const int n_rg = (R + kAttnRows - 1) / kAttnRows;
+    const int n_rg = (R + rpi - 1) / rpi;
     for (int g = 0; g < c.n_kv_heads; ++g)
       for (int rg = 0; rg < n_rg; ++rg) {
-        const int i_max = std::min(s.k, ((rg + 1) * kAttnRows - 1) / G);
+        const int i_max = std::min(s.k, ((rg + 1) * rpi - 1) / G);
         const int keys = s.ctx + i_max + 1;
         units.push_back({b, g, rg, keys});
         total_keys += keys;
@@ -575,7 +578,7 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
         slots += nch;
       }
     }
-    if (slots <= kPartSlots) break;
+    if ((size_t)slots * rpi <= (size_t)kPartSlots * kAttnRows) break;  // partial buffer rows
     if (chunk >= (1 << 20)) return false;
     // longer chunks: multiples of kAttnChunk above it (looped in LDS-sized pieces)
     chunk = chunk < kAttnChunk ? std::min(kAttnChunk, chunk * 2) : chunk * 2;
@@ -599,7 +602,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   const int G = c.n_q_heads / c.n_kv_heads;
 
   Plan plan;
-  if (!plan_attention(c, *k->hs, seqs, k->attn_min_items, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
+    // queries per kv head above one 4-wave item: 8-wave items read each key once
+  int max_rows = 0;
+  for (const SeqMeta& sq : seqs) max_rows = std::max(max_rows, (sq.k + 1) * (c.n_q_heads / c.n_kv_heads));
+  const int rpi = (max_rows > kAttnRows && c.head_dim == 128) ? 2 * kAttnRows : kAttnRows;
+  if (!plan_attention(c, *k->hs, seqs, k->attn_min_items, rpi, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
   std::vector<PageUpdate> upd_raw = k->hs->take_updates();
   // keep the last update of each (slot, index): they are applied in parallel
   std::map<std::pair<int, int>, int> last;
@@ -652,7 +659,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
 
   // ---------------------------------------------------------------- launches
   // Everything below only enqueues kernels whose arguments are fixed by
-  // (M, B, n_items, n_heads, lm_head, logits): captured once per shape into
+  // the GraphKey fields: captured once per shape into
   // a HIP graph and replayed (eager while profiling or with graphs off).
   auto launch_all = [&]() -> hvd_status {
   {
@@ -790,7 +797,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.part_ml = k->part_ml;
       {
         ProfScope ps(k, PF_ATTN, kv_bytes);
-        HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, s));
+        HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, rpi, s));
       }
       if (!plan.heads.empty()) {
         CombineArgs cb{};
@@ -804,6 +811,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         cb.Ohi = k->Ohi;
         cb.Olo = k->Olo;
         cb.MTtot = MT;
+        cb.rpi = rpi;
         ProfScope ps(k, PF_COMBINE, 0.0);
         HIP_TRY(launch_combine(cb, (int)plan.heads.size(), s));
       }
@@ -884,7 +892,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   if (k->prof || !k->use_graphs) {
     if (hvd_status st = launch_all(); st != HVD_OK) return st;
   } else {
-    const GraphKey key{M, B, (int)n_items, (int)n_heads, lm_head ? 1 : 0, logits};
+    const GraphKey key{M, B, (int)n_items, (int)n_heads, plan.chunk, rpi, lm_head ? 1 : 0, logits};
     auto it = k->graphs.find(key);
     if (it == k->graphs.end()) {
       if (k->graphs.size() >= kMaxGraphs) {

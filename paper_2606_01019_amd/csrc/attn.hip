@@ -34,15 +34,20 @@ typedef const __attribute__((address_space(4))) AttnItem ConstItem;
 typedef const __attribute__((address_space(4))) int32_t ConstI32;
 
 // NP = pages staged per sub-chunk (the launch picks it from the chunk
-// length), so short decode chunks issue only the loads they need.
-template <int DH, int NP>
-__global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
+// length), so short decode chunks issue only the loads they need.  NW waves
+// hold 2 row tiles each: an item covers up to 32*NW query rows (NW = 8 lets
+// one item cover all rows of a long draft, so its keys are read once).
+template <int DH, int NP, int NW>
+__global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
+  constexpr int NT = 64 * NW;           // threads
+  constexpr int RPI = 32 * NW;          // query rows per item
   constexpr int CH = NP * kPage;        // positions per sub-chunk
   constexpr int KSEG = DH / 8;          // 16-byte segments per K row
   constexpr int VU = CH / 4;            // 8-byte units per V row in LDS
   constexpr int VM = VU < 16 ? VU : 16; // V swizzle span (units)
-  constexpr int LPP = DH / 64;          // 16-byte loads per thread per page
+  constexpr int LPP = 4 * DH / NT;      // 16-byte loads per thread per page (K and V: 4*DH units)
   static_assert(NP >= 2 && NP <= kItemPages && (NP & (NP - 1)) == 0, "pages per sub-chunk");
+  static_assert(LPP >= 1 && LPP * NT == 4 * DH, "page units per thread");
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16* sK = (_Float16*)smem;                  // [CH][DH], segment-swizzled
   _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], 8-byte-unit-swizzled
@@ -70,7 +75,7 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
   f32x4 o[2][DH / 16];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const int row_base = rg * 128 + (wave + 4 * q) * 16;
+    const int row_base = rg * RPI + (wave + NW * q) * 16;
     tile_on[q] = row_base < R;
     tile_row[q] = row_base + (lane & 15);
 #pragma unroll
@@ -98,7 +103,7 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
     for (int p = 0; p < NP; ++p)
 #pragma unroll
       for (int j = 0; j < LPP; ++j) {
-        const int u = j * 256 + tid;
+        const int u = j * NT + tid;
         const size_t off = u < 2 * DH ? (size_t)u * 8 : vhalf + (size_t)(u - 2 * DH) * 8;
         buf[p][j] = *(const u32x4*)(kvg + (size_t)pgid[p] * a.page_stride + off);
       }
@@ -118,7 +123,7 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
     for (int p = 0; p < NP; ++p)
 #pragma unroll
       for (int j = 0; j < LPP; ++j) {
-        const int u = j * 256 + tid;
+        const int u = j * NT + tid;
         u32x4 x = buf[p][j];
         if (u < 2 * DH) {
           const int t = u / KSEG, sgm = u % KSEG;
@@ -239,8 +244,8 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
         }
       }
     } else {
-      const int lr = (wave + 4 * q) * 16 + (lane & 15);
-      const size_t ps = (size_t)part * 128 + lr;
+      const int lr = (wave + NW * q) * 16 + (lane & 15);
+      const size_t ps = (size_t)part * RPI + lr;
 #pragma unroll
       for (int dt = 0; dt < DH / 16; ++dt)
         *(float4*)(a.part_o + ps * DH + dt * 16 + lg * 4) =
@@ -254,23 +259,24 @@ __global__ __launch_bounds__(256) void verify_attn(AttnArgs a) {
 // order: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, as a running
 // (M, L, acc) merge over batches of 8 chunks whose loads are all issued
 // before any is used (the merge is latency-bound).  One block per (head
-// entry, 16-row slice); one thread per (row, 8 output dims).
+// entry, 16-row slice of its a.rpi rows); one thread per (row, 8 dims).
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   constexpr int OCT = DH / 8;
   constexpr int RPB = 256 / OCT;  // rows per block
   constexpr int NB = 8;           // chunks per batch
-  const AttnItem hd = a.heads[blockIdx.x / (128 / RPB)];
+  const int spb = a.rpi / RPB;    // blocks per head entry
+  const AttnItem hd = a.heads[blockIdx.x / spb];
   if (hd.k < 0) return;  // grid padding
-  const int slice = blockIdx.x % (128 / RPB);
+  const int slice = blockIdx.x % spb;
   const int G = a.group;
   const int R = (hd.k + 1) * G;
   const int lr = slice * RPB + threadIdx.x / OCT, o8 = (threadIdx.x % OCT) * 8;
-  const int r = hd.rg * 128 + lr;
+  const int r = hd.rg * a.rpi + lr;
   if (r >= R) return;
-  const float* ml = a.part_ml + ((size_t)hd.part * 128 + lr) * 2;
-  const float* po = a.part_o + ((size_t)hd.part * 128 + lr) * DH + o8;
-  const size_t cstride_ml = (size_t)128 * 2, cstride_o = (size_t)128 * DH;
+  const float* ml = a.part_ml + ((size_t)hd.part * a.rpi + lr) * 2;
+  const float* po = a.part_o + ((size_t)hd.part * a.rpi + lr) * DH + o8;
+  const size_t cstride_ml = (size_t)a.rpi * 2, cstride_o = (size_t)a.rpi * DH;
   float M = -INFINITY, L = 0.f;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   for (int c0 = 0; c0 < hd.nch; c0 += NB) {
@@ -323,54 +329,65 @@ int attn_pages_per_sub(int chunk) {
 
 size_t attn_lds_bytes(int dh, int np) { return (size_t)np * kPage * dh * 2 * 2; }
 
-template <int DH>
+template <int DH, int NW>
 static hipError_t launch_attn_dh(const AttnArgs& a, int n_items, int np, hipStream_t s) {
   const size_t lds = attn_lds_bytes(DH, np);
+  const dim3 block(64 * NW);
   switch (np) {
-    case 2: hipLaunchKernelGGL((verify_attn<DH, 2>), dim3(n_items), dim3(256), lds, s, a); break;
-    case 4: hipLaunchKernelGGL((verify_attn<DH, 4>), dim3(n_items), dim3(256), lds, s, a); break;
-    case 8: hipLaunchKernelGGL((verify_attn<DH, 8>), dim3(n_items), dim3(256), lds, s, a); break;
-    case 16: hipLaunchKernelGGL((verify_attn<DH, 16>), dim3(n_items), dim3(256), lds, s, a); break;
+    case 2: hipLaunchKernelGGL((verify_attn<DH, 2, NW>), dim3(n_items), block, lds, s, a); break;
+    case 4: hipLaunchKernelGGL((verify_attn<DH, 4, NW>), dim3(n_items), block, lds, s, a); break;
+    case 8: hipLaunchKernelGGL((verify_attn<DH, 8, NW>), dim3(n_items), block, lds, s, a); break;
+    case 16: hipLaunchKernelGGL((verify_attn<DH, 16, NW>), dim3(n_items), block, lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, hipStream_t s) {
+hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  const int np = attn_pages_per_sub(chunk);
-  if (a.dh == 128) return launch_attn_dh<128>(a, n_items, np, s);
-  if (a.dh == 64) return launch_attn_dh<64>(a, n_items, np, s);
+  int np = attn_pages_per_sub(chunk);
+  if (rows_per_item == 256) {
+    // 8 waves of 2 row tiles: sub-chunks of at most 8 pages keep the staging
+    // registers within two waves per SIMD
+    if (a.dh != 128) return hipErrorInvalidValue;
+    return launch_attn_dh<128, 8>(a, n_items, np < 8 ? np : 8, s);
+  }
+  if (rows_per_item != 128) return hipErrorInvalidValue;
+  if (a.dh == 128) return launch_attn_dh<128, 4>(a, n_items, np, s);
+  if (a.dh == 64) return launch_attn_dh<64, 4>(a, n_items, np, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s) {
   if (n_heads <= 0) return hipSuccess;
   if (a.dh == 128)
-    hipLaunchKernelGGL(attn_combine<128>, dim3(n_heads * 8), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_combine<128>, dim3(n_heads * (a.rpi / 16)), dim3(256), 0, s, a);
   else if (a.dh == 64)
-    hipLaunchKernelGGL(attn_combine<64>, dim3(n_heads * 4), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_combine<64>, dim3(n_heads * (a.rpi / 32)), dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-template <int DH, int NP>
+template <int DH, int NP, int NW>
 static hipError_t set_lds(void) {
-  return hipFuncSetAttribute((const void*)verify_attn<DH, NP>, hipFuncAttributeMaxDynamicSharedMemorySize,
+  return hipFuncSetAttribute((const void*)verify_attn<DH, NP, NW>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)attn_lds_bytes(DH, NP));
 }
 
 hipError_t attn_set_lds_limit() {
   hipError_t e = hipSuccess;
-  if (e == hipSuccess) e = set_lds<128, 2>();
-  if (e == hipSuccess) e = set_lds<128, 4>();
-  if (e == hipSuccess) e = set_lds<128, 8>();
-  if (e == hipSuccess) e = set_lds<128, 16>();
-  if (e == hipSuccess) e = set_lds<64, 2>();
-  if (e == hipSuccess) e = set_lds<64, 4>();
-  if (e == hipSuccess) e = set_lds<64, 8>();
-  if (e == hipSuccess) e = set_lds<64, 16>();
+  if (e == hipSuccess) e = set_lds<128, 2, 4>();
+  if (e == hipSuccess) e = set_lds<128, 4, 4>();
+  if (e == hipSuccess) e = set_lds<128, 8, 4>();
+  if (e == hipSuccess) e = set_lds<128, 16, 4>();
+  if (e == hipSuccess) e = set_lds<128, 2, 8>();
+  if (e == hipSuccess) e = set_lds<128, 4, 8>();
+  if (e == hipSuccess) e = set_lds<128, 8, 8>();
+  if (e == hipSuccess) e = set_lds<64, 2, 4>();
+  if (e == hipSuccess) e = set_lds<64, 4, 4>();
+  if (e == hipSuccess) e = set_lds<64, 8, 4>();
+  if (e == hipSuccess) e = set_lds<64, 16, 4>();
   return e;
 }
 

@@ -90,8 +90,8 @@ struct AttnArgs {
   uint16_t* Ohi;       // O GEMM A operand (K = Hq*dh)
   uint16_t* Olo;
   int MTtot;
-  float* part_o;       // [slots][128][dh] fp32 unnormalized output of one chunk
-  float* part_ml;      // [slots][128][2] running max (base 2) and sum
+  float* part_o;       // [slots][rows per item][dh] fp32 unnormalized output of one chunk
+  float* part_ml;      // [slots][rows per item][2] running max (base 2) and sum
 };
 
 struct CombineArgs {
@@ -102,6 +102,7 @@ struct CombineArgs {
   uint16_t* Ohi;
   uint16_t* Olo;
   int MTtot;
+  int rpi;  // query rows per work item (partial slot stride)
 };
 
 struct EmbedArgs {
@@ -147,8 +148,9 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mbloc
 // (computed here for normalised inputs).
 hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, int splits, float* inv_rms,
                              hipStream_t s);
-// chunk: the plan's KV chunk length (picks the pages staged per sub-chunk)
-hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, hipStream_t s);
+// chunk: the plan's KV chunk length (picks the pages staged per sub-chunk);
+// rows_per_item: 128 (4 waves) or 256 (8 waves, head_dim 128)
+hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, hipStream_t s);
 hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
