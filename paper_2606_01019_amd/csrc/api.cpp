@@ -495,11 +495,11 @@ struct ProfScope {
     r.b = take_event(k);
     r.family = family;
     r.bytes = bytes;
-    (void)hipEventRecord(r.a, k->stream);
+    tl_timing = LaunchTiming{r.a, r.b};  // the role's kernels record the events
   }
   ~ProfScope() {
     if (!k->prof) return;
-    (void)hipEventRecord(r.b, k->stream);
+    tl_timing = LaunchTiming{};
     k->prof_pending.push_back(r);
   }
 };

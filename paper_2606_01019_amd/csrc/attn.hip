@@ -334,10 +334,10 @@ static hipError_t launch_attn_dh(const AttnArgs& a, int n_items, int np, hipStre
   const size_t lds = attn_lds_bytes(DH, np);
   const dim3 block(64 * NW);
   switch (np) {
-    case 2: hipLaunchKernelGGL((verify_attn<DH, 2, NW>), dim3(n_items), block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((verify_attn<DH, 4, NW>), dim3(n_items), block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((verify_attn<DH, 8, NW>), dim3(n_items), block, lds, s, a); break;
-    case 16: hipLaunchKernelGGL((verify_attn<DH, 16, NW>), dim3(n_items), block, lds, s, a); break;
+    case 2: hvd_launch((verify_attn<DH, 2, NW>), dim3(n_items), block, lds, s, a); break;
+    case 4: hvd_launch((verify_attn<DH, 4, NW>), dim3(n_items), block, lds, s, a); break;
+    case 8: hvd_launch((verify_attn<DH, 8, NW>), dim3(n_items), block, lds, s, a); break;
+    case 16: hvd_launch((verify_attn<DH, 16, NW>), dim3(n_items), block, lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -361,9 +361,9 @@ hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_i
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s) {
   if (n_heads <= 0) return hipSuccess;
   if (a.dh == 128)
-    hipLaunchKernelGGL(attn_combine<128>, dim3(n_heads * (a.rpi / 16)), dim3(256), 0, s, a);
+    hvd_launch(attn_combine<128>, dim3(n_heads * (a.rpi / 16)), dim3(256), 0, s, a);
   else if (a.dh == 64)
-    hipLaunchKernelGGL(attn_combine<64>, dim3(n_heads * (a.rpi / 32)), dim3(256), 0, s, a);
+    hvd_launch(attn_combine<64>, dim3(n_heads * (a.rpi / 32)), dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -576,8 +576,8 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
 #define HVD_CASE(X)                                                                                     \
   case X:                                                                                               \
     if constexpr (NS * X <= 16) {                                                                       \
-      hipLaunchKernelGGL((gemm_skinny<X, NS, EPI>), grid, dim3(512), 0, s, a);                          \
-      if (splits > 1) hipLaunchKernelGGL((gemm_finish<X, NS, EPI>), fgrid, dim3(512), 0, s, a, splits); \
+      hvd_launch((gemm_skinny<X, NS, EPI>), grid, dim3(512), 0, s, a);                          \
+      if (splits > 1) hvd_launch((gemm_finish<X, NS, EPI>), fgrid, dim3(512), 0, s, a, splits); \
       break;                                                                                            \
     } else {                                                                                            \
       return hipErrorInvalidValue;                                                                      \

@@ -431,10 +431,10 @@ static hipError_t launch_t(const GemmArgs& a, const float* inv_rms, int splits, 
   const int BM = 32 * WM * WY, BN = 32 * WN * WX, NT = 64 * WY * WX;
   const int CB = a.NT * 16 / BN, RB = (a.MTtot * 16 + BM - 1) / BM;
   const int total = CB * RB * splits;
-  hipLaunchKernelGGL((gemm_tiled<WY, WX, WM, WN, EPI, HI_LO>), dim3(total), dim3(NT), 0, s, a, inv_rms, RB, CB,
+  hvd_launch((gemm_tiled<WY, WX, WM, WN, EPI, HI_LO>), dim3(total), dim3(NT), 0, s, a, inv_rms, RB, CB,
                      splits);
   if (splits > 1)
-    hipLaunchKernelGGL((gemm_tiled_finish<WY, WX, WM, WN, EPI>), dim3(CB * RB), dim3(NT), 0, s, a, inv_rms, RB, CB,
+    hvd_launch((gemm_tiled_finish<WY, WX, WM, WN, EPI>), dim3(CB * RB), dim3(NT), 0, s, a, inv_rms, RB, CB,
                        splits);
   return hipGetLastError();
 }
@@ -459,7 +459,7 @@ hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, i
                              hipStream_t s) {
   if (epi != EPI_RESID) {
     const int rows = a.MTtot * 16;
-    hipLaunchKernelGGL(row_inv_rms, dim3((rows + 3) / 4), dim3(256), 0, s, a.ss, a.ss_n, rows, a.inv_dim, a.eps,
+    hvd_launch(row_inv_rms, dim3((rows + 3) / 4), dim3(256), 0, s, a.ss, a.ss_n, rows, a.inv_dim, a.eps,
                        inv_rms);
   }
   switch (epi) {

@@ -2,9 +2,29 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 namespace hvd {
+
+// Per-role kernel timing (profiling only): while a role's scope is open, its
+// launches go through hipExtLaunchKernel with these events, so `start` marks
+// the start of the role's first kernel and `stop` the end of its last one
+// (kernel execution only, as a kernel trace measures it).
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchTiming tl_timing;
+
+template <typename F, typename... Args>
+inline void hvd_launch(F kernel, const dim3& grid, const dim3& block, uint32_t lds, hipStream_t s, Args... args) {
+  if (tl_timing.start != nullptr || tl_timing.stop != nullptr) {
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, s, tl_timing.start, tl_timing.stop, 0u, args...);
+    tl_timing.start = nullptr;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+  }
+}
 
 constexpr int kPage = 16;        // tokens per KV page
 constexpr int kAttnChunk = 256;  // most KV positions one attention workgroup stages in LDS

@@ -6,6 +6,8 @@
 
 namespace hvd {
 
+thread_local LaunchTiming tl_timing;
+
 // dst fragment (strip s, K step kt), lane l, half j =
 //   fp16(src[rowmap[16 s + l%16]][32 kt + 8 (l/16) + j])   (src bf16)
 // stored at ((s/4 * KT + kt) * 4 + s%4) * 512 halves: the 4 strips of a
@@ -38,7 +40,7 @@ hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst
   size_t total = (size_t)(N / 16) * (K / 32) * 64;
   int blocks = (int)((total + 255) / 256);
   if (blocks > 65535 * 8) blocks = 65535 * 8;
-  hipLaunchKernelGGL(pack_weight, dim3(blocks), dim3(256), 0, s, src, rowmap, dst, N, K);
+  hvd_launch(pack_weight, dim3(blocks), dim3(256), 0, s, src, rowmap, dst, N, K);
   return hipGetLastError();
 }
 
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
 }
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(embed_rows, dim3(a.Mpad), dim3(256), 0, s, a);
+  hvd_launch(embed_rows, dim3(a.Mpad), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -149,7 +151,7 @@ __global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(argmax_accept, dim3(a.M), dim3(256), 0, s, a);
+  hvd_launch(argmax_accept, dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
