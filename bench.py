@@ -48,6 +48,28 @@ def algorithmic_bytes(cfg, ctx, k):
     return weights + kv
 
 
+def counter_traffic():
+    """HBM bytes per launch of the gate/up GEMM from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE record (profiles/), or None when the kernel source
+    changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gateup_gemm_8b_b1_hbm_counters.md")
+    if not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-record:"):
+                rec = json.loads(line.split(":", 1)[1])
+    if rec is None:
+        return None
+    h = hashlib.sha256()
+    for name in ("gemm.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2606_01019_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return rec["traffic_bytes_per_launch"] if h.hexdigest()[:16] == rec["source_sha256_16"] else None
+
+
 def layer_params(cfg):
     D, F = cfg.d_model, cfg.ffn_dim
     return D * (cfg.q_dim + 2 * cfg.kv_dim) + cfg.q_dim * D + 3 * D * F
@@ -157,9 +179,11 @@ def leg_long_context(model, reps):
         sweep[str(k)] = t * 1e6
         if k >= 32:
             r = rooflines(cfg, [(n - 1, k)], t)
+            fam = profiled_families(kv, [0], [d])
             cache_legs.append({"k": k, "planted": a_plan, "accepted": acc[0], "latency_us": t * 1e6,
                                "committed_tokens_per_s": (acc[0] + 1) / t, "hbm_frac": r["hbm_frac"],
-                               "mfma_frac": r["mfma_frac"]})
+                               "mfma_frac": r["mfma_frac"],
+                               "kernel_families_ms": {f: v["ms"] for f, v in fam.items()}})
     kv.close()
     return {"workload": f"8B shape, batch 1, context {n} (64-token segments, 16 bases, 20% mutation), cache "
                         f"drafts k = 32/48/64 planted bimodal",
@@ -310,7 +334,19 @@ def main():
     ap.add_argument("--workloads", default="long_context,mixed_batch,multistep_32b",
                     help="extra workloads reported beside the headline (comma list, '' for none)")
     ap.add_argument("--reps", type=int, default=5, help="repeats per timed step of the extra workloads")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES a few times (reference for HBM counters)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n * 4}))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the verify step of one "
               f"sequence batch does not shard across GPUs in this build", file=sys.stderr)
@@ -426,7 +462,8 @@ def main():
                           "frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
         "roofline": {"bound": "hbm", "kernel": f"gemm_skinny {dom} GEMM (incl. its split-K finish pass, if any)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "avg_launch_us": d_ms * 1e3 / max(d_n, 1), "launches": d_n,
+                     "traffic": counter_traffic() if dom == "gateup" else None,
+                     "avg_launch_us": d_ms * 1e3 / max(d_n, 1), "launches": d_n,
                      "bytes_per_launch": d_b / max(d_n, 1)},
         "kernel_families": fam,
     }
