@@ -171,11 +171,11 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   measured slightly faster for single-sequence verifies.  Results are
  *   identical either way.  Profiling (hvd_profile_enable) always launches
  *   eagerly.
- * HVD_OPT_MLP_SINGLE (default 1): in verify forwards of more than 64 rows
- *   (the MFMA-bound regime), the gate/up and down GEMMs take the fp16
- *   activation alone (11 bits) instead of the fp16 hi + lo pair (~22 bits),
- *   halving their MFMA work; 0 keeps the pair.  Prefill always uses the
- *   pair.  Logit differences stay within the verify step's tolerance. */
+ * HVD_OPT_MLP_SINGLE (default 1): in verify forwards of more than 32 rows,
+ *   the gate/up and down GEMMs take the fp16 activation alone (11 bits)
+ *   instead of the fp16 hi + lo pair (~22 bits), halving their activation
+ *   traffic and MFMA work; 0 keeps the pair.  Prefill always uses the pair.
+ *   Logit differences stay within the verify step's tolerance. */
 enum { HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2 };
 hvd_status hvd_kv_set_option(hvd_kv kv, int32_t option, int32_t value);
 

@@ -746,7 +746,9 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.n_part = lm_parts;
     }
     ProfScope ps(k, family, (double)N * K * 2.0);
-    HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, s));
+    // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
+    const bool single = k->mlp_single && lm_head && MT > 2 && (epi == EPI_SILU || family == PF_DOWN);
+    HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, !single, s));
     return HVD_OK;
   };
   double kv_bytes = 0;

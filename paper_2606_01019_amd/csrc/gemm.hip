@@ -43,9 +43,9 @@ namespace hvd {
 // (A one-workgroup-per-CU variant with a 16-stage queue measured no faster:
 // these launches are not limited by weight bytes in flight.)
 constexpr int gemm_occupancy(int MT) { return MT <= 2 ? 4 : 2; }
-constexpr int gemm_depth(int MT, int NS) {
-  const int budget = gemm_occupancy(MT) == 4 ? 80 : 160;
-  const int d = budget / (4 * (NS + 2 * MT));
+constexpr int gemm_depth(int MT, int NS, bool HL) {
+  const int budget = gemm_occupancy(MT) == 4 ? 80 : (HL ? 160 : 128);
+  const int d = budget / (4 * (NS + (HL ? 2 : 1) * MT));
   return d < 1 ? 1 : (d > 8 ? 8 : d);
 }
 
@@ -369,9 +369,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[N
   }
 }
 
-template <int MT, int NS, int EPI>
+// HL: activation as the fp16 hi + lo pair (two MFMAs per tile), or the hi
+// part alone (one MFMA; used for the MLP GEMMs of verify batches over 32 rows)
+template <int MT, int NS, int EPI, bool HL>
 __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs a) {
-  constexpr int U = gemm_depth(MT, NS);
+  constexpr int U = gemm_depth(MT, NS, HL);
   constexpr int ROWS = MT * 16;
   constexpr int COLS = NS * 16;
 
@@ -418,7 +420,7 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   // Stage u of the prefetch queue holds the fragments of one K step.  Row
   // tiles past this block's last are read from the operand's padding and
   // computed, then dropped (no per-tile branches in the loop).
-  u32x4 qb[U][NS], qh[U][MT], ql[U][MT];
+  u32x4 qb[U][NS], qh[U][MT], ql[U][HL ? MT : 1];
   auto load = [&](int u, int j) __attribute__((always_inline)) {
     const int kt = kb + j * kKG;
 #pragma unroll
@@ -426,7 +428,7 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       qh[u][m] = hp[kt * astride + m * 64 + lane];
-      ql[u][m] = lp[kt * astride + m * 64 + lane];
+      if constexpr (HL) ql[u][m] = lp[kt * astride + m * 64 + lane];
     }
   };
   auto consume = [&](int u) __attribute__((always_inline)) {
@@ -435,7 +437,7 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
 #pragma unroll
       for (int n = 0; n < NS; ++n) {
         acc[m][n] = mfma_f16(qh[u][m], qb[u][n], acc[m][n]);
-        acc[m][n] = mfma_f16(ql[u][m], qb[u][n], acc[m][n]);
+        if constexpr (HL) acc[m][n] = mfma_f16(ql[u][m], qb[u][n], acc[m][n]);
       }
   };
 
@@ -567,47 +569,62 @@ __global__ __launch_bounds__(512) void gemm_finish(GemmArgs a, int splits) {
   gemm_epilogue<MT, NS, EPI>(a, tile, pre, cb, mt0, mcount);
 }
 
+template <int MT, int NS, int EPI, bool HL>
+static void launch_one(const GemmArgs& a, int splits, int mblocks, hipStream_t s) {
+  const dim3 grid(a.NT / NS, splits, mblocks), fgrid(a.NT / NS, 1, mblocks);
+  hvd_launch((gemm_skinny<MT, NS, EPI, HL>), grid, dim3(512), 0, s, a);
+  if (splits > 1) hvd_launch((gemm_finish<MT, NS, EPI>), fgrid, dim3(512), 0, s, a, splits);
+}
+
 template <int NS, int EPI>
-static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, hipStream_t s) {
-  dim3 grid(a.NT / NS, splits, mblocks);
-  dim3 fgrid(a.NT / NS, 1, mblocks);
+static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, bool hi_lo, hipStream_t s) {
+  // single-pass activations only for the MLP GEMMs at 3-4 row tiles
+  constexpr bool kSingle = EPI == EPI_SILU || EPI == EPI_RESID;
   switch (mt) {
-// (8-strip blocks only up to 2 row tiles: LDS)
-#define HVD_CASE(X)                                                                                     \
-  case X:                                                                                               \
-    if constexpr (NS * X <= 16) {                                                                       \
-      hvd_launch((gemm_skinny<X, NS, EPI>), grid, dim3(512), 0, s, a);                          \
-      if (splits > 1) hvd_launch((gemm_finish<X, NS, EPI>), fgrid, dim3(512), 0, s, a, splits); \
-      break;                                                                                            \
-    } else {                                                                                            \
-      return hipErrorInvalidValue;                                                                      \
-    }
-    HVD_CASE(1) HVD_CASE(2) HVD_CASE(3) HVD_CASE(4)
-#undef HVD_CASE
+    case 1: launch_one<1, NS, EPI, true>(a, splits, mblocks, s); break;
+    case 2: launch_one<2, NS, EPI, true>(a, splits, mblocks, s); break;
+    case 3:
+    case 4:
+      if constexpr (NS <= 4) {  // 8-strip blocks only up to 2 row tiles (LDS)
+        if (kSingle && !hi_lo) {
+          if constexpr (kSingle) {
+            if (mt == 3) launch_one<3, NS, EPI, false>(a, splits, mblocks, s);
+            else launch_one<4, NS, EPI, false>(a, splits, mblocks, s);
+          }
+        } else if (mt == 3) {
+          launch_one<3, NS, EPI, true>(a, splits, mblocks, s);
+        } else {
+          launch_one<4, NS, EPI, true>(a, splits, mblocks, s);
+        }
+        break;
+      } else {
+        return hipErrorInvalidValue;
+      }
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 template <int EPI>
-static hipError_t launch_epi(const GemmArgs& a, int ns, int splits, int mblocks, int mt, hipStream_t s) {
+static hipError_t launch_epi(const GemmArgs& a, int ns, int splits, int mblocks, int mt, bool hi_lo, hipStream_t s) {
   switch (ns) {
     case 1:
-      if constexpr (EPI != EPI_SILU) return launch_ns<1, EPI>(a, splits, mblocks, mt, s);
+      if constexpr (EPI != EPI_SILU) return launch_ns<1, EPI>(a, splits, mblocks, mt, hi_lo, s);
       return hipErrorInvalidValue;
-    case 2: return launch_ns<2, EPI>(a, splits, mblocks, mt, s);
-    case 4: return launch_ns<4, EPI>(a, splits, mblocks, mt, s);
-    case 8: return launch_ns<8, EPI>(a, splits, mblocks, mt, s);
+    case 2: return launch_ns<2, EPI>(a, splits, mblocks, mt, hi_lo, s);
+    case 4: return launch_ns<4, EPI>(a, splits, mblocks, mt, hi_lo, s);
+    case 8: return launch_ns<8, EPI>(a, splits, mblocks, mt, hi_lo, s);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, hipStream_t s) {
+hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, bool hi_lo,
+                       hipStream_t s) {
   switch (epi) {
-    case EPI_QKV: return launch_epi<EPI_QKV>(a, ns, splits, mblocks, mt_block, s);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, ns, splits, mblocks, mt_block, s);
-    case EPI_SILU: return launch_epi<EPI_SILU>(a, ns, splits, mblocks, mt_block, s);
-    case EPI_LM: return launch_epi<EPI_LM>(a, ns, splits, mblocks, mt_block, s);
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, ns, splits, mblocks, mt_block, hi_lo, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, ns, splits, mblocks, mt_block, hi_lo, s);
+    case EPI_SILU: return launch_epi<EPI_SILU>(a, ns, splits, mblocks, mt_block, hi_lo, s);
+    case EPI_LM: return launch_epi<EPI_LM>(a, ns, splits, mblocks, mt_block, hi_lo, s);
   }
   return hipErrorInvalidValue;
 }

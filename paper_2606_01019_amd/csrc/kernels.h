@@ -161,7 +161,10 @@ hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 // ns: 16-column strips per workgroup (1, 2, 4; >= 2 for EPI_SILU); grid.x = NT / ns.
 // splits > 1 splits K across workgroups and adds the gemm_finish pass.
-hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, hipStream_t s);
+// hi_lo false: the hi activation part alone (honoured for the residual and
+// SiLU GEMMs at 3-4 row tiles; other shapes keep the pair)
+hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, bool hi_lo,
+                       hipStream_t s);
 // Large-batch GEMM (gemm_tiled.hip): tile 0 = 128 x 128, 1 = 128 x 256,
 // 2 = 256 x 256 (rows x columns); hi_lo false = the hi activation part
 // alone; K split `splits` ways; inv_rms is a per-row scratch vector
