@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <map>
@@ -281,11 +282,11 @@ extern "C" void hvd_model_free(hvd_model m) {
 // rows, sequences, attention grid sizes and kernel variants (chunk length,
 // rows per item), LM head on/off and the logits pointer.
 struct GraphKey {
-  int M, B, n_items, n_heads, chunk, rpi, lm_head;
+  int M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head;
   float* logits;
   bool operator<(const GraphKey& o) const {
-    return std::tie(M, B, n_items, n_heads, chunk, rpi, lm_head, logits) <
-           std::tie(o.M, o.B, o.n_items, o.n_heads, o.chunk, o.rpi, o.lm_head, o.logits);
+    return std::tie(M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head, logits) <
+           std::tie(o.M, o.B, o.n_items, o.n_heads, o.chunk, o.rpi, o.comb_rows, o.lm_head, o.logits);
   }
 };
 
@@ -321,6 +322,7 @@ struct hvd_kv_s {
   bool use_graphs = false;
   std::map<GraphKey, hipGraphExec_t> graphs;
   int attn_min_items = kAttnMinItems;
+  int gemm_force[PF_LM + 1][2] = {};  // per GEMM family: {strips per workgroup, K splits} of the skinny kernel, 0 = policy
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
   bool mlp_single = true;    // large-batch verify MLP GEMMs on the hi activation part only
@@ -447,6 +449,26 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_GRAPHS")) k->use_graphs = atoi(e) != 0;
+  // tuning override of the skinny GEMM shape: "qkv=2:1,o=1:1" (family=strips:splits)
+  if (const char* e = getenv("HVD_GEMM_SHAPE")) {
+    static const char* names[PF_LM + 1] = {"qkv", "o", "gateup", "down", "lm"};
+    std::string spec(e);
+    size_t at = 0;
+    while (at < spec.size()) {
+      size_t end = spec.find(',', at);
+      if (end == std::string::npos) end = spec.size();
+      const std::string item = spec.substr(at, end - at);
+      int ns = 0, sp = 0;
+      const size_t eq = item.find('=');
+      if (eq != std::string::npos && sscanf(item.c_str() + eq + 1, "%d:%d", &ns, &sp) == 2)
+        for (int f = 0; f <= PF_LM; ++f)
+          if (item.compare(0, eq, names[f]) == 0 && (ns == 1 || ns == 2 || ns == 4 || ns == 8) && sp >= 1 && sp <= 16) {
+            k->gemm_force[f][0] = ns;
+            k->gemm_force[f][1] = sp;
+          }
+      at = end + 1;
+    }
+  }
   if (hipError_t e = attn_set_lds_limit(); e != hipSuccess) {
     hvd_kv_free(k);
     return set_err(HVD_ERR_DEVICE, std::string("attention LDS limit: ") + hipGetErrorString(e));
@@ -560,10 +582,12 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
         total_keys += keys;
       }
   }
-  // smallest chunk (multiple of 32, <= kAttnChunk) that still yields about
-  // min_items workgroups; longer chunks mean fewer partials to combine
-  int chunk = (int)((total_keys + min_items - 1) / min_items);
-  chunk = std::max(32, std::min(kAttnChunk, (chunk + 31) / 32 * 32));
+  // chunk: a power-of-two number of pages (32..kAttnChunk positions, the
+  // kernel's sub-chunk sizes, so only a head's last chunk is partial), the
+  // largest that still yields about min_items workgroups
+  const int64_t want = (total_keys + min_items - 1) / min_items;
+  int chunk = 32;
+  while (chunk < kAttnChunk && 2 * chunk <= want) chunk *= 2;
   for (;;) {
     p.items.clear();
     p.heads.clear();
@@ -602,10 +626,13 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   const int G = c.n_q_heads / c.n_kv_heads;
 
   Plan plan;
-    // queries per kv head above one 4-wave item: 8-wave items read each key once
+  // query rows per item: 64 (one 4-wave tile set), 128, or 256 (head dim
+  // 128) when a kv head has more, so each key is read once per item
   int max_rows = 0;
   for (const SeqMeta& sq : seqs) max_rows = std::max(max_rows, (sq.k + 1) * (c.n_q_heads / c.n_kv_heads));
-  const int rpi = (max_rows > kAttnRows && c.head_dim == 128) ? 2 * kAttnRows : kAttnRows;
+  const int rpi = max_rows <= kAttnRows / 2 ? kAttnRows / 2
+                  : (max_rows > kAttnRows && c.head_dim == 128) ? 2 * kAttnRows : kAttnRows;
+  const int comb_rows = std::max(1, std::min(rpi, max_rows));  // rows of the largest combine entry
   if (!plan_attention(c, *k->hs, seqs, k->attn_min_items, rpi, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
   std::vector<PageUpdate> upd_raw = k->hs->take_updates();
   // keep the last update of each (slot, index): they are applied in parallel
@@ -688,8 +715,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // Workgroup shape per GEMM (measured on the 8B verify shapes): 4 strips
   // per workgroup when that alone gives enough workgroups (8 for two row
   // tiles, which halves the activation fragments per weight byte); for
-  // long-K GEMMs 4 strips plus a K split; otherwise 2 strips, K-split if
-  // still too few.
+  // long-K GEMMs 4 strips plus a K split; otherwise 2 strips, or for one
+  // row tile 1 strip when that fills the GPU; K-split if still too few.
   int lm_parts = 0;
   auto gemm = [&](int epi, GemmArgs& a, int N, int K, int family) -> hvd_status {
     a.KT = K / 32;
@@ -736,9 +763,19 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       splits = std::max(1, std::min((kGemmSplitTarget + nb4 - 1) / nb4, a.KT / 64));
     } else if (nb2 >= want) {
       ns = 2;
+    } else if (mt_block == 1 && epi != EPI_SILU && nb2 * 2 >= want) {
+      ns = 1;  // one strip per workgroup beats a K split plus its finish pass
     } else {
       ns = 2;
       splits = std::max(1, std::min((kGemmSplitTarget + nb2 - 1) / nb2, a.KT / 64));
+    }
+    if (family <= PF_LM && k->gemm_force[family][0]) {
+      const int fns = k->gemm_force[family][0];
+      const bool ok = a.NT % fns == 0 && !(fns == 1 && epi == EPI_SILU) && !(fns == 8 && (mt_block > 2 || N % 128));
+      if (ok) {
+        ns = fns;
+        splits = std::min(k->gemm_force[family][1], a.KT);
+      }
     }
     while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > kGemmPartBytes) --splits;
     if (epi == EPI_LM) {
@@ -814,6 +851,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         cb.Olo = k->Olo;
         cb.MTtot = MT;
         cb.rpi = rpi;
+        cb.max_rows = comb_rows;
         ProfScope ps(k, PF_COMBINE, 0.0);
         HIP_TRY(launch_combine(cb, (int)plan.heads.size(), s));
       }
@@ -894,7 +932,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   if (k->prof || !k->use_graphs) {
     if (hvd_status st = launch_all(); st != HVD_OK) return st;
   } else {
-    const GraphKey key{M, B, (int)n_items, (int)n_heads, plan.chunk, rpi, lm_head ? 1 : 0, logits};
+    const GraphKey key{M, B, (int)n_items, (int)n_heads, plan.chunk, rpi, comb_rows, lm_head ? 1 : 0, logits};
     auto it = k->graphs.find(key);
     if (it == k->graphs.end()) {
       if (k->graphs.size() >= kMaxGraphs) {

@@ -21,7 +21,7 @@
 // positions >= ctx+k+1 are never used (their contents may be stale).
 // A single-chunk item writes the normalized output straight into the O GEMM's
 // hi/lo operand; multi-chunk items write (m, l, unnormalized O) partials that
-// attn_combine merges in chunk order.
+// attn_combine merges.
 #include "common.h"
 #include "kernels.h"
 
@@ -35,12 +35,17 @@ typedef const __attribute__((address_space(4))) int32_t ConstI32;
 
 // NP = pages staged per sub-chunk (the launch picks it from the chunk
 // length), so short decode chunks issue only the loads they need.  NW waves
-// hold 2 row tiles each: an item covers up to 32*NW query rows (NW = 8 lets
-// one item cover all rows of a long draft, so its keys are read once).
-template <int DH, int NP, int NW>
-__global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
+// hold TPW row tiles each: an item covers up to 16*NW*TPW query rows (64 for
+// short drafts, up to 256 so one item covers all rows of a long draft and
+// its keys are read once).
+// Workgroups per CU the register budget is sized for: two 4-wave
+// workgroups share a CU while their staged sub-chunks fit LDS together.
+constexpr int attn_occupancy(int DH, int NP, int NW) { return NW == 4 && NP * kPage * DH <= 64 * 128 ? 2 : 1; }
+
+template <int DH, int NP, int NW, int TPW>
+__global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_attn(AttnArgs a) {
   constexpr int NT = 64 * NW;           // threads
-  constexpr int RPI = 32 * NW;          // query rows per item
+  constexpr int RPI = 16 * NW * TPW;    // query rows per item
   constexpr int CH = NP * kPage;        // positions per sub-chunk
   constexpr int KSEG = DH / 8;          // 16-byte segments per K row
   constexpr int VU = CH / 4;            // 8-byte units per V row in LDS
@@ -67,14 +72,16 @@ __global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
   const _Float16* kvg = a.kv + (size_t)g * kPage * DH;  // this kv head's K block in a page
   ConstI32* ptrow = (ConstI32*)a.pt + (size_t)slot * a.pt_stride;
 
-  // per-wave state of its (up to) two 16-row tiles, kept across sub-chunks
-  int tile_row[2];
-  bool tile_on[2];
-  f16x8 qf[2][DH / 32];
-  float m[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
-  f32x4 o[2][DH / 16];
+  // per-wave state of its (up to) TPW 16-row tiles, kept across sub-chunks
+  int tile_row[TPW];
+  bool tile_on[TPW];
+  f16x8 qf[TPW][DH / 32];
+  float m[TPW], lsum[TPW];
+  f32x4 o[TPW][DH / 16];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < TPW; ++q) {
+    m[q] = -INFINITY;
+    lsum[q] = 0.f;
     const int row_base = rg * RPI + (wave + NW * q) * 16;
     tile_on[q] = row_base < R;
     tile_row[q] = row_base + (lane & 15);
@@ -110,7 +117,7 @@ __global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
     if (sub == p_begin) {
       // query fragments (rows past R read a valid row; their results are dropped)
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
+      for (int q = 0; q < TPW; ++q) {
         const int r = tile_row[q];
         const int i = r < R ? r / G : kdr;
         const int h = g * G + (r < R ? r % G : 0);
@@ -132,16 +139,14 @@ __global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
         } else {
           const int v = u - 2 * DH;
           const int d = v >> 1, hh = v & 1;
-          // 8 positions pp .. pp+7 of row d; zero positions past the end
+          // 8 positions pp .. pp+7 of row d; positions past the end are
+          // zeroed (their probabilities are 0, and stale values must not
+          // turn that into NaN)
           const int pp = p * kPage + hh * 8;
-          if (pp >= n_pos) {
-            x = u32x4{0u, 0u, 0u, 0u};
-          } else if (pp + 8 > n_pos) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const uint32_t keep = (pp + 2 * e + 1 < n_pos) ? 0xffffffffu : (pp + 2 * e < n_pos ? 0xffffu : 0u);
-              x[e] &= keep;
-            }
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t keep = (pp + 2 * e + 1 < n_pos) ? 0xffffffffu : (pp + 2 * e < n_pos ? 0xffffu : 0u);
+            x[e] &= keep;
           }
           const int u0 = pp >> 2;  // 8-byte units (4 positions)
           uint2* row = (uint2*)(sV + (size_t)d * CH);
@@ -151,76 +156,90 @@ __global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
       }
     __syncthreads();
 
+    // Each row tile over the sub-chunk in groups of SG 16-position blocks:
+    // all scores S^T = K Q^T of a group first (SG independent accumulator
+    // chains, K fragments read from LDS a DH/32 step at a time), one
+    // online-softmax update, then O^T += V^T P^T over its block pairs.
+    // Every position is computed; those past the end are masked, so no load
+    // is conditional.
+    constexpr int NB = CH / 16;                                // 16-position blocks
+    constexpr int SG = NB < 4 / TPW ? NB : 4 / TPW;  // blocks per score group (register budget)
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < TPW; ++q) {
       if (!tile_on[q]) continue;
       const int r = tile_row[q];
       const int i = r < R ? r / G : kdr;
       const int lim = ctx + i - sub;  // last visible position, sub-chunk-relative
-      for (int p0 = 0; p0 < n_pos; p0 += 32) {
-        const bool has1 = p0 + 16 < n_pos;
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-        {
-          const int p = p0 + (lane & 15);
+#pragma unroll 1
+      for (int g0 = 0; g0 < NB; g0 += SG) {  // not unrolled: keeps each group's LDS reads in its group
+        f32x4 sc[SG];
 #pragma unroll
-          for (int kd = 0; kd < DH / 32; ++kd) {
-            const int sg = kd * 4 + lg;
-            const f16x8 kf = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
-            s0 = mfma_f16(kf, qf[q][kd], s0);
+        for (int kd = 0; kd < DH / 32; ++kd) {
+          const int sg = kd * 4 + lg;
+          f16x8 kf[SG];
+#pragma unroll
+          for (int b = 0; b < SG; ++b) {
+            const int p = (g0 + b) * 16 + (lane & 15);
+            kf[b] = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
           }
-        }
-        if (has1) {
-          const int p = p0 + 16 + (lane & 15);
 #pragma unroll
-          for (int kd = 0; kd < DH / 32; ++kd) {
-            const int sg = kd * 4 + lg;
-            const f16x8 kf = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
-            s1 = mfma_f16(kf, qf[q][kd], s1);
+          for (int b = 0; b < SG; ++b) sc[b] = mfma_f16(kf[b], qf[q][kd], kd ? sc[b] : f32x4{0.f, 0.f, 0.f, 0.f});
+        }
+        float bm = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < SG; ++b)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int pa = (g0 + b) * 16 + lg * 4 + j;
+            sc[b][j] = (pa <= lim && pa < n_pos) ? sc[b][j] * a.scale_log2 : -INFINITY;
+            bm = fmaxf(bm, sc[b][j]);
           }
-        }
-        float sv[8];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int pa = p0 + lg * 4 + j, pb = pa + 16;
-          sv[j] = (pa <= lim && pa < n_pos) ? s0[j] * a.scale_log2 : -INFINITY;
-          sv[4 + j] = (pb <= lim && pb < n_pos) ? s1[j] * a.scale_log2 : -INFINITY;
-        }
-        float bm = sv[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) bm = fmaxf(bm, sv[j]);
         bm = fmaxf(bm, __shfl_xor(bm, 16));
         bm = fmaxf(bm, __shfl_xor(bm, 32));
         const float mn = fmaxf(m[q], bm);
         const float alpha = (m[q] == -INFINITY) ? 0.f : exp2f(m[q] - mn);
-        float pv[8];
         float ps = 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          pv[j] = (sv[j] == -INFINITY) ? 0.f : exp2f(sv[j] - mn);
-          ps += pv[j];
-        }
+        for (int b = 0; b < SG; ++b)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            sc[b][j] = (sc[b][j] == -INFINITY) ? 0.f : exp2f(sc[b][j] - mn);
+            ps += sc[b][j];
+          }
         lsum[q] = lsum[q] * alpha + ps;
         m[q] = mn;
-        f16x8 pf;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) pf[j] = (_Float16)pv[j];
-        const int ua = (p0 >> 2) + lg, ub = ua + 4;  // 8-byte units of positions 4lg.. and 16+4lg..
+        for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
 #pragma unroll
-        for (int dt = 0; dt < DH / 16; ++dt) {
-          o[q][dt] *= alpha;
-          const int d = dt * 16 + (lane & 15);
-          const uint2* row = (const uint2*)(sV + (size_t)d * CH);
-          const uint2 va = row[(ua & ~(VM - 1)) | ((ua & (VM - 1)) ^ (d & (VM - 1)))];
-          const uint2 vb = has1 ? row[(ub & ~(VM - 1)) | ((ub & (VM - 1)) ^ (d & (VM - 1)))] : uint2{0, 0};
-          const u32x4 vv = {va.x, va.y, vb.x, vb.y};
-          o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf, o[q][dt]);
+        for (int c = 0; c < SG / 2; ++c) {
+          // positions 32c' + {4lg..4lg+3} and 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
+          f16x8 pf;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            pf[j] = (_Float16)sc[2 * c][j];
+            pf[4 + j] = (_Float16)sc[2 * c + 1][j];
+          }
+          const int ua = 4 * g0 + 8 * c + lg, ub = ua + 4;
+          uint2 va[DH / 16], vb[DH / 16];
+#pragma unroll
+          for (int dt = 0; dt < DH / 16; ++dt) {
+            const int d = dt * 16 + (lane & 15);
+            const uint2* row = (const uint2*)(sV + (size_t)d * CH);
+            va[dt] = row[(ua & ~(VM - 1)) | ((ua & (VM - 1)) ^ (d & (VM - 1)))];
+            vb[dt] = row[(ub & ~(VM - 1)) | ((ub & (VM - 1)) ^ (d & (VM - 1)))];
+          }
+#pragma unroll
+          for (int dt = 0; dt < DH / 16; ++dt) {
+            const u32x4 vv = {va[dt].x, va[dt].y, vb[dt].x, vb[dt].y};
+            o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf, o[q][dt]);
+          }
         }
       }
     }
   }
 
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < TPW; ++q) {
     if (!tile_on[q]) continue;
     float l = lsum[q];
     l += __shfl_xor(l, 16);
@@ -255,36 +274,41 @@ __global__ __launch_bounds__(64 * NW) void verify_attn(AttnArgs a) {
   }
 }
 
-// Merge the chunk partials of one (sequence, kv head, row group) in chunk
-// order: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, as a running
-// (M, L, acc) merge over batches of 8 chunks whose loads are all issued
-// before any is used (the merge is latency-bound).  One block per (head
-// entry, 16-row slice of its a.rpi rows); one thread per (row, 8 dims).
+// Merge the chunk partials of one (sequence, kv head, row group):
+// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c.  The merge is
+// latency-bound, so QS lanes share one (row, 8 dims): lane q takes chunks
+// q, q + QS, ... as a running (M, L, acc) merge over batches whose loads are
+// all issued before any is used, and the QS lanes then merge by shuffles.
+// One block per (head entry, slice of RPB rows); a.max_rows bounds the
+// slices per entry.
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
-  constexpr int OCT = DH / 8;
-  constexpr int RPB = 256 / OCT;  // rows per block
-  constexpr int NB = 8;           // chunks per batch
-  const int spb = a.rpi / RPB;    // blocks per head entry
+  constexpr int OCT = DH / 8;            // 8-dim octets per row
+  constexpr int QS = 8;                  // lanes per (row, octet)
+  constexpr int RPB = 256 / (OCT * QS);  // rows per block
+  constexpr int NB = 8;                  // chunks per lane per batch
+  const int spb = (a.max_rows + RPB - 1) / RPB;
   const AttnItem hd = a.heads[blockIdx.x / spb];
   if (hd.k < 0) return;  // grid padding
   const int slice = blockIdx.x % spb;
   const int G = a.group;
   const int R = (hd.k + 1) * G;
-  const int lr = slice * RPB + threadIdx.x / OCT, o8 = (threadIdx.x % OCT) * 8;
+  const int t = threadIdx.x;
+  const int qq = t % QS, o8 = (t / QS % OCT) * 8;
+  const int lr = slice * RPB + t / (QS * OCT);
   const int r = hd.rg * a.rpi + lr;
-  if (r >= R) return;
+  if (lr >= a.rpi || r >= R) return;  // the QS lanes of a row leave together
   const float* ml = a.part_ml + ((size_t)hd.part * a.rpi + lr) * 2;
   const float* po = a.part_o + ((size_t)hd.part * a.rpi + lr) * DH + o8;
   const size_t cstride_ml = (size_t)a.rpi * 2, cstride_o = (size_t)a.rpi * DH;
   float M = -INFINITY, L = 0.f;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int c0 = 0; c0 < hd.nch; c0 += NB) {
+  for (int c0 = qq; c0 < hd.nch; c0 += QS * NB) {
     float2 mlc[NB];
     float4 x0[NB], x1[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const int c = c0 + j;
+      const int c = c0 + j * QS;
       mlc[j] = float2{-INFINITY, 0.f};
       x0[j] = x1[j] = float4{0.f, 0.f, 0.f, 0.f};
       if (c < hd.nch) {
@@ -309,16 +333,33 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
     }
     M = Mn;
   }
+  // merge the QS lanes of this (row, octet)
+  float Mx = fmaxf(M, __shfl_xor(M, 1));
+  Mx = fmaxf(Mx, __shfl_xor(Mx, 2));
+  Mx = fmaxf(Mx, __shfl_xor(Mx, 4));
+  const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mx);
+  L *= sc;
+  L += __shfl_xor(L, 1);
+  L += __shfl_xor(L, 2);
+  L += __shfl_xor(L, 4);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    acc[e] *= sc;
+    acc[e] += __shfl_xor(acc[e], 1);
+    acc[e] += __shfl_xor(acc[e], 2);
+    acc[e] += __shfl_xor(acc[e], 4);
+  }
+  if (qq >= 2) return;
   const float inv = L > 0.f ? 1.f / L : 0.f;
   const int i = r / G, h = hd.g * G + r % G;
   uint16_t hi[8], lo[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) split_f16(acc[j] * inv, hi[j], lo[j]);
   const size_t off = afrag_off(hd.cu + i, h * DH + o8, a.MTtot);
-  *(uint4*)(a.Ohi + off) = uint4{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16),
-                                 hi[4] | ((uint32_t)hi[5] << 16), hi[6] | ((uint32_t)hi[7] << 16)};
-  *(uint4*)(a.Olo + off) = uint4{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16),
-                                 lo[4] | ((uint32_t)lo[5] << 16), lo[6] | ((uint32_t)lo[7] << 16)};
+  const uint16_t* w = qq == 0 ? hi : lo;
+  *(uint4*)((qq == 0 ? a.Ohi : a.Olo) + off) =
+      uint4{w[0] | ((uint32_t)w[1] << 16), w[2] | ((uint32_t)w[3] << 16), w[4] | ((uint32_t)w[5] << 16),
+            w[6] | ((uint32_t)w[7] << 16)};
 }
 
 int attn_pages_per_sub(int chunk) {
@@ -329,65 +370,86 @@ int attn_pages_per_sub(int chunk) {
 
 size_t attn_lds_bytes(int dh, int np) { return (size_t)np * kPage * dh * 2 * 2; }
 
-template <int DH, int NW>
+template <int DH, int NW, int TPW>
 static hipError_t launch_attn_dh(const AttnArgs& a, int n_items, int np, hipStream_t s) {
   const size_t lds = attn_lds_bytes(DH, np);
   const dim3 block(64 * NW);
   switch (np) {
-    case 2: hvd_launch((verify_attn<DH, 2, NW>), dim3(n_items), block, lds, s, a); break;
-    case 4: hvd_launch((verify_attn<DH, 4, NW>), dim3(n_items), block, lds, s, a); break;
-    case 8: hvd_launch((verify_attn<DH, 8, NW>), dim3(n_items), block, lds, s, a); break;
-    case 16: hvd_launch((verify_attn<DH, 16, NW>), dim3(n_items), block, lds, s, a); break;
+    case 2: hvd_launch((verify_attn<DH, 2, NW, TPW>), dim3(n_items), block, lds, s, a); break;
+    case 4: hvd_launch((verify_attn<DH, 4, NW, TPW>), dim3(n_items), block, lds, s, a); break;
+    case 8: hvd_launch((verify_attn<DH, 8, NW, TPW>), dim3(n_items), block, lds, s, a); break;
+    case 16:
+      if constexpr (TPW == 1 || DH == 64) {
+        hvd_launch((verify_attn<DH, 16, NW, TPW>), dim3(n_items), block, lds, s, a);
+        break;
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+// rows_per_item: 64 (4 waves of one row tile), 128 (8 waves of one tile;
+// 4 waves of two for head dim 64, whose page has too few 16-byte units for
+// 8 waves) or 256 (8 waves of two tiles; head dim 128, sub-chunks of at most
+// 8 pages so the staging registers fit two waves per SIMD)
 hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  int np = attn_pages_per_sub(chunk);
-  if (rows_per_item == 256) {
-    // 8 waves of 2 row tiles: sub-chunks of at most 8 pages keep the staging
-    // registers within two waves per SIMD
-    if (a.dh != 128) return hipErrorInvalidValue;
-    return launch_attn_dh<128, 8>(a, n_items, np < 8 ? np : 8, s);
+  const int np = attn_pages_per_sub(chunk);
+  switch (rows_per_item) {
+    case 64:
+      if (a.dh == 128) return launch_attn_dh<128, 4, 1>(a, n_items, np, s);
+      if (a.dh == 64) return launch_attn_dh<64, 4, 1>(a, n_items, np, s);
+      return hipErrorInvalidValue;
+    case 128:
+      if (a.dh == 128) return launch_attn_dh<128, 8, 1>(a, n_items, np, s);
+      if (a.dh == 64) return launch_attn_dh<64, 4, 2>(a, n_items, np, s);
+      return hipErrorInvalidValue;
+    case 256:
+      if (a.dh == 128) return launch_attn_dh<128, 8, 2>(a, n_items, np < 8 ? np : 8, s);
+      return hipErrorInvalidValue;
   }
-  if (rows_per_item != 128) return hipErrorInvalidValue;
-  if (a.dh == 128) return launch_attn_dh<128, 4>(a, n_items, np, s);
-  if (a.dh == 64) return launch_attn_dh<64, 4>(a, n_items, np, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s) {
   if (n_heads <= 0) return hipSuccess;
+  if (a.max_rows <= 0 || a.max_rows > a.rpi) return hipErrorInvalidValue;
   if (a.dh == 128)
-    hvd_launch(attn_combine<128>, dim3(n_heads * (a.rpi / 16)), dim3(256), 0, s, a);
+    hvd_launch(attn_combine<128>, dim3(n_heads * ((a.max_rows + 1) / 2)), dim3(256), 0, s, a);
   else if (a.dh == 64)
-    hvd_launch(attn_combine<64>, dim3(n_heads * (a.rpi / 32)), dim3(256), 0, s, a);
+    hvd_launch(attn_combine<64>, dim3(n_heads * ((a.max_rows + 3) / 4)), dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-template <int DH, int NP, int NW>
+template <int DH, int NP, int NW, int TPW>
 static hipError_t set_lds(void) {
-  return hipFuncSetAttribute((const void*)verify_attn<DH, NP, NW>, hipFuncAttributeMaxDynamicSharedMemorySize,
+  return hipFuncSetAttribute((const void*)verify_attn<DH, NP, NW, TPW>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)attn_lds_bytes(DH, NP));
 }
 
+template <int DH, int NW>
+static hipError_t set_lds_tpw1(void) {
+  hipError_t e = set_lds<DH, 2, NW, 1>();
+  if (e == hipSuccess) e = set_lds<DH, 4, NW, 1>();
+  if (e == hipSuccess) e = set_lds<DH, 8, NW, 1>();
+  if (e == hipSuccess) e = set_lds<DH, 16, NW, 1>();
+  return e;
+}
+
 hipError_t attn_set_lds_limit() {
-  hipError_t e = hipSuccess;
-  if (e == hipSuccess) e = set_lds<128, 2, 4>();
-  if (e == hipSuccess) e = set_lds<128, 4, 4>();
-  if (e == hipSuccess) e = set_lds<128, 8, 4>();
-  if (e == hipSuccess) e = set_lds<128, 16, 4>();
-  if (e == hipSuccess) e = set_lds<128, 2, 8>();
-  if (e == hipSuccess) e = set_lds<128, 4, 8>();
-  if (e == hipSuccess) e = set_lds<128, 8, 8>();
-  if (e == hipSuccess) e = set_lds<64, 2, 4>();
-  if (e == hipSuccess) e = set_lds<64, 4, 4>();
-  if (e == hipSuccess) e = set_lds<64, 8, 4>();
-  if (e == hipSuccess) e = set_lds<64, 16, 4>();
+  hipError_t e = set_lds_tpw1<128, 4>();
+  if (e == hipSuccess) e = set_lds_tpw1<128, 8>();
+  if (e == hipSuccess) e = set_lds_tpw1<64, 4>();
+  if (e == hipSuccess) e = set_lds<64, 2, 4, 2>();
+  if (e == hipSuccess) e = set_lds<64, 4, 4, 2>();
+  if (e == hipSuccess) e = set_lds<64, 8, 4, 2>();
+  if (e == hipSuccess) e = set_lds<64, 16, 4, 2>();
+  if (e == hipSuccess) e = set_lds<128, 2, 8, 2>();
+  if (e == hipSuccess) e = set_lds<128, 4, 8, 2>();
+  if (e == hipSuccess) e = set_lds<128, 8, 8, 2>();
   return e;
 }
 

@@ -122,7 +122,8 @@ struct CombineArgs {
   uint16_t* Ohi;
   uint16_t* Olo;
   int MTtot;
-  int rpi;  // query rows per work item (partial slot stride)
+  int rpi;       // query rows per work item (partial slot stride)
+  int max_rows;  // most rows of any head entry (1..rpi): sizes the grid
 };
 
 struct EmbedArgs {
@@ -172,7 +173,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mbloc
 hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, int splits, float* inv_rms,
                              hipStream_t s);
 // chunk: the plan's KV chunk length (picks the pages staged per sub-chunk);
-// rows_per_item: 128 (4 waves) or 256 (8 waves, head_dim 128)
+// rows_per_item: 64, 128 or 256 (256 for head_dim 128 only)
 hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, hipStream_t s);
 hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
