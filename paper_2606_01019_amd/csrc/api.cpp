@@ -35,6 +35,10 @@ hvd_status set_err(hvd_status s, const std::string& m) {
 
 constexpr size_t kAlign = 256;
 constexpr int kPrefillRows = 128;  // rows per prefill chunk
+// Up to 8 row tiles (128 rows) the skinny kernel in row blocks of <= 4
+// tiles beats the tiled kernel and its K-split finish (measured: 65-row
+// verifies and 128-row prefill chunks of the 8B shape)
+constexpr int kSkinnyMaxMT = 8;
 constexpr int kGemmMinBlocks = 192;          // GEMM workgroups below which the shape changes
 constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (one per CU)
 constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
@@ -322,6 +326,7 @@ struct hvd_kv_s {
   bool use_graphs = false;
   std::map<GraphKey, hipGraphExec_t> graphs;
   int attn_min_items = kAttnMinItems;
+  int skinny_max_mt = kSkinnyMaxMT;   // row tiles above which GEMMs take the MFMA-tiled kernel
   int gemm_force[PF_LM + 1][2] = {};  // per GEMM family: {strips per workgroup, K splits} of the skinny kernel, 0 = policy
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
@@ -449,6 +454,7 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_GRAPHS")) k->use_graphs = atoi(e) != 0;
+  if (const char* e = getenv("HVD_SKINNY_MAX_MT")) k->skinny_max_mt = std::max(1, std::min(64, atoi(e)));
   // tuning override of the skinny GEMM shape: "qkv=2:1,o=1:1" (family=strips:splits)
   if (const char* e = getenv("HVD_GEMM_SHAPE")) {
     static const char* names[PF_LM + 1] = {"qkv", "o", "gateup", "down", "lm"};
@@ -710,8 +716,9 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     HIP_TRY(launch_embed(e, s));
   }
 
-  const int mt_block = std::min(MT, kGemmMaxMT);
-  const int mblocks = (MT + mt_block - 1) / mt_block;
+  // skinny GEMMs: row blocks of at most kGemmMaxMT tiles, balanced
+  const int mblocks = (MT + kGemmMaxMT - 1) / kGemmMaxMT;
+  const int mt_block = (MT + mblocks - 1) / mblocks;
   // Workgroup shape per GEMM (measured on the 8B verify shapes): 4 strips
   // per workgroup when that alone gives enough workgroups (8 for two row
   // tiles, which halves the activation fragments per weight byte); for
@@ -727,7 +734,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.M = M;
     a.part = k->gemm_part;
     const int want = k->gemm_min_blocks;
-    if (MT > kGemmMaxMT && N % 128 == 0) {
+    if (MT > k->skinny_max_mt && N % 128 == 0) {
       // many rows: MFMA-tiled kernel, weights read once per XCD.  The
       // largest tile (256 x 256, 128 x 256, 128 x 128) that still gives
       // enough workgroups, and a K split when even the smallest is too few

@@ -280,11 +280,12 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
 // q, q + QS, ... as a running (M, L, acc) merge over batches whose loads are
 // all issued before any is used, and the QS lanes then merge by shuffles.
 // One block per (head entry, slice of RPB rows); a.max_rows bounds the
-// slices per entry.
-template <int DH>
+// slices per entry.  QS is 8 for short drafts (few rows to spread over) and
+// smaller when an entry has more rows, so blocks past a short entry's rows
+// stay few.
+template <int DH, int QS>
 __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   constexpr int OCT = DH / 8;            // 8-dim octets per row
-  constexpr int QS = 8;                  // lanes per (row, octet)
   constexpr int RPB = 256 / (OCT * QS);  // rows per block
   constexpr int NB = 8;                  // chunks per lane per batch
   const int spb = (a.max_rows + RPB - 1) / RPB;
@@ -334,32 +335,31 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
     M = Mn;
   }
   // merge the QS lanes of this (row, octet)
-  float Mx = fmaxf(M, __shfl_xor(M, 1));
-  Mx = fmaxf(Mx, __shfl_xor(Mx, 2));
-  Mx = fmaxf(Mx, __shfl_xor(Mx, 4));
+  float Mx = M;
+#pragma unroll
+  for (int o = 1; o < QS; o *= 2) Mx = fmaxf(Mx, __shfl_xor(Mx, o));
   const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mx);
   L *= sc;
-  L += __shfl_xor(L, 1);
-  L += __shfl_xor(L, 2);
-  L += __shfl_xor(L, 4);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    acc[e] *= sc;
-    acc[e] += __shfl_xor(acc[e], 1);
-    acc[e] += __shfl_xor(acc[e], 2);
-    acc[e] += __shfl_xor(acc[e], 4);
+  for (int e = 0; e < 8; ++e) acc[e] *= sc;
+#pragma unroll
+  for (int o = 1; o < QS; o *= 2) {
+    L += __shfl_xor(L, o);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o);
   }
-  if (qq >= 2) return;
   const float inv = L > 0.f ? 1.f / L : 0.f;
   const int i = r / G, h = hd.g * G + r % G;
   uint16_t hi[8], lo[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) split_f16(acc[j] * inv, hi[j], lo[j]);
   const size_t off = afrag_off(hd.cu + i, h * DH + o8, a.MTtot);
-  const uint16_t* w = qq == 0 ? hi : lo;
-  *(uint4*)((qq == 0 ? a.Ohi : a.Olo) + off) =
-      uint4{w[0] | ((uint32_t)w[1] << 16), w[2] | ((uint32_t)w[3] << 16), w[4] | ((uint32_t)w[5] << 16),
-            w[6] | ((uint32_t)w[7] << 16)};
+  if (qq == 0 || QS == 1)
+    *(uint4*)(a.Ohi + off) = uint4{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16),
+                                   hi[4] | ((uint32_t)hi[5] << 16), hi[6] | ((uint32_t)hi[7] << 16)};
+  if (qq == 1 || QS == 1)
+    *(uint4*)(a.Olo + off) = uint4{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16),
+                                   lo[4] | ((uint32_t)lo[5] << 16), lo[6] | ((uint32_t)lo[7] << 16)};
 }
 
 int attn_pages_per_sub(int chunk) {
@@ -412,13 +412,26 @@ hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_i
   return hipErrorInvalidValue;
 }
 
+template <int DH, int QS>
+static void launch_combine_q(const CombineArgs& a, int n_heads, hipStream_t s) {
+  constexpr int RPB = 256 / (DH / 8 * QS);
+  hvd_launch((attn_combine<DH, QS>), dim3(n_heads * ((a.max_rows + RPB - 1) / RPB)), dim3(256), 0, s, a);
+}
+
+template <int DH>
+static void launch_combine_dh(const CombineArgs& a, int n_heads, hipStream_t s) {
+  if (a.rpi <= 64) launch_combine_q<DH, 8>(a, n_heads, s);
+  else if (a.rpi <= 128) launch_combine_q<DH, 4>(a, n_heads, s);
+  else launch_combine_q<DH, 2>(a, n_heads, s);
+}
+
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s) {
   if (n_heads <= 0) return hipSuccess;
   if (a.max_rows <= 0 || a.max_rows > a.rpi) return hipErrorInvalidValue;
   if (a.dh == 128)
-    hvd_launch(attn_combine<128>, dim3(n_heads * ((a.max_rows + 1) / 2)), dim3(256), 0, s, a);
+    launch_combine_dh<128>(a, n_heads, s);
   else if (a.dh == 64)
-    hvd_launch(attn_combine<64>, dim3(n_heads * ((a.max_rows + 3) / 4)), dim3(256), 0, s, a);
+    launch_combine_dh<64>(a, n_heads, s);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -362,11 +362,36 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, float (*tile)[N
         }
       }
       if (lane == 0) {
-        a.part_val[(size_t)R * a.n_part + blockIdx.x] = best;
-        a.part_idx[(size_t)R * a.n_part + blockIdx.x] = bidx;
+        a.part_val[(size_t)R * a.n_part + cb] = best;
+        a.part_idx[(size_t)R * a.n_part + cb] = bidx;
       }
     }
   }
+}
+
+// Workgroup -> (column block, K split, row block).  With several row
+// blocks, those of one (column block, split) get workgroup ids 8 apart: the
+// same XCD under round-robin dispatch, started at nearly the same time, so
+// the weights are read from HBM once and from that XCD's L2 after.
+struct SkinnyCoord {
+  int cb, split, mb;
+};
+__device__ __forceinline__ SkinnyCoord skinny_coord() {
+  const int gx = gridDim.x, gy = gridDim.y, mbs = gridDim.z;
+  if (mbs == 1) return {(int)blockIdx.x, (int)blockIdx.y, 0};
+  const int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int units = gx * gy, u8 = units - units % 8;
+  int unit, mb;
+  if (lin < u8 * mbs) {
+    const int r = lin / 8;
+    mb = r % mbs;
+    unit = (r / mbs) * 8 + lin % 8;
+  } else {  // the last units % 8 units: row blocks adjacent
+    const int rem = lin - u8 * mbs;
+    unit = u8 + rem / mbs;
+    mb = rem % mbs;
+  }
+  return {unit % gx, unit / gx, mb};
 }
 
 // HL: activation as the fp16 hi + lo pair (two MFMAs per tile), or the hi
@@ -386,8 +411,9 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   // scalar registers (one VGPR per lane of addressing, no register reuse
   // that would force the prefetch queue to drain)
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int cb = blockIdx.x;
-  const int mt0 = blockIdx.z * MT;
+  const SkinnyCoord co = skinny_coord();
+  const int cb = co.cb;
+  const int mt0 = co.mb * MT;
   const int mcount = min(MT, a.MTtot - mt0);
   const bool split = gridDim.y > 1;
 
@@ -396,7 +422,7 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   // one contiguous window of weights (kKG adjacent K steps) rather than kKG
   // distant streams
   const int kts = (a.KT + gridDim.y - 1) / gridDim.y;
-  const int wk0 = blockIdx.y * kts, wk1 = min(a.KT, wk0 + kts);
+  const int wk0 = co.split * kts, wk1 = min(a.KT, wk0 + kts);
   const int kb = wk0 + wave;
   const int nsteps = kb < wk1 ? (wk1 - kb + kKG - 1) / kKG : 0;  // wave-uniform
 
@@ -511,7 +537,7 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   if (split) {
     // K split across workgroups: publish the partial tile; gemm_finish sums
     // the splits in order and runs the epilogue.
-    float* dst = a.part + ((size_t)(blockIdx.z * gridDim.x + cb) * gridDim.y + blockIdx.y) * ROWS * COLS;
+    float* dst = a.part + ((size_t)(co.mb * gridDim.x + cb) * gridDim.y + co.split) * ROWS * COLS;
     for (int e = tid; e < mcount * 16 * COLS; e += 512) dst[e] = tile[e / COLS][e % COLS];
     return;
   }
