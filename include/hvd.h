@@ -175,8 +175,11 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   the gate/up and down GEMMs take the fp16 activation alone (11 bits)
  *   instead of the fp16 hi + lo pair (~22 bits), halving their activation
  *   traffic and MFMA work; 0 keeps the pair.  Prefill always uses the pair.
- *   Logit differences stay within the verify step's tolerance. */
-enum { HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2 };
+ *   Logit differences stay within the verify step's tolerance.
+ * HVD_OPT_LM_SINGLE (default 1): likewise for the LM-head GEMM of verify
+ *   forwards of more than 32 rows (its rounding error, ~1e-4 on the logits,
+ *   is far below the tolerance); 0 keeps the pair. */
+enum { HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3 };
 hvd_status hvd_kv_set_option(hvd_kv kv, int32_t option, int32_t value);
 
 /* Message of the last failing call on this thread ("" if none). */

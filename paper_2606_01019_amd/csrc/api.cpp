@@ -331,6 +331,7 @@ struct hvd_kv_s {
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
   bool mlp_single = true;    // large-batch verify MLP GEMMs on the hi activation part only
+  bool lm_single = true;     // large-batch verify LM head on the hi activation part only
   int32_t* g = nullptr;
   int32_t* out = nullptr;
   uint32_t* counter = nullptr;
@@ -756,7 +757,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         a.n_part = lm_parts;
       }
       ProfScope ps(k, family, (double)N * K * 2.0);
-      HIP_TRY(launch_gemm_tiled(epi, a, tile, !(mlp && k->mlp_single && lm_head), splits, k->inv_rms, s));
+      const bool single = lm_head && ((mlp && k->mlp_single) || (epi == EPI_LM && k->lm_single));
+      HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, k->inv_rms, s));
       return HVD_OK;
     }
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
@@ -791,7 +793,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     }
     ProfScope ps(k, family, (double)N * K * 2.0);
     // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
-    const bool single = k->mlp_single && lm_head && MT > 2 && (epi == EPI_SILU || family == PF_DOWN);
+    const bool single = lm_head && MT > 2 &&
+                        ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
     HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, !single, s));
     return HVD_OK;
   };
@@ -1087,7 +1090,8 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
       }
       return HVD_OK;
     case HVD_OPT_MLP_SINGLE:
-      k->mlp_single = value != 0;
+    case HVD_OPT_LM_SINGLE:
+      (option == HVD_OPT_MLP_SINGLE ? k->mlp_single : k->lm_single) = value != 0;
       for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);  // captured with the old choice
       k->graphs.clear();
       return HVD_OK;

@@ -89,23 +89,13 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
     for (int d = 0; d < DH / 16; ++d) o[q][d] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int sub = p_begin; sub < p_end; sub += CH) {
-    const int n_pos = min(CH, p_end - sub);
-    const int n_pages = (n_pos + kPage - 1) / kPage;
-    // pool page of each staged page; pages past the sub-chunk's end repeat
-    // its first page (in-bounds, cached; their V is zeroed below)
-    int pgid[NP];
-    if (sub == p_begin) {
-#pragma unroll
-      for (int p = 0; p < NP; ++p) pgid[p] = ip->pages[p];
-    } else {
-#pragma unroll
-      for (int p = 0; p < NP; ++p) pgid[p] = ptrow[(sub >> 4) + (p < n_pages ? p : 0)];
-      __syncthreads();  // previous sub-chunk fully consumed
-    }
-    // ---- all K/V loads of the sub-chunk in flight at once (page-major:
-    // per page, units [0, 2DH) are K rows, [2DH, 4DH) V rows of the head)
-    u32x4 buf[NP][LPP];
+  // ---- K/V loads of one sub-chunk, all in flight at once (page-major: per
+  // page, units [0, 2DH) are K rows, [2DH, 4DH) V rows of the head).  Pages
+  // past the sub-chunk's end repeat its first page (in-bounds, cached; their
+  // V is zeroed when staged).  The next sub-chunk's loads are issued before
+  // the current one is computed, so its latency hides behind the MFMAs.
+  u32x4 buf[NP][LPP];
+  auto issue = [&](const int (&pgid)[NP]) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -114,18 +104,27 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
         const size_t off = u < 2 * DH ? (size_t)u * 8 : vhalf + (size_t)(u - 2 * DH) * 8;
         buf[p][j] = *(const u32x4*)(kvg + (size_t)pgid[p] * a.page_stride + off);
       }
-    if (sub == p_begin) {
-      // query fragments (rows past R read a valid row; their results are dropped)
+  };
+  {
+    int pgid[NP];
 #pragma unroll
-      for (int q = 0; q < TPW; ++q) {
-        const int r = tile_row[q];
-        const int i = r < R ? r / G : kdr;
-        const int h = g * G + (r < R ? r % G : 0);
+    for (int p = 0; p < NP; ++p) pgid[p] = ip->pages[p];
+    issue(pgid);
+  }
+  // query fragments (rows past R read a valid row; their results are dropped)
 #pragma unroll
-        for (int kd = 0; kd < DH / 32; ++kd)
-          qf[q][kd] = *(const f16x8*)(a.Q + ((size_t)(cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8);
-      }
-    }
+  for (int q = 0; q < TPW; ++q) {
+    const int r = tile_row[q];
+    const int i = r < R ? r / G : kdr;
+    const int h = g * G + (r < R ? r % G : 0);
+#pragma unroll
+    for (int kd = 0; kd < DH / 32; ++kd)
+      qf[q][kd] = *(const f16x8*)(a.Q + ((size_t)(cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8);
+  }
+
+  for (int sub = p_begin; sub < p_end; sub += CH) {
+    const int n_pos = min(CH, p_end - sub);
+    if (sub != p_begin) __syncthreads();  // previous sub-chunk fully consumed
 #pragma unroll
     for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -155,6 +154,14 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
         }
       }
     __syncthreads();
+    if (sub + CH < p_end) {
+      const int nsub = sub + CH;
+      const int nn_pages = (min(CH, p_end - nsub) + kPage - 1) / kPage;
+      int pgid[NP];
+#pragma unroll
+      for (int p = 0; p < NP; ++p) pgid[p] = ptrow[(nsub >> 4) + (p < nn_pages ? p : 0)];
+      issue(pgid);
+    }
 
     // Each row tile over the sub-chunk in groups of SG 16-position blocks:
     // all scores S^T = K Q^T of a group first (SG independent accumulator

@@ -604,8 +604,8 @@ static void launch_one(const GemmArgs& a, int splits, int mblocks, hipStream_t s
 
 template <int NS, int EPI>
 static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, bool hi_lo, hipStream_t s) {
-  // single-pass activations only for the MLP GEMMs at 3-4 row tiles
-  constexpr bool kSingle = EPI == EPI_SILU || EPI == EPI_RESID;
+  // single-pass activations only for the MLP and LM-head GEMMs at 3-4 row tiles
+  constexpr bool kSingle = EPI == EPI_SILU || EPI == EPI_RESID || EPI == EPI_LM;
   switch (mt) {
     case 1: launch_one<1, NS, EPI, true>(a, splits, mblocks, s); break;
     case 2: launch_one<2, NS, EPI, true>(a, splits, mblocks, s); break;

@@ -22,6 +22,7 @@ EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes"
            "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error")
 HVD_OPT_GRAPHS = 1
 HVD_OPT_MLP_SINGLE = 2
+HVD_OPT_LM_SINGLE = 3
 
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
@@ -216,6 +217,11 @@ class KVCache:
         """Large-batch verify MLP GEMMs on the fp16 activation alone (default)
         or on the fp16 hi + lo pair."""
         _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_MLP_SINGLE, 1 if on else 0))
+
+    def set_lm_single(self, on: bool):
+        """Large-batch verify LM head on the fp16 activation alone (default)
+        or on the fp16 hi + lo pair."""
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_LM_SINGLE, 1 if on else 0))
 
     def set_graphs(self, on: bool):
         """Replay step kernels from cached HIP graphs, or launch eagerly (default)."""
