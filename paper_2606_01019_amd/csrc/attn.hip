@@ -17,7 +17,8 @@
 // for lane group g).  V is stored transposed inside each 16-token page
 // ([dh][16]) and kept transposed in LDS.  LDS rows are XOR-swizzled so the
 // 16 lanes of a fragment read hit distinct banks.
-// Online softmax in fp32 base 2; rows see only their causal prefix; keys at
+// Online softmax in fp32 base 2 (the hardware exp2, whose results below
+// 2^-126 flush to zero); rows see only their causal prefix; keys at
 // positions >= ctx+k+1 are never used (their contents may be stale).
 // A single-chunk item writes the normalized output straight into the O GEMM's
 // hi/lo operand; multi-chunk items write (m, l, unnormalized O) partials that
@@ -27,11 +28,10 @@
 
 namespace hvd {
 
-// Item and page-table reads go through the constant address space: both
-// are read-only while attention runs, and uniform addresses there become
-// scalar loads whose results (page ids included) sit in SGPRs.
+// Item reads go through the constant address space: items are read-only
+// while attention runs, and uniform addresses there become scalar loads
+// whose results (the first sub-chunk's page ids included) sit in SGPRs.
 typedef const __attribute__((address_space(4))) AttnItem ConstItem;
-typedef const __attribute__((address_space(4))) int32_t ConstI32;
 
 // NP = pages staged per sub-chunk (the launch picks it from the chunk
 // length), so short decode chunks issue only the loads they need.  NW waves
@@ -70,7 +70,6 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
   const int lg = lane >> 4;
   const size_t vhalf = (size_t)a.Hkv * kPage * DH;
   const _Float16* kvg = a.kv + (size_t)g * kPage * DH;  // this kv head's K block in a page
-  ConstI32* ptrow = (ConstI32*)a.pt + (size_t)slot * a.pt_stride;
 
   // per-wave state of its (up to) TPW 16-row tiles, kept across sub-chunks
   int tile_row[TPW];
@@ -94,6 +93,16 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
   // past the sub-chunk's end repeat its first page (in-bounds, cached; their
   // V is zeroed when staged).  The next sub-chunk's loads are issued before
   // the current one is computed, so its latency hides behind the MFMAs.
+  // query fragments (rows past R read a valid row; their results are dropped)
+#pragma unroll
+  for (int q = 0; q < TPW; ++q) {
+    const int r = tile_row[q];
+    const int i = r < R ? r / G : kdr;
+    const int h = g * G + (r < R ? r % G : 0);
+#pragma unroll
+    for (int kd = 0; kd < DH / 32; ++kd)
+      qf[q][kd] = *(const f16x8*)(a.Q + ((size_t)(cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8);
+  }
   u32x4 buf[NP][LPP];
   auto issue = [&](const int (&pgid)[NP]) __attribute__((always_inline)) {
 #pragma unroll
@@ -111,16 +120,19 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
     for (int p = 0; p < NP; ++p) pgid[p] = ip->pages[p];
     issue(pgid);
   }
-  // query fragments (rows past R read a valid row; their results are dropped)
-#pragma unroll
-  for (int q = 0; q < TPW; ++q) {
-    const int r = tile_row[q];
-    const int i = r < R ? r / G : kdr;
-    const int h = g * G + (r < R ? r % G : 0);
-#pragma unroll
-    for (int kd = 0; kd < DH / 32; ++kd)
-      qf[q][kd] = *(const f16x8*)(a.Q + ((size_t)(cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8);
-  }
+  // pool pages of the next sub-chunk to issue, one per lane (lane p < NP:
+  // page p; past the sub-chunk's end, its first page), loaded a sub-chunk
+  // ahead so issuing never waits on a page-table read
+  auto next_pages = [&](int nsub) __attribute__((always_inline)) {
+    const int np_sub = (min(CH, p_end - nsub) + kPage - 1) / kPage;
+    return a.pt[(size_t)slot * a.pt_stride + (nsub >> 4) + (lane < np_sub ? lane : 0)];
+  };
+  int pg_next = p_begin + CH < p_end ? next_pages(p_begin + CH) : 0;
+  // Wait here for everything issued so far (the first sub-chunk is staged
+  // right after anyway): the waitcnt pass then knows the query fragments are
+  // in, and places no wait for them inside the loop, where it would also
+  // wait for the next sub-chunk's loads.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 
   for (int sub = p_begin; sub < p_end; sub += CH) {
     const int n_pos = min(CH, p_end - sub);
@@ -155,31 +167,32 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
       }
     __syncthreads();
     if (sub + CH < p_end) {
-      const int nsub = sub + CH;
-      const int nn_pages = (min(CH, p_end - nsub) + kPage - 1) / kPage;
       int pgid[NP];
 #pragma unroll
-      for (int p = 0; p < NP; ++p) pgid[p] = ptrow[(nsub >> 4) + (p < nn_pages ? p : 0)];
+      for (int p = 0; p < NP; ++p) pgid[p] = __builtin_amdgcn_readlane(pg_next, p);
       issue(pgid);
+      if (sub + 2 * CH < p_end) pg_next = next_pages(sub + 2 * CH);
     }
 
-    // Each row tile over the sub-chunk in groups of SG 16-position blocks:
-    // all scores S^T = K Q^T of a group first (SG independent accumulator
-    // chains, K fragments read from LDS a DH/32 step at a time), one
-    // online-softmax update, then O^T += V^T P^T over its block pairs.
-    // Every position is computed; those past the end are masked, so no load
-    // is conditional.
-    constexpr int NB = CH / 16;                                // 16-position blocks
+    // The wave's row tiles over the sub-chunk in groups of SG 16-position
+    // blocks: all scores S^T = K Q^T of a group first (independent
+    // accumulator chains; each K fragment read from LDS once and used by
+    // every tile of the wave), one online-softmax update per tile, then
+    // O^T += V^T P^T over the group's block pairs (each V fragment read once
+    // for all tiles).  Every position is computed; those past the end are
+    // masked, so no load is conditional.  Tile 0 is live whenever any is.
+    constexpr int NB = CH / 16;                      // 16-position blocks
     constexpr int SG = NB < 4 / TPW ? NB : 4 / TPW;  // blocks per score group (register budget)
+    if (tile_on[0]) {
+      int lim[TPW];  // last visible position of each tile's rows, sub-chunk-relative
 #pragma unroll
-    for (int q = 0; q < TPW; ++q) {
-      if (!tile_on[q]) continue;
-      const int r = tile_row[q];
-      const int i = r < R ? r / G : kdr;
-      const int lim = ctx + i - sub;  // last visible position, sub-chunk-relative
+      for (int q = 0; q < TPW; ++q) {
+        const int r = tile_row[q];
+        lim[q] = ctx + (r < R ? r / G : kdr) - sub;
+      }
 #pragma unroll 1
       for (int g0 = 0; g0 < NB; g0 += SG) {  // not unrolled: keeps each group's LDS reads in its group
-        f32x4 sc[SG];
+        f32x4 sc[TPW][SG];
 #pragma unroll
         for (int kd = 0; kd < DH / 32; ++kd) {
           const int sg = kd * 4 + lg;
@@ -190,42 +203,54 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
             kf[b] = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
           }
 #pragma unroll
-          for (int b = 0; b < SG; ++b) sc[b] = mfma_f16(kf[b], qf[q][kd], kd ? sc[b] : f32x4{0.f, 0.f, 0.f, 0.f});
+          for (int q = 0; q < TPW; ++q)
+            if (q == 0 || tile_on[q]) {
+#pragma unroll
+              for (int b = 0; b < SG; ++b)
+                sc[q][b] = mfma_f16(kf[b], qf[q][kd], kd ? sc[q][b] : f32x4{0.f, 0.f, 0.f, 0.f});
+            }
         }
-        float bm = -INFINITY;
+        f16x8 pf[TPW][SG / 2 > 0 ? SG / 2 : 1];
 #pragma unroll
-        for (int b = 0; b < SG; ++b)
+        for (int q = 0; q < TPW; ++q) {
+          if (q > 0 && !tile_on[q]) continue;
+          float bm = -INFINITY;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int pa = (g0 + b) * 16 + lg * 4 + j;
-            sc[b][j] = (pa <= lim && pa < n_pos) ? sc[b][j] * a.scale_log2 : -INFINITY;
-            bm = fmaxf(bm, sc[b][j]);
-          }
-        bm = fmaxf(bm, __shfl_xor(bm, 16));
-        bm = fmaxf(bm, __shfl_xor(bm, 32));
-        const float mn = fmaxf(m[q], bm);
-        const float alpha = (m[q] == -INFINITY) ? 0.f : exp2f(m[q] - mn);
-        float ps = 0.f;
+          for (int b = 0; b < SG; ++b)
 #pragma unroll
-        for (int b = 0; b < SG; ++b)
+            for (int j = 0; j < 4; ++j) {
+              const int pa = (g0 + b) * 16 + lg * 4 + j;
+              sc[q][b][j] = (pa <= lim[q] && pa < n_pos) ? sc[q][b][j] * a.scale_log2 : -INFINITY;
+              bm = fmaxf(bm, sc[q][b][j]);
+            }
+          bm = fmaxf(bm, __shfl_xor(bm, 16));
+          bm = fmaxf(bm, __shfl_xor(bm, 32));
+          const float mn = fmaxf(m[q], bm);
+          const float alpha = (m[q] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[q] - mn);
+          float ps = 0.f;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            sc[b][j] = (sc[b][j] == -INFINITY) ? 0.f : exp2f(sc[b][j] - mn);
-            ps += sc[b][j];
-          }
-        lsum[q] = lsum[q] * alpha + ps;
-        m[q] = mn;
+          for (int b = 0; b < SG; ++b)
 #pragma unroll
-        for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
+            for (int j = 0; j < 4; ++j) {
+              sc[q][b][j] = (sc[q][b][j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sc[q][b][j] - mn);
+              ps += sc[q][b][j];
+            }
+          lsum[q] = lsum[q] * alpha + ps;
+          m[q] = mn;
+#pragma unroll
+          for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
+          // B operand of block pair c: positions 32c' + {4lg..4lg+3} and
+          // 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
+#pragma unroll
+          for (int c = 0; c < SG / 2; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              pf[q][c][j] = (_Float16)sc[q][2 * c][j];
+              pf[q][c][4 + j] = (_Float16)sc[q][2 * c + 1][j];
+            }
+        }
 #pragma unroll
         for (int c = 0; c < SG / 2; ++c) {
-          // positions 32c' + {4lg..4lg+3} and 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
-          f16x8 pf;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            pf[j] = (_Float16)sc[2 * c][j];
-            pf[4 + j] = (_Float16)sc[2 * c + 1][j];
-          }
           const int ua = 4 * g0 + 8 * c + lg, ub = ua + 4;
           uint2 va[DH / 16], vb[DH / 16];
 #pragma unroll
@@ -236,10 +261,14 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
             vb[dt] = row[(ub & ~(VM - 1)) | ((ub & (VM - 1)) ^ (d & (VM - 1)))];
           }
 #pragma unroll
-          for (int dt = 0; dt < DH / 16; ++dt) {
-            const u32x4 vv = {va[dt].x, va[dt].y, vb[dt].x, vb[dt].y};
-            o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf, o[q][dt]);
-          }
+          for (int q = 0; q < TPW; ++q)
+            if (q == 0 || tile_on[q]) {
+#pragma unroll
+              for (int dt = 0; dt < DH / 16; ++dt) {
+                const u32x4 vv = {va[dt].x, va[dt].y, vb[dt].x, vb[dt].y};
+                o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf[q][c], o[q][dt]);
+              }
+            }
         }
       }
     }
@@ -328,13 +357,13 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
     float Mn = M;
 #pragma unroll
     for (int j = 0; j < NB; ++j) Mn = fmaxf(Mn, mlc[j].x);
-    const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mn);
+    const float sc = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
     L *= sc;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] *= sc;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const float w = (mlc[j].x == -INFINITY) ? 0.f : exp2f(mlc[j].x - Mn);
+      const float w = (mlc[j].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mlc[j].x - Mn);
       L += w * mlc[j].y;
       acc[0] += w * x0[j].x; acc[1] += w * x0[j].y; acc[2] += w * x0[j].z; acc[3] += w * x0[j].w;
       acc[4] += w * x1[j].x; acc[5] += w * x1[j].y; acc[6] += w * x1[j].z; acc[7] += w * x1[j].w;
@@ -345,7 +374,7 @@ __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
   float Mx = M;
 #pragma unroll
   for (int o = 1; o < QS; o *= 2) Mx = fmaxf(Mx, __shfl_xor(Mx, o));
-  const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mx);
+  const float sc = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mx);
   L *= sc;
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] *= sc;
