@@ -8,7 +8,9 @@ What it computes (Verify in §3.1 and §3.4, Alg. 1 "Verify" step): one forward
 of the unchanged target model over the pending token plus a chain draft, the
 greedy accepted length (the longest draft prefix equal to the target's argmax
 continuation, the same quantity as the label equation of §3.3 and App. B),
-and the committed block of accepted tokens plus one target token.  At
+and the committed block of accepted tokens plus one target token; the same
+rule over a token tree (the tree-shaped model drafts of App. A), where each
+node sees its own path and the accepted path follows the target's argmax.  At
 temperature 0 (App. A generation table) greedy speculative verification is
 lossless, so the oracle is the plain definition: a Llama-style decoder forward
 in float64 (or float32 on request) over bf16-valued weights, and the prefix
@@ -26,11 +28,17 @@ from .model import (  # noqa: F401
     OracleModel,
     SeqState,
     VerifyResult,
+    TreeVerifyResult,
     accept_length,
     argmax_lowest,
     brute_force_greedy,
     commit,
+    commit_tree,
     greedy_decode,
     prefill,
+    tree_accept,
+    tree_ancestors,
+    tree_depths,
     verify,
+    verify_tree,
 )

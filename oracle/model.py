@@ -265,3 +265,159 @@ def brute_force_greedy(model: OracleModel, tokens, n: int):
         rows.append(last)
         toks.append(nxt)
     return out, np.stack(rows)
+
+
+# ------------------------------------------- tree-shaped drafts (App. A)
+#
+# The model drafter of App. A (EAGLE3, tree depth 8, top-k 4) proposes a
+# token tree rather than a chain.  Verification is the same rule applied
+# along the tree: every node is a draft token whose parent is the pending
+# token or an earlier node; a node's row sees the cached context and the rows
+# on its own path from the pending token, at position ctx + depth; the
+# accepted path starts at the pending token and repeatedly moves to the child
+# whose token equals the target's argmax of the current row.  With a chain
+# (every node's parent the node before it) this is exactly `verify`.
+
+def tree_depths(parents) -> np.ndarray:
+    """Depth of each node: 1 for children of the pending token (parent -1),
+    else 1 + the parent's depth.  Parents must precede their children."""
+    par = [int(p) for p in parents]
+    dep = np.zeros(len(par), dtype=np.int64)
+    for j, p in enumerate(par):
+        assert -1 <= p < j, "a node's parent is the pending token or an earlier node"
+        dep[j] = 1 if p < 0 else dep[p] + 1
+    return dep
+
+
+def tree_ancestors(parents) -> np.ndarray:
+    """allowed[i, j] over the rows [pending] + nodes: row j is row i itself or
+    one of its ancestors (row 0, the pending token, is every row's root)."""
+    n = len(parents)
+    allowed = np.zeros((n + 1, n + 1), dtype=bool)
+    allowed[0, 0] = True
+    for j, p in enumerate(parents):
+        r = j + 1
+        allowed[r] = allowed[int(p) + 1]
+        allowed[r, r] = True
+    return allowed
+
+
+def attend_masked(q, K, V, allowed):
+    """Grouped-query attention with an explicit mask allowed [n, T] over the
+    key rows of K, V [T, Hkv, dh]."""
+    n, Hq, dh = q.shape
+    group = Hq // K.shape[1]
+    out = np.empty_like(q)
+    scale = 1.0 / np.sqrt(dh)
+    for h in range(Hq):
+        g = h // group
+        s = (q[:, h, :] @ K[:, g, :].T) * scale
+        s = np.where(allowed, s, -np.inf)
+        out[:, h, :] = softmax_rows(s) @ V[:, g, :]
+    return out
+
+
+def forward_tree(model: OracleModel, K_cache, V_cache, tokens, positions, row_allowed):
+    """Decoder forward of rows ``tokens`` at ``positions`` over cached K/V of
+    ctx positions; row i sees every cached position and the new rows j with
+    row_allowed[i, j].  Same layer arithmetic as `forward`."""
+    c = model.cfg
+    tokens = np.asarray(tokens, dtype=np.int64)
+    positions = np.asarray(positions, dtype=np.int64)
+    n = tokens.shape[0]
+    ctx = 0 if K_cache is None or K_cache[0] is None else K_cache[0].shape[0]
+    allowed = np.concatenate([np.ones((n, ctx), dtype=bool), np.asarray(row_allowed, dtype=bool)], axis=1)
+    x = model.w("embed")[tokens] if model.cache else bf16_bits_to_float(
+        np.asarray(model.weights["embed"])[tokens], model.dtype)
+    new_k, new_v = [], []
+    for l in range(c.n_layers):
+        p = f"layers.{l}."
+        h = rms_norm(x, model.w(p + "attn_norm"), c.rms_eps)
+        q = (h @ model.w(p + "wq").T).reshape(n, c.n_q_heads, c.head_dim)
+        k = (h @ model.w(p + "wk").T).reshape(n, c.n_kv_heads, c.head_dim)
+        v = (h @ model.w(p + "wv").T).reshape(n, c.n_kv_heads, c.head_dim)
+        q = rotary(q, positions, c.rope_theta)
+        k = rotary(k, positions, c.rope_theta)
+        Kc = k if ctx == 0 else np.concatenate([K_cache[l], k], axis=0)
+        Vc = v if ctx == 0 else np.concatenate([V_cache[l], v], axis=0)
+        o = attend_masked(q, Kc, Vc, allowed).reshape(n, c.q_dim)
+        x = x + o @ model.w(p + "wo").T
+        h2 = rms_norm(x, model.w(p + "mlp_norm"), c.rms_eps)
+        a = silu(h2 @ model.w(p + "wg").T) * (h2 @ model.w(p + "wu").T)
+        x = x + a @ model.w(p + "wd").T
+        new_k.append(k)
+        new_v.append(v)
+    logits = rms_norm(x, model.w("final_norm"), c.rms_eps) @ model.w("lm_head").T
+    return logits, new_k, new_v
+
+
+def tree_accept(g, tokens, parents):
+    """The verification rule along a tree: from the pending token (row 0),
+    move to the child whose token equals the argmax of the current row
+    (lowest node index if several), until none does.  Returns the accepted
+    node indices in order; their count is the accepted length a."""
+    path, cur = [], -1
+    while True:
+        want = int(g[cur + 1])
+        nxt = next((j for j, p in enumerate(parents) if int(p) == cur and int(tokens[j]) == want), None)
+        if nxt is None:
+            return path
+        path.append(nxt)
+        cur = nxt
+
+
+@dataclass
+class TreeVerifyResult:
+    """Verify of a token tree: accepted node path, its length a, next token
+    (argmax of the last accepted row), per-row argmax and logits (row 0 =
+    pending, row j+1 = node j), and the tentative K/V rows."""
+    path: List[int]
+    next_token: int
+    tokens: np.ndarray
+    parents: np.ndarray
+    argmax: np.ndarray
+    logits: np.ndarray
+    new_k: list
+    new_v: list
+
+    @property
+    def accepted(self) -> int:
+        return len(self.path)
+
+    @property
+    def committed(self) -> List[int]:
+        return [int(self.tokens[j]) for j in self.path] + [int(self.next_token)]
+
+
+def verify_tree(model: OracleModel, st: SeqState, tokens, parents) -> TreeVerifyResult:
+    """One verification step over a token tree: forward the pending token
+    and every node (node at position ctx + depth, seeing its own path), take
+    each row's argmax and walk the accepted path."""
+    tok = np.asarray(tokens, dtype=np.int64).reshape(-1)
+    par = np.asarray(parents, dtype=np.int64).reshape(-1)
+    assert tok.shape == par.shape
+    dep = tree_depths(par)
+    rows = np.concatenate([[st.pending], tok]).astype(np.int64)
+    pos = st.ctx + np.concatenate([[0], dep])
+    logits, nk, nv = forward_tree(model, st.K if st.ctx else None, st.V if st.ctx else None, rows, pos,
+                                  tree_ancestors(par))
+    g = argmax_lowest(logits)
+    path = tree_accept(g, tok, par)
+    last = 0 if not path else path[-1] + 1
+    return TreeVerifyResult(path, int(g[last]), tok, par, g, logits, nk, nv)
+
+
+def commit_tree(st: SeqState, res: TreeVerifyResult, keep: Optional[int] = None) -> SeqState:
+    """Append the committed block of a tree verify: the pending row and the
+    first ``keep`` (default a) accepted nodes enter the cache in path order
+    (their positions are ctx, ctx + 1, ...), the rest is discarded."""
+    keep = res.accepted if keep is None else int(keep)
+    assert 0 <= keep <= res.accepted
+    rows = [0] + [j + 1 for j in res.path[:keep]]
+    K = [nk[rows] if (not st.K or st.K[l] is None) else np.concatenate([st.K[l], nk[rows]])
+         for l, nk in enumerate(res.new_k)]
+    V = [nv[rows] if (not st.V or st.V[l] is None) else np.concatenate([st.V[l], nv[rows]])
+         for l, nv in enumerate(res.new_v)]
+    last = rows[-1]
+    toks = list(st.tokens) + [int(res.tokens[j]) for j in res.path[:keep]] + [int(res.argmax[last])]
+    return SeqState(tokens=toks, K=K, V=V)

@@ -77,3 +77,37 @@ def test_acceptance_samplers():
     assert abs(np.mean(geo) - exact) < 0.05
     bi = [wt.bimodal_accept(rng, 64) for _ in range(4000)]
     assert all(0 <= a <= 2 or 32 <= a <= 64 for a in bi)
+
+
+def test_eagle_trees_are_breadth_first_and_bounded():
+    from workloads import trees
+    rng = wt.rng_for("misc", 41)
+    for _ in range(200):
+        n, depth, topk = int(rng.integers(1, 64)), int(rng.integers(1, 9)), int(rng.integers(1, 5))
+        par = trees.eagle_tree(rng, n, depth, topk)
+        assert 1 <= len(par) <= n
+        assert all(-1 <= p < j for j, p in enumerate(par))
+        assert max(len(trees.path_to(par, j)) for j in range(len(par))) <= depth
+        assert all(len(k) <= topk * topk for k in trees.children(par).values())
+
+
+def test_plant_path_gives_the_planted_acceptance_length():
+    from workloads import trees
+    rng = wt.rng_for("misc", 42)
+    for _ in range(200):
+        par = trees.eagle_tree(rng, 32, 8, 4)
+        greedy = rng.integers(0, 50, size=10)
+        a = int(rng.integers(0, 9))
+        tok = trees.plant_path(rng, par, greedy, a, 50)
+        for p, kids in trees.children(par).items():
+            assert len({int(tok[c]) for c in kids}) == len(kids)
+        # walk with the greedy continuation standing in for the target
+        cur, n = -1, 0
+        kids = trees.children(par)
+        while True:
+            nxt = [c for c in kids.get(cur, []) if tok[c] == greedy[n]]
+            if not nxt:
+                break
+            cur, n = nxt[0], n + 1
+        deepest = max(len(trees.path_to(par, j)) for j in range(len(par)))
+        assert n == min(a, deepest)

@@ -16,3 +16,4 @@ from .weights import (  # noqa: F401
 )
 from . import tokens  # noqa: F401
 from . import batches  # noqa: F401
+from . import trees  # noqa: F401
