@@ -128,6 +128,32 @@ hvd_status hvd_verify(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_
                       const int32_t* ctx_lens, const int32_t* draft_tokens, const int32_t* draft_lens,
                       int32_t* accepted_len, int32_t* next_token, float* logits);
 
+/* One verification step over token trees (the tree-shaped drafts of the
+ * model drafter, App. A: EAGLE3 with tree depth 8 and top-k 4), under the
+ * same rule: for sequence b, node_counts[b] = n_b <= 63 nodes, packed in
+ * batch order in node_tokens and node_parents (sum n_b entries each).  Node
+ * j's parent is node_parents[j] = -1 (the pending token) or an earlier node
+ * of the same tree (< j).  One forward covers the pending token (rotary
+ * position ctx_b) and every node (rotary position ctx_b + depth, depth 1 for
+ * children of the pending token); each row attends to the cached context
+ * and to the rows on its own path.  The accepted path starts at the pending
+ * token and moves to the child whose token is the target's argmax of the
+ * current row (the lowest node index if several), while one exists.
+ * Outputs (host): accepted_len[b] = a_b, the path length; next_token[b] =
+ * the argmax of the path's last row; accepted_nodes (nullable, [batch][63])
+ * receives the path's node indices in order.  The K/V of the path is moved
+ * to positions ctx_b + 1 .. ctx_b + a_b before the call returns, so
+ * hvd_commit keeps a prefix of the path exactly as for a chain draft (the
+ * pending token after keep < a_b is the token of path node keep).  logits
+ * (nullable, DEVICE) receives fp32 logits [sum(n_b + 1)][vocab], row 0 of
+ * each sequence the pending token, row j + 1 node j.  Errors as hvd_verify;
+ * a node count outside [0, 63] is HVD_ERR_RANGE, a parent that is not -1 or
+ * an earlier node HVD_ERR_ARG. */
+hvd_status hvd_verify_tree(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_ids,
+                           const int32_t* ctx_lens, const int32_t* node_tokens, const int32_t* node_parents,
+                           const int32_t* node_counts, int32_t* accepted_len, int32_t* next_token,
+                           int32_t* accepted_nodes, float* logits);
+
 /* Commit the last verify of each listed sequence (Alg. 1: append z_t).
  * keep_lens (nullable = the accepted lengths) keeps 0 <= keep <= a_b draft
  * tokens: ctx_len += keep + 1 and the new pending token is the target's argmax

@@ -286,11 +286,11 @@ extern "C" void hvd_model_free(hvd_model m) {
 // rows, sequences, attention grid sizes and kernel variants (chunk length,
 // rows per item), LM head on/off and the logits pointer.
 struct GraphKey {
-  int M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head;
+  int M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head, tree;
   float* logits;
   bool operator<(const GraphKey& o) const {
-    return std::tie(M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head, logits) <
-           std::tie(o.M, o.B, o.n_items, o.n_heads, o.chunk, o.rpi, o.comb_rows, o.lm_head, o.logits);
+    return std::tie(M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head, tree, logits) <
+           std::tie(o.M, o.B, o.n_items, o.n_heads, o.chunk, o.rpi, o.comb_rows, o.lm_head, o.tree, o.logits);
   }
 };
 
@@ -361,8 +361,8 @@ size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int p
   // items <= units + kPartSlots and heads <= units, each padded up (to 64
   // and 16 entries); header and per-section alignment fit in the last term
   const size_t item_ints = sizeof(AttnItem) / 4;
-  return 4 * (size_t)max_rows + 4 * (size_t)max_seqs + item_ints * (2 * units + kPartSlots + 64 + 16) +
-         3 * (size_t)max_seqs * pt_stride + 64;
+  return (4 + 3) * (size_t)max_rows + sizeof(SeqMeta) / 4 * (size_t)max_seqs +
+         item_ints * (2 * units + kPartSlots + 64 + 16) + 3 * (size_t)max_seqs * pt_stride + 64;
 }
 
 size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, void* base) {
@@ -394,7 +394,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->gemm_part = cv.take<float>(kGemmPartBytes / 4);
   k->inv_rms = cv.take<float>(Mp);
   k->g = cv.take<int32_t>(Mp);
-  k->out = cv.take<int32_t>(2 * (size_t)max_seqs);
+  k->out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)max_seqs);  // [B][2] results, then [B][63] tree paths
   k->counter = cv.take<uint32_t>(64);
   k->part_o = cv.take<float>((size_t)kPartSlots * kAttnRows * c.head_dim);
   k->part_ml = cv.take<float>((size_t)kPartSlots * kAttnRows * 2);
@@ -436,7 +436,8 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   }
   carve_kv(k, c, max_seqs, n_pages, k->base);
   if (hipHostMalloc((void**)&k->meta_host, k->meta_ints * 4, hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&k->out_host, 2 * (size_t)max_seqs * 4, hipHostMallocDefault) != hipSuccess) {
+      hipHostMalloc((void**)&k->out_host, (2 + kMaxTreeNodes) * (size_t)max_seqs * 4, hipHostMallocDefault) !=
+          hipSuccess) {
     if (k->meta_host) (void)hipHostFree(k->meta_host);
     if (k->owned) (void)hipFree(k->base);
     delete k;
@@ -561,7 +562,7 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   auto item = [&](const Unit& u, int c, int nch, int part, int chunk) {
     const SeqMeta& s = seqs[u.b];
     AttnItem it{};
-    it.slot = s.slot; it.ctx = s.ctx; it.k = s.k; it.cu = s.cu;
+    it.slot = s.slot; it.ctx = s.ctx; it.k = s.k; it.cu = s.cu; it.tree = s.tree;
     it.g = u.g; it.c = c; it.nch = nch; it.rg = u.rg; it.part = part;
     it.p_begin = c * chunk;
     it.p_end = std::min(s.ctx + s.k + 1, (c + 1) * chunk);
@@ -618,10 +619,17 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   return true;
 }
 
+// rows[].kvs holds each row's K/V position on entry; tree (optional): per
+// row, the ancestor mask over positions ctx.. and the parent node.
+struct TreeRows {
+  std::vector<uint64_t> mask;
+  std::vector<int32_t> parent;
+};
+
 hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<RowMeta> rows, bool lm_head,
-                   float* logits) {
-  // each row's K/V page (the QKV epilogue writes K/V there)
-  for (RowMeta& r : rows) r.page = k->hs->seq(r.slot).pages[(size_t)(r.pos / kPage)];
+                   float* logits, const TreeRows* tree = nullptr) {
+  // each row's pool slot: page * kPage + offset (the QKV epilogue writes K/V there)
+  for (RowMeta& r : rows) r.kvs = k->hs->seq(r.slot).pages[(size_t)(r.kvs / kPage)] * kPage + r.kvs % kPage;
   hvd_model_s* m = k->m;
   const hvd_config& c = m->cfg;
   hipStream_t s = k->stream;
@@ -667,7 +675,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     off += (ints + 3) / 4 * 4;
     return o;
   };
-  const size_t need_ints = 16 + 4 * (size_t)M + 4 * (size_t)B + 32 * (n_items + n_heads) + 3 * last.size() + 32;
+  const size_t need_ints = 16 + 4 * (size_t)M + sizeof(SeqMeta) / 4 * (size_t)B + 32 * (n_items + n_heads) +
+                           3 * (size_t)M + 3 * last.size() + 40;
   if (need_ints > k->meta_ints) {
     k->hs->take_updates();
     return set_err(HVD_ERR_OOM, "metadata buffer too small");
@@ -675,9 +684,17 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   int32_t header[16] = {(int32_t)last.size()};
   put(header, 16);
   const size_t o_rows = put(rows.data(), 4 * (size_t)M);
-  const size_t o_seqs = put(seqs.data(), 4 * (size_t)B);
+  const size_t o_seqs = put(seqs.data(), sizeof(SeqMeta) / 4 * (size_t)B);
   const size_t o_items = put(plan.items.data(), sizeof(AttnItem) / 4 * n_items);
   const size_t o_heads = put(plan.heads.data(), sizeof(AttnItem) / 4 * n_heads);
+  // tree rows (fixed size per M, before the variable-length updates so every
+  // offset a captured graph holds depends on the graph key only)
+  off = (off + 7) / 8 * 8;  // 8-byte alignment of the masks
+  size_t o_mask = 0, o_parent = 0;
+  if (tree) {
+    o_mask = put(tree->mask.data(), 2 * (size_t)M);
+    o_parent = put(tree->parent.data(), (size_t)M);
+  }
   std::vector<int32_t> upd;
   for (auto& kv : last) {
     upd.push_back(kv.first.first);
@@ -690,6 +707,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   const SeqMeta* d_seqs = (const SeqMeta*)(k->meta_dev + o_seqs);
   const AttnItem* d_items = (const AttnItem*)(k->meta_dev + o_items);
   const AttnItem* d_heads = (const AttnItem*)(k->meta_dev + o_heads);
+  const uint64_t* d_mask = tree ? (const uint64_t*)(k->meta_dev + o_mask) : nullptr;
+  const int32_t* d_parent = tree ? k->meta_dev + o_parent : nullptr;
 
   // ---------------------------------------------------------------- launches
   // Everything below only enqueues kernels whose arguments are fixed by
@@ -844,6 +863,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.MTtot = MT;
       a.part_o = k->part_o;
       a.part_ml = k->part_ml;
+      a.tree_mask = d_mask;
       {
         ProfScope ps(k, PF_ATTN, kv_bytes);
         HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, rpi, s));
@@ -931,9 +951,27 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     ac.B = B;
     ac.out = k->out;
     ac.counter = k->counter;
+    ac.tree_parent = d_parent;
+    ac.path = k->out + 2 * B;
     {
       ProfScope ps(k, PF_OTHER, 0.0);
       HIP_TRY(launch_accept(ac, s));
+    }
+    if (tree) {
+      CompactArgs cp{};
+      cp.pool = k->pool;
+      cp.page_stride = k->page_stride;
+      cp.layer_stride = k->layer_stride;
+      cp.n_layers = c.n_layers;
+      cp.Hkv = c.n_kv_heads;
+      cp.dh = dh;
+      cp.pt = k->pt;
+      cp.pt_stride = k->pt_stride;
+      cp.seqs = d_seqs;
+      cp.out = k->out;
+      cp.path = k->out + 2 * B;
+      ProfScope ps(k, PF_OTHER, 0.0);
+      HIP_TRY(launch_compact(cp, B, s));
     }
   }
   return HVD_OK;
@@ -942,7 +980,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   if (k->prof || !k->use_graphs) {
     if (hvd_status st = launch_all(); st != HVD_OK) return st;
   } else {
-    const GraphKey key{M, B, (int)n_items, (int)n_heads, plan.chunk, rpi, comb_rows, lm_head ? 1 : 0, logits};
+    const GraphKey key{M, B, (int)n_items, (int)n_heads, plan.chunk, rpi, comb_rows, lm_head ? 1 : 0,
+                       tree ? 1 : 0, logits};
     auto it = k->graphs.find(key);
     if (it == k->graphs.end()) {
       if (k->graphs.size() >= kMaxGraphs) {
@@ -966,7 +1005,9 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     }
     HIP_TRY(hipGraphLaunch(it->second, s));
   }
-  if (lm_head) HIP_TRY(hipMemcpyAsync(k->out_host, k->out, 2 * (size_t)B * 4, hipMemcpyDeviceToHost, s));
+  if (lm_head)  // results, and for trees the accepted paths behind them
+    HIP_TRY(hipMemcpyAsync(k->out_host, k->out, (tree ? 2 + kMaxTreeNodes : 2) * (size_t)B * 4,
+                           hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (k->prof) prof_collect(k);
   return HVD_OK;
@@ -988,7 +1029,7 @@ extern "C" hvd_status hvd_prefill(hvd_model m, hvd_kv k, int32_t seq_id, const i
     const int cnt = std::min(kPrefillRows, body - s0);
     std::vector<SeqMeta> seqs{{seq_id, s0, cnt - 1, 0}};
     std::vector<RowMeta> rows(cnt);
-    for (int i = 0; i < cnt; ++i) rows[i] = {tokens[s0 + i], seq_id, s0 + i, 0};
+    for (int i = 0; i < cnt; ++i) rows[i] = {tokens[s0 + i], seq_id, s0 + i, s0 + i};
     hvd_status st = forward(k, seqs, rows, false, nullptr);
     if (st != HVD_OK) {
       k->hs->abort_prefill(seq_id);
@@ -1014,8 +1055,9 @@ extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int
     const SeqSlot& sl = k->hs->seq(seq_ids[b]);
     const int kk = draft_lens[b];
     seqs[b] = {seq_ids[b], sl.ctx, kk, (int32_t)rows.size()};
-    rows.push_back({sl.pending, seq_ids[b], sl.ctx, 0});
-    for (int i = 0; i < kk; ++i) rows.push_back({draft_tokens[off + i], seq_ids[b], sl.ctx + 1 + i, 0});
+    rows.push_back({sl.pending, seq_ids[b], sl.ctx, sl.ctx});
+    for (int i = 0; i < kk; ++i)
+      rows.push_back({draft_tokens[off + i], seq_ids[b], sl.ctx + 1 + i, sl.ctx + 1 + i});
     off += kk;
   }
   hvd_status st = forward(k, seqs, rows, true, logits);
@@ -1028,6 +1070,79 @@ extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int
     next_token[b] = k->out_host[2 * b + 1];
   }
   k->hs->finish_verify(batch, seq_ids, draft_tokens, draft_lens, accepted_len, next_token);
+  return HVD_OK;
+}
+
+extern "C" hvd_status hvd_verify_tree(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids,
+                                      const int32_t* ctx_lens, const int32_t* node_tokens, const int32_t* node_parents,
+                                      const int32_t* node_counts, int32_t* accepted_len, int32_t* next_token,
+                                      int32_t* accepted_nodes, float* logits) {
+  if (!m || !k) return set_err(HVD_ERR_ARG, "null handle");
+  if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
+  if (!accepted_len || !next_token) return set_err(HVD_ERR_ARG, "null output");
+  if (batch < 1 || !node_counts) return set_err(HVD_ERR_ARG, "bad batch");
+  // tree structure first (node counts, parents before children), then the
+  // checks every verify makes (tokens, positions, pages) on the node list
+  {
+    int64_t off = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int n = node_counts[b];
+      if (n < 0 || n > kMaxTreeNodes) return set_err(HVD_ERR_RANGE, "tree node count outside [0, 63]");
+      if (n > 0 && (!node_tokens || !node_parents)) return set_err(HVD_ERR_ARG, "null tree arrays");
+      for (int j = 0; j < n; ++j)
+        if (node_parents[off + j] < -1 || node_parents[off + j] >= j)
+          return set_err(HVD_ERR_ARG, "a node's parent must be -1 or an earlier node");
+      off += n;
+    }
+  }
+  if (hvd_status st = from_host(k->hs->begin_verify(batch, seq_ids, ctx_lens, node_tokens, node_counts), k);
+      st != HVD_OK)
+    return st;
+  std::vector<SeqMeta> seqs(batch);
+  std::vector<RowMeta> rows;
+  TreeRows tr;
+  int64_t off = 0;
+  for (int b = 0; b < batch; ++b) {
+    const SeqSlot& sl = k->hs->seq(seq_ids[b]);
+    const int n = node_counts[b];
+    seqs[b] = {seq_ids[b], sl.ctx, n, (int32_t)rows.size(), 1};
+    // row 0: the pending token; row j + 1: node j at rotary position
+    // ctx + depth, K/V position ctx + 1 + j; ancestor bits over rows
+    std::vector<int> depth(n);
+    std::vector<uint64_t> anc(n + 1);
+    anc[0] = 1;
+    rows.push_back({sl.pending, seq_ids[b], sl.ctx, sl.ctx});
+    tr.mask.push_back(anc[0]);
+    tr.parent.push_back(-1);
+    for (int j = 0; j < n; ++j) {
+      const int p = node_parents[off + j];
+      depth[j] = p < 0 ? 1 : depth[p] + 1;
+      anc[j + 1] = anc[p + 1] | (1ull << (j + 1));
+      rows.push_back({node_tokens[off + j], seq_ids[b], sl.ctx + depth[j], sl.ctx + 1 + j});
+      tr.mask.push_back(anc[j + 1]);
+      tr.parent.push_back(p);
+    }
+    off += n;
+  }
+  hvd_status st = forward(k, seqs, rows, true, logits, &tr);
+  if (st != HVD_OK) {
+    k->hs->abort_verify(batch, seq_ids);
+    return st;
+  }
+  // the accepted path's tokens become the "draft" that commit keeps a prefix of
+  std::vector<int32_t> path_tokens, acc(batch);
+  off = 0;
+  for (int b = 0; b < batch; ++b) {
+    accepted_len[b] = acc[b] = k->out_host[2 * b];
+    next_token[b] = k->out_host[2 * b + 1];
+    const int32_t* path = k->out_host + 2 * batch + (size_t)b * kMaxTreeNodes;
+    for (int d = 0; d < acc[b]; ++d) {
+      path_tokens.push_back(node_tokens[off + path[d]]);
+      if (accepted_nodes) accepted_nodes[(size_t)b * kMaxTreeNodes + d] = path[d];
+    }
+    off += node_counts[b];
+  }
+  k->hs->finish_verify(batch, seq_ids, path_tokens.data(), acc.data(), accepted_len, next_token);
   return HVD_OK;
 }
 

@@ -2,13 +2,16 @@
 //
 // For one sequence, the (k+1) query rows of the verify step times the
 // Hq/Hkv q-heads of one kv head g form R = (k+1)*group query vectors; row
-// r = i*group + hh is draft row i (position ctx+i) of q-head g*group+hh and
-// may attend to key positions 0..ctx+i.  A workgroup (4 waves) handles one KV
-// chunk of one (sequence, kv head, row group of up to 128 rows), in
-// sub-chunks of up to kAttnChunk positions: it copies a sub-chunk's K and V
-// pages into LDS with every load in flight at once (decode-size chunks are
-// latency-bound, not bandwidth-bound), then each wave runs its <= 2 row tiles
-// over it, carrying the online-softmax state to the next sub-chunk.
+// r = i*group + hh is draft row i (K/V at position ctx+i) of q-head
+// g*group+hh and may attend to key positions 0..ctx+i.  For a token tree,
+// row i is the pending token (i = 0) or node i-1, and it attends to
+// positions 0..ctx-1 and to the positions of its ancestors and itself.  A
+// workgroup (4 or 8 waves) handles one KV chunk of one (sequence, kv head,
+// row group of 64, 128 or 256 rows), in sub-chunks of up to kAttnChunk
+// positions: it copies a sub-chunk's K and V pages into LDS with every load
+// in flight at once (decode-size chunks are latency-bound, not
+// bandwidth-bound), then each wave runs its 1 or 2 row tiles over it,
+// carrying the online-softmax state to the next sub-chunk.
 //
 // Scores are computed transposed, S^T = K Q^T, so the fp32 C fragment of a
 // lane holds 4 key positions of one query row; the same registers, converted
@@ -18,7 +21,9 @@
 // ([dh][16]) and kept transposed in LDS.  LDS rows are XOR-swizzled so the
 // 16 lanes of a fragment read hit distinct banks.
 // Online softmax in fp32 base 2 (the hardware exp2, whose results below
-// 2^-126 flush to zero); rows see only their causal prefix; keys at
+// 2^-126 flush to zero); rows see only their causal prefix (for a token
+// tree: the context and the positions of their own path, from a per-row
+// ancestor mask); keys at
 // positions >= ctx+k+1 are never used (their contents may be stale).
 // A single-chunk item writes the normalized output straight into the O GEMM's
 // hi/lo operand; multi-chunk items write (m, l, unnormalized O) partials that
@@ -62,6 +67,7 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
   if (kdr < 0) return;  // grid padding
   const int slot = ip->slot, ctx = ip->ctx, cu = ip->cu, g = ip->g;
   const int nch = ip->nch, rg = ip->rg, part = ip->part;
+  const bool tree = ip->tree != 0;  // token tree: rows see the context and their own path
   const int p_begin = ip->p_begin, p_end = ip->p_end;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -93,6 +99,13 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
   // past the sub-chunk's end repeat its first page (in-bounds, cached; their
   // V is zeroed when staged).  The next sub-chunk's loads are issued before
   // the current one is computed, so its latency hides behind the MFMAs.
+  // tree rows: ancestor sets (rows past R take the last row's)
+  uint64_t anc[TPW];
+#pragma unroll
+  for (int q = 0; q < TPW; ++q) {
+    const int r = tile_row[q];
+    anc[q] = tree ? a.tree_mask[cu + (r < R ? r / G : kdr)] : 0;
+  }
   // query fragments (rows past R read a valid row; their results are dropped)
 #pragma unroll
   for (int q = 0; q < TPW; ++q) {
@@ -190,6 +203,8 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
         const int r = tile_row[q];
         lim[q] = ctx + (r < R ? r / G : kdr) - sub;
       }
+      // smallest of them over the wave (its first row: rows ascend)
+      const int lim_min = tree ? ctx - 1 - sub : ctx + (rg * RPI + wave * 16) / G - sub;
 #pragma unroll 1
       for (int g0 = 0; g0 < NB; g0 += SG) {  // not unrolled: keeps each group's LDS reads in its group
         f32x4 sc[TPW][SG];
@@ -211,34 +226,52 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
             }
         }
         f16x8 pf[TPW][SG / 2 > 0 ? SG / 2 : 1];
+        // whole group visible to every row of the wave (wave-uniform): no mask
+        const bool full = (g0 + SG) * 16 <= min(lim_min + 1, n_pos);
 #pragma unroll
         for (int q = 0; q < TPW; ++q) {
           if (q > 0 && !tile_on[q]) continue;
+          // running max m in log2 units; scores scaled inside the exp2's fma
           float bm = -INFINITY;
+          if (full) {
 #pragma unroll
-          for (int b = 0; b < SG; ++b)
+            for (int b = 0; b < SG; ++b)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int pa = (g0 + b) * 16 + lg * 4 + j;
-              sc[q][b][j] = (pa <= lim[q] && pa < n_pos) ? sc[q][b][j] * a.scale_log2 : -INFINITY;
-              bm = fmaxf(bm, sc[q][b][j]);
-            }
+              for (int j = 0; j < 4; ++j) bm = fmaxf(bm, sc[q][b][j]);
+          } else {
+#pragma unroll
+            for (int b = 0; b < SG; ++b)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const int pa = (g0 + b) * 16 + lg * 4 + j;
+                bool vis = pa <= lim[q];
+                if (tree) {  // the context, then the row's ancestors (bit j = position ctx + j)
+                  const int rel = pa + sub - ctx;
+                  vis = rel < 0 || ((anc[q] >> (rel & 63)) & 1);
+                }
+                sc[q][b][j] = (vis && pa < n_pos) ? sc[q][b][j] : -INFINITY;
+                bm = fmaxf(bm, sc[q][b][j]);
+              }
+          }
           bm = fmaxf(bm, __shfl_xor(bm, 16));
           bm = fmaxf(bm, __shfl_xor(bm, 32));
-          const float mn = fmaxf(m[q], bm);
-          const float alpha = (m[q] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[q] - mn);
+          const float mn = fmaxf(m[q], bm * a.scale_log2);
+          const float ms = mn == -INFINITY ? 0.f : mn;  // nothing visible yet: every weight is 0
+          const float alpha = __builtin_amdgcn_exp2f(m[q] - ms);
           float ps = 0.f;
 #pragma unroll
           for (int b = 0; b < SG; ++b)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-              sc[q][b][j] = (sc[q][b][j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sc[q][b][j] - mn);
+              sc[q][b][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][b][j], a.scale_log2, -ms));
               ps += sc[q][b][j];
             }
           lsum[q] = lsum[q] * alpha + ps;
           m[q] = mn;
+          if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {  // the max moved for some row
 #pragma unroll
-          for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
+            for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
+          }
           // B operand of block pair c: positions 32c' + {4lg..4lg+3} and
           // 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
 #pragma unroll

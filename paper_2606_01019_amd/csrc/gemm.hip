@@ -60,7 +60,7 @@ struct EpiPre {
   float gain[EPI == EPI_RESID ? COLS : 1];
   float2 rope[EPI == EPI_QKV ? ROWS : 1][EPI == EPI_QKV ? COLS / 2 : 1];
   int page[EPI == EPI_QKV ? ROWS : 1];
-  int pos[EPI == EPI_QKV ? ROWS : 1];
+  int pos[EPI == EPI_QKV ? ROWS : 1];  // the K/V position's offset in its page
 };
 
 // The same inputs on their way in, held in registers.  epi_issue() requests
@@ -144,7 +144,7 @@ __device__ __forceinline__ void epi_settle(EpiRegs<MT, NS, EPI>& e) {
     asm volatile("" : "+v"(e.gain));
   }
   if constexpr (EPI == EPI_QKV) {
-    asm volatile("" : "+v"(e.rm.pos), "+v"(e.rm.page));
+    asm volatile("" : "+v"(e.rm.pos), "+v"(e.rm.kvs));
 #pragma unroll
     for (int i = 0; i < E::RQ; ++i) asm volatile("" : "+v"(e.rpos[i]));
   }
@@ -216,8 +216,8 @@ __device__ __forceinline__ void epi_commit(const GemmArgs& a, const EpiRegs<MT, 
   if constexpr (EPI == EPI_QKV) {
     if (tid < rows_here) {
       const bool ok = row0 + tid < a.M;
-      p.pos[tid] = ok ? e.rm.pos : 0;
-      p.page[tid] = ok ? e.rm.page : 0;
+      p.pos[tid] = ok ? (e.rm.kvs & (kPage - 1)) : 0;
+      p.page[tid] = ok ? e.rm.kvs / kPage : 0;
     }
   }
 }

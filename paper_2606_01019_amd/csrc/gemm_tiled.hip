@@ -110,15 +110,15 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
                 *(uint32_t*)(a.Q + (size_t)R * a.q_cols + C) = packed;
               } else {
                 const int g = (C - base) / a.dh;
-                *(uint32_t*)(a.kv + (size_t)rm.page * a.page_stride + ((size_t)g * kPage + (rm.pos & 15)) * a.dh +
-                             dp) = packed;
+                *(uint32_t*)(a.kv + (size_t)(rm.kvs / kPage) * a.page_stride +
+                             ((size_t)g * kPage + (rm.kvs & (kPage - 1))) * a.dh + dp) = packed;
               }
             }
           } else {
             const int cv = C - a.q_cols - a.kv_cols;
             const int g = cv / a.dh, d = cv % a.dh;
-            a.kv[(size_t)rm.page * a.page_stride + (size_t)a.Hkv * kPage * a.dh + ((size_t)g * a.dh + d) * kPage +
-                 (rm.pos & 15)] = (_Float16)v;
+            a.kv[(size_t)(rm.kvs / kPage) * a.page_stride + (size_t)a.Hkv * kPage * a.dh +
+                 ((size_t)g * a.dh + d) * kPage + (rm.kvs & (kPage - 1))] = (_Float16)v;
           }
         }
       } else if constexpr (EPI == EPI_RESID) {

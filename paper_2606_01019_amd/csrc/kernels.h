@@ -29,16 +29,22 @@ inline void hvd_launch(F kernel, const dim3& grid, const dim3& block, uint32_t l
 constexpr int kPage = 16;        // tokens per KV page
 constexpr int kAttnChunk = 256;  // most KV positions one attention workgroup stages in LDS
 
-// Row metadata of one forward: token, sequence slot, absolute position, and
-// the pool page holding that position's K/V.
+// Row metadata of one forward: token, sequence slot, rotary position, and
+// where the row's K/V goes: kvs = pool page * kPage + offset in the page.
+// (For a chain row the K/V position is its rotary position; a tree node at
+// depth d sits at rotary position ctx + d and K/V position ctx + 1 + node.)
 struct RowMeta {
-  int32_t tok, slot, pos, page;
+  int32_t tok, slot, pos, kvs;
 };
-// Sequence metadata of one forward: slot, cached length, draft length k,
-// first row (rows cu .. cu+k).
+// Sequence metadata of one forward: slot, cached length, draft length k (or
+// tree node count), first row (rows cu .. cu+k), tree = 1 for a token tree.
 struct SeqMeta {
   int32_t slot, ctx, k, cu;
+  int32_t tree, pad0, pad1, pad2;
 };
+// Token trees: at most this many nodes, so a row's ancestor set over the
+// pending token and the nodes fits one 64-bit mask (bit 0 = pending row).
+constexpr int kMaxTreeNodes = 63;
 // One attention work item, self-contained so a workgroup needs no other
 // metadata: sequence slot, cached length ctx, draft length k, first row cu;
 // kv head g; KV chunk c of nch covering positions [p_begin, p_end); the row
@@ -50,7 +56,7 @@ constexpr int kItemPages = 16;  // kAttnChunk / kPage
 struct AttnItem {
   int32_t slot, ctx, k, cu;
   int32_t g, c, nch, rg;
-  int32_t part, p_begin, p_end, pad0;
+  int32_t part, p_begin, p_end, tree;
   int32_t pad1, pad2, pad3, pad4;
   int32_t pages[kItemPages];
 };
@@ -112,6 +118,7 @@ struct AttnArgs {
   int MTtot;
   float* part_o;       // [slots][rows per item][dh] fp32 unnormalized output of one chunk
   float* part_ml;      // [slots][rows per item][2] running max (base 2) and sum
+  const uint64_t* tree_mask;  // [rows]: tree rows' ancestor sets over positions ctx.. (bit j = ctx + j)
 };
 
 struct CombineArgs {
@@ -154,6 +161,20 @@ struct AcceptArgs {
   int B;
   int32_t* out;        // [B][2]: accepted, next
   uint32_t* counter;   // one uint32, zero between launches
+  const int32_t* tree_parent;  // [rows]: parent node of a tree row (-1 = the pending token)
+  int32_t* path;       // [B][kMaxTreeNodes]: accepted node indices of tree sequences
+};
+// Moves the K/V of each tree sequence's accepted path from the nodes'
+// positions (ctx + 1 + node) to the chain positions ctx + 1 .. ctx + a.
+struct CompactArgs {
+  _Float16* pool;      // all layers
+  size_t page_stride, layer_stride;
+  int n_layers, Hkv, dh;
+  const int32_t* pt;
+  int pt_stride;
+  const SeqMeta* seqs;
+  const int32_t* out;  // [B][2] accepted, next
+  const int32_t* path; // [B][kMaxTreeNodes]
 };
 
 // Launchers: all enqueue on `s` and return the launch status.
@@ -178,6 +199,7 @@ hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_i
 hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+hipError_t launch_compact(const CompactArgs& a, int B, hipStream_t s);
 
 constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
 

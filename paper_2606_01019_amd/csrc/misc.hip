@@ -137,17 +137,74 @@ __global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
   __threadfence();
   for (int b = threadIdx.x; b < a.B; b += 256) {
     const SeqMeta sq = a.seqs[b];
-    int acc = 0;
-    while (acc < sq.k) {
-      const int drafted = a.rows[sq.cu + acc + 1].tok;  // draft token acc
-      const int target = __atomic_load_n(&a.g[sq.cu + acc], __ATOMIC_RELAXED);
-      if (drafted != target) break;
-      ++acc;
+    int acc = 0, last = 0;  // accepted count; row of the last accepted token
+    if (!sq.tree) {
+      while (acc < sq.k) {
+        const int drafted = a.rows[sq.cu + acc + 1].tok;  // draft token acc
+        const int target = __atomic_load_n(&a.g[sq.cu + acc], __ATOMIC_RELAXED);
+        if (drafted != target) break;
+        ++acc;
+      }
+      last = acc;
+    } else {
+      // from the pending token, move to the child (lowest node index) whose
+      // token is the target's argmax of the current row, while one exists
+      int cur = -1;
+      for (;;) {
+        const int target = __atomic_load_n(&a.g[sq.cu + cur + 1], __ATOMIC_RELAXED);
+        int nxt = -1;
+        for (int j = cur + 1; j < sq.k; ++j)  // children come after their parent
+          if (a.tree_parent[sq.cu + 1 + j] == cur && a.rows[sq.cu + 1 + j].tok == target) {
+            nxt = j;
+            break;
+          }
+        if (nxt < 0) break;
+        a.path[b * kMaxTreeNodes + acc] = nxt;
+        ++acc;
+        cur = nxt;
+      }
+      last = cur + 1;
     }
     a.out[2 * b] = acc;
-    a.out[2 * b + 1] = __atomic_load_n(&a.g[sq.cu + acc], __ATOMIC_RELAXED);
+    a.out[2 * b + 1] = __atomic_load_n(&a.g[sq.cu + last], __ATOMIC_RELAXED);
   }
   if (threadIdx.x == 0) *a.counter = 0u;
+}
+
+// After a tree verify: the accepted path's K/V moves from the nodes'
+// positions ctx + 1 + node to the chain positions ctx + 1 .. ctx + a, so a
+// commit keeps a prefix exactly as for a chain.  One block per (sequence,
+// layer); each thread owns fixed (kv head, dims) across all positions and
+// moves them in path order (target ctx + d never holds a later source:
+// nodes follow their parents, so path node d - 1 has index >= d - 1).
+__global__ __launch_bounds__(256) void tree_compact(CompactArgs a) {
+  const int b = blockIdx.x, l = blockIdx.y;
+  const SeqMeta sq = a.seqs[b];
+  if (!sq.tree) return;
+  const int acc = a.out[2 * b];
+  const int32_t* ptrow = a.pt + (size_t)sq.slot * a.pt_stride;
+  _Float16* lay = a.pool + (size_t)l * a.layer_stride;
+  const size_t vhalf = (size_t)a.Hkv * kPage * a.dh;
+  const int n_k = a.Hkv * a.dh / 8;  // 16-byte K units (8 dims) per position
+  const int n_v = a.Hkv * a.dh;      // V elements per position
+  for (int d = 1; d <= acc; ++d) {
+    const int src = sq.ctx + 1 + a.path[b * kMaxTreeNodes + d - 1], dst = sq.ctx + d;
+    if (src == dst) continue;
+    const size_t ps = (size_t)ptrow[src / kPage] * a.page_stride, pd = (size_t)ptrow[dst / kPage] * a.page_stride;
+    const int ts = src % kPage, td = dst % kPage;
+    for (int u = threadIdx.x; u < n_k; u += 256) {
+      const int g = u / (a.dh / 8), c8 = (u % (a.dh / 8)) * 8;
+      *(uint4*)(lay + pd + ((size_t)g * kPage + td) * a.dh + c8) =
+          *(const uint4*)(lay + ps + ((size_t)g * kPage + ts) * a.dh + c8);
+    }
+    for (int e = threadIdx.x; e < n_v; e += 256)  // V is [kv head][dim][16 positions] in a page
+      lay[pd + vhalf + (size_t)e * kPage + td] = lay[ps + vhalf + (size_t)e * kPage + ts];
+  }
+}
+
+hipError_t launch_compact(const CompactArgs& a, int B, hipStream_t s) {
+  hvd_launch(tree_compact, dim3(B, a.n_layers), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {

@@ -18,11 +18,12 @@ _STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM
            -5: "HVD_ERR_DEVICE"}
 
 EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
-           "hvd_prefill", "hvd_verify", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
+           "hvd_prefill", "hvd_verify", "hvd_verify_tree", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
            "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error")
 HVD_OPT_GRAPHS = 1
 HVD_OPT_MLP_SINGLE = 2
 HVD_OPT_LM_SINGLE = 3
+MAX_TREE_NODES = 63  # nodes per token tree (hvd_verify_tree)
 
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
@@ -74,6 +75,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hvd_kv_free": (None, [P]),
         "hvd_prefill": (I32, [P, P, I32, PI32, I32]),
         "hvd_verify": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
+        "hvd_verify_tree": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
         "hvd_commit": (I32, [P, P, I32, PI32, PI32]),
         "hvd_truncate": (I32, [P, I32, I32, I32]),
         "hvd_seq_free": (I32, [P, I32]),
@@ -196,6 +198,30 @@ class KVCache:
         _check(self.lib.hvd_verify(self.model.handle, self.handle, ids.size, _ptr(ids), _ptr(ctx), _ptr(flat),
                                    _ptr(lens), _ptr(acc), _ptr(nxt), lp))
         return acc, nxt
+
+    def verify_tree(self, seq_ids, ctx_lens, trees, logits=None):
+        """trees: list of (node_tokens, node_parents) pairs (parent -1 = the
+        pending token, else an earlier node).  logits: optional torch float32
+        CUDA tensor [sum(n+1), vocab].  Returns (accepted, next_token,
+        accepted node paths as lists)."""
+        ids = _i32(seq_ids)
+        ctx = _i32(ctx_lens)
+        counts = _i32([len(t) for t, _ in trees])
+        cat = lambda xs: np.concatenate([np.asarray(x, dtype=np.int64).reshape(-1) for x in xs]) if xs else np.zeros(0)
+        toks = _i32(cat([t for t, _ in trees]))
+        pars = _i32(cat([p for _, p in trees]))
+        acc = np.zeros(ids.size, dtype=np.int32)
+        nxt = np.zeros(ids.size, dtype=np.int32)
+        paths = np.zeros((ids.size, MAX_TREE_NODES), dtype=np.int32)
+        lp = None
+        if logits is not None:
+            rows = int(counts.sum()) + ids.size
+            assert logits.is_cuda and logits.dtype.is_floating_point and logits.element_size() == 4
+            assert logits.is_contiguous() and logits.numel() >= rows * self.model.cfg.vocab
+            lp = ctypes.c_void_p(logits.data_ptr())
+        _check(self.lib.hvd_verify_tree(self.model.handle, self.handle, ids.size, _ptr(ids), _ptr(ctx), _ptr(toks),
+                                        _ptr(pars), _ptr(counts), _ptr(acc), _ptr(nxt), _ptr(paths), lp))
+        return acc, nxt, [paths[b, :acc[b]].tolist() for b in range(ids.size)]
 
     def commit(self, seq_ids, keep=None):
         ids = _i32(seq_ids)
