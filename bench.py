@@ -193,6 +193,72 @@ def leg_long_context(model, reps):
                                       sum(c["latency_us"] * 1e-6 for c in cache_legs)}
 
 
+def timed_tree(kv, b, tokens, parents, reps):
+    """Median wall time of a tree verify + commit of sequence b over reps
+    repeats, rolled back after each."""
+    base = kv.seq_info(b)[:2]
+    times, acc = [], None
+    for _ in range(reps):
+        t = time.perf_counter()
+        a, _, _ = kv.verify_tree([b], [base[0]], [(tokens, parents)])
+        kv.commit([b])
+        times.append(time.perf_counter() - t)
+        acc = int(a[0])
+        kv.truncate(b, *base)
+    return float(np.median(times)), acc
+
+
+def leg_tree_drafts(model, reps):
+    """Tree-shaped model drafts (App. A: EAGLE3 with tree depth 8 and top-k 4)
+    on the headline context (8B shape, batch 1, 2048 Zipf tokens): 32-node
+    trees with the acceptance planted along a deepest path, drawn
+    geometric(p=0.3) and capped at the depth, beside the k = 8 chain with the
+    same planted acceptance.  The plant follows the greedy continuation of
+    one-row verifies; a 33-row verify takes the MLP and LM-head GEMMs on the
+    fp16 activation alone, which can flip a row whose top-2 logits are within
+    the near-tie margin, so the accepted length may stop short of the plant."""
+    import paper_2606_01019_amd as hvd
+    from workloads import tokens as wt, trees
+    cfg = model.cfg
+    n = 2048
+    ctx = wt.zipf_context(wt.rng_for("context", 2), n, cfg.vocab)
+    kv = hvd.KVCache(model, max_seqs=1, n_pages=(n + 96) // 16 + 8)
+    kv.prefill(0, ctx)
+    greedy = greedy_batch(kv, [0], {0: 10})[0]
+    rng = wt.rng_for("draft", 6)
+    rows = []
+    for _ in range(8):
+        a_plan = wt.geometric_accept(rng, 0.3, 8)
+        par = trees.eagle_tree(rng, 32, 8, 4)
+        tok = trees.plant_path(rng, par, greedy, a_plan, cfg.vocab)
+        t_tree, a_tree = timed_tree(kv, 0, tok, par, reps)
+        d = wt.plant_chain(rng, greedy, a_plan, 8, cfg.vocab)
+        t_chain, a_chain = timed_batch(kv, [0], [d], reps)
+        rows.append({"nodes": len(par), "depth": max(len(trees.path_to(par, j)) for j in range(len(par))),
+                     "planted": a_plan, "accepted": a_tree, "latency_us": t_tree * 1e6,
+                     "chain_k8_accepted": a_chain[0], "chain_k8_latency_us": t_chain * 1e6})
+    # per-role device time of one tree verify
+    base = kv.seq_info(0)[:2]
+    kv.profile_enable(True)
+    kv.verify_tree([0], [base[0]], [(tok, par)])
+    kv.commit([0])
+    fam = {name: kv.profile_read(i)[0] for i, name in enumerate(FAMILIES)}
+    kv.profile_enable(False)
+    kv.truncate(0, *base)
+    kv.close()
+    t_tree = sum(r["latency_us"] for r in rows) * 1e-6
+    t_chain = sum(r["chain_k8_latency_us"] for r in rows) * 1e-6
+    return {"workload": f"8B shape, batch 1, context {n} Zipf(1.1), EAGLE-shaped trees (32 nodes, depth 8, top-k 4), "
+                        "acceptance planted geometric(p=0.3) along a deepest path; k = 8 chains alongside",
+            "steps": rows,
+            "tree_committed_tokens_per_s": sum(r["accepted"] + 1 for r in rows) / t_tree,
+            "chain_k8_committed_tokens_per_s": sum(r["chain_k8_accepted"] + 1 for r in rows) / t_chain,
+            "accept_mismatch_vs_plant": sum(1 for r in rows if r["accepted"] != r["planted"]),
+            "median_tree_latency_us": float(np.median([r["latency_us"] for r in rows])),
+            "median_chain_k8_latency_us": float(np.median([r["chain_k8_latency_us"] for r in rows])),
+            "kernel_families_ms": fam}
+
+
 def leg_mixed_batch(model, reps):
     """32 sequences, contexts 1024..8192 over the paged cache, half model
     chains k = 8 (geometric 0.4), half cache drafts k in 16..64 (uniform)."""
@@ -331,7 +397,7 @@ def main():
     ap.add_argument("--ctx", type=int, default=2048)
     ap.add_argument("--layers", type=int, default=0, help="override depth (0 = full 32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workloads", default="long_context,mixed_batch,multistep_32b",
+    ap.add_argument("--workloads", default="long_context,tree_drafts,mixed_batch,multistep_32b",
                     help="extra workloads reported beside the headline (comma list, '' for none)")
     ap.add_argument("--reps", type=int, default=5, help="repeats per timed step of the extra workloads")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -474,6 +540,8 @@ def main():
         t0 = time.time()
         if leg == "long_context":
             extra[leg] = leg_long_context(model, args.reps)
+        elif leg == "tree_drafts":
+            extra[leg] = leg_tree_drafts(model, args.reps)
         elif leg == "mixed_batch":
             extra[leg] = leg_mixed_batch(model, args.reps)
         elif leg == "multistep_32b":

@@ -177,3 +177,37 @@ def test_tree_argument_errors(tiny):
     assert e.value.status == hvd.HVD_ERR_RANGE
     a, n, paths = kv.verify_tree([0], [39], [([1, 2], [-1, 0])])  # the state is unchanged by the failures
     assert 0 <= int(a[0]) <= 2
+
+
+
+@pytest.fixture(scope="module")
+def mid():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_01019_amd as hvd
+    from tests.test_gpu_mid import MID as cfg
+    w = make_weights(cfg, seed=5, gain_std=0.1)
+    return cfg, oracle.OracleModel(cfg, w), hvd.Model(cfg, w)
+
+
+@pytest.mark.parametrize("n_nodes,accept", [(15, 4), (32, 6), (63, 8)])
+def test_mid_trees_grouped_query(mid, n_nodes, accept):
+    """Group-4 attention with head dim 128: 16 tree rows (64 query rows, the
+    4-wave items), 33 and 64 rows (132 and 256 query rows, the 8-wave items
+    of two row tiles per wave)."""
+    import paper_2606_01019_amd as hvd
+    cfg, om, gm = mid
+    kv = hvd.KVCache(gm, max_seqs=1, n_pages=128)
+    ctx = wt.uniform_context(wt.rng_for("context", 70 + n_nodes), 600, cfg.vocab)
+    st = oracle.prefill(om, ctx)
+    kv.prefill(0, ctx)
+    greedy, _ = oracle.greedy_decode(om, st, accept + 1)
+    rng = wt.rng_for("draft", 70 + n_nodes)
+    par = trees.eagle_tree(rng, n_nodes, 8, 4) if n_nodes < 63 else [-1] + [j // 4 for j in range(62)]
+    tok = trees.plant_path(rng, par, greedy, accept, cfg.vocab)
+    res = oracle.verify_tree(om, st, tok, par)
+    a, n, paths, L = _verify_tree(kv, [0], [st.ctx], [(tok, par)])
+    rep = Report()
+    check_tree(rep, res, L, int(a[0]), int(n[0]), paths[0])
+    print(f"{n_nodes} nodes: accepted {int(a[0])} (oracle {res.accepted}) {rep}")
