@@ -326,6 +326,7 @@ struct hvd_kv_s {
   bool use_graphs = false;
   std::map<GraphKey, hipGraphExec_t> graphs;
   int attn_min_items = kAttnMinItems;
+  int attn_max_np = kItemPages;  // most pages one attention sub-chunk stages
   int skinny_max_mt = kSkinnyMaxMT;   // row tiles above which GEMMs take the MFMA-tiled kernel
   int gemm_force[PF_LM + 1][2] = {};  // per GEMM family: {strips per workgroup, K splits} of the skinny kernel, 0 = policy
   float* gemm_part = nullptr;
@@ -455,6 +456,7 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   k->hs = new HostState(max_seqs, n_pages, kPage, c.max_pos, c.max_draft, c.vocab);
   if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
+  if (const char* e = getenv("HVD_ATTN_MAX_NP")) k->attn_max_np = std::max(2, std::min(kItemPages, atoi(e)));
   if (const char* e = getenv("HVD_GRAPHS")) k->use_graphs = atoi(e) != 0;
   if (const char* e = getenv("HVD_SKINNY_MAX_MT")) k->skinny_max_mt = std::max(1, std::min(64, atoi(e)));
   // tuning override of the skinny GEMM shape: "qkv=2:1,o=1:1" (family=strips:splits)
@@ -866,7 +868,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.tree_mask = d_mask;
       {
         ProfScope ps(k, PF_ATTN, kv_bytes);
-        HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, rpi, s));
+        HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, rpi, k->attn_max_np, s));
       }
       if (!plan.heads.empty()) {
         CombineArgs cb{};

@@ -462,9 +462,16 @@ static hipError_t launch_attn_dh(const AttnArgs& a, int n_items, int np, hipStre
 // 4 waves of two for head dim 64, whose page has too few 16-byte units for
 // 8 waves) or 256 (8 waves of two tiles; head dim 128, sub-chunks of at most
 // 8 pages so the staging registers fit two waves per SIMD)
-hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, hipStream_t s) {
+hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, int max_np, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  const int np = attn_pages_per_sub(chunk);
+  // Sub-chunks of 2 pages for 64-row items, 4 otherwise (measured at
+  // context 16384: smaller sub-chunks need fewer staging registers, so more
+  // workgroups share a CU and hide each other's load latency; the next
+  // sub-chunk's loads overlap the current one's MFMAs anyway)
+  int np = attn_pages_per_sub(chunk);
+  const int pref = rows_per_item == 64 ? 2 : 4;
+  const int cap = max_np < pref ? max_np : pref;
+  while (np > 2 && np > cap) np /= 2;
   switch (rows_per_item) {
     case 64:
       if (a.dh == 128) return launch_attn_dh<128, 4, 1>(a, n_items, np, s);

@@ -195,7 +195,8 @@ hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, i
                              hipStream_t s);
 // chunk: the plan's KV chunk length (picks the pages staged per sub-chunk);
 // rows_per_item: 64, 128 or 256 (256 for head_dim 128 only)
-hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, hipStream_t s);
+// max_np caps the pages staged per sub-chunk (longer chunks loop over sub-chunks)
+hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, int max_np, hipStream_t s);
 hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);

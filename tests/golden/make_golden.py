@@ -11,7 +11,7 @@ The 8B- and 32B-shaped references use the oracle in float32 (the float64
 path of the same code would need twice the memory and time); a reduced-depth
 pin (tests/test_oracle_precision.py) bounds the float32/float64 difference.
 
-Usage: python tests/golden/make_golden.py cfg2 [cfg3 cfg4 cfg5]
+Usage: python tests/golden/make_golden.py cfg2 [cfg3 cfg4 cfg5 tree2]
 """
 
 import json
@@ -191,8 +191,55 @@ def case_cfg5():
             "seqs": out, "oracle_dtype": "float32"}
 
 
+def record_tree(res, ids, top_n=TOP):
+    lg = res.logits
+    part = np.partition(lg, -2, axis=-1)
+    top = np.argsort(-lg, axis=-1)[:, :top_n]
+    return {
+        "tokens": [int(t) for t in res.tokens],
+        "parents": [int(p) for p in res.parents],
+        "path": [int(j) for j in res.path],
+        "next": int(res.next_token),
+        "argmax": [int(t) for t in res.argmax],
+        "margin": [float(x) for x in (part[:, -1] - part[:, -2])],
+        "sample_logits": [[float(x) for x in row] for row in lg[:, ids]],
+        "top_ids": [[int(t) for t in row] for row in top],
+        "top_logits": [[float(lg[r, t]) for t in top[r]] for r in range(lg.shape[0])],
+    }
+
+
+def case_tree2():
+    """Token trees on the workload-2 context: EAGLE-shaped trees (32 nodes,
+    depth 8, top-k 4) with 2, 5 and 8 tokens planted along a deepest path,
+    and a 63-node 4-ary tree with 3 planted."""
+    from workloads import trees
+    cfg = SHAPE_8B
+    log("tree2: weights")
+    m = fp32_model(cfg)
+    ctx = wt.zipf_context(wt.rng_for("context", 2), 2048, cfg.vocab)
+    log("tree2: prefill")
+    st = oracle.prefill(m, ctx)
+    ids = sample_ids(cfg.vocab)
+    g = greedy(m, st, 9)
+    rng = wt.rng_for("draft", 22)
+    shapes = [(trees.eagle_tree(rng, 32, 8, 4), 2), (trees.eagle_tree(rng, 32, 8, 4), 5),
+              (trees.eagle_tree(rng, 32, 8, 4), 8), ([-1] + [j // 4 for j in range(62)], 3)]
+    steps = []
+    for par, a in shapes:
+        tok = trees.plant_path(rng, par, g, a, cfg.vocab)
+        res = oracle.verify_tree(m, st, tok, par)
+        log(f"tree2: {len(par)} nodes planted={a} accepted={res.accepted}")
+        steps.append(record_tree(res, ids))
+    return {"config": "8B shape, batch 1, context 2048 Zipf(1.1) (workload 2), token trees: three EAGLE-shaped "
+                      "(32 nodes, depth 8, top-k 4) with 2, 5, 8 tokens planted along a deepest path from the "
+                      "oracle's greedy continuation, and a 63-node 4-ary tree with 3 planted",
+            "model": cfg.as_dict(), "context_seed": ["context", 2], "context_len": 2048,
+            "context_kind": "zipf", "sample_ids": [int(i) for i in ids], "steps": steps,
+            "oracle_dtype": "float32"}
+
+
 def main():
-    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3, "cfg4": case_cfg4, "cfg5": case_cfg5}
+    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3, "cfg4": case_cfg4, "cfg5": case_cfg5, "tree2": case_tree2}
     for name in sys.argv[1:]:
         t0 = time.time()
         out = cases[name]()

@@ -211,3 +211,43 @@ def test_mid_trees_grouped_query(mid, n_nodes, accept):
     rep = Report()
     check_tree(rep, res, L, int(a[0]), int(n[0]), paths[0])
     print(f"{n_nodes} nodes: accepted {int(a[0])} (oracle {res.accepted}) {rep}")
+
+
+def test_8b_trees_against_oracle_record(model8b):
+    """Full 8B shape at the workload-2 context: four trees (tests/golden/
+    tree2.json, written by tests/golden/make_golden.py from the oracle alone),
+    compared at the sampled and top logits, per-row argmax and the accepted
+    path."""
+    import torch
+    import paper_2606_01019_amd as hvd
+    from tests.conftest import load_golden
+    gold = load_golden("tree2.json")
+    V = gold["model"]["vocab"]
+    kv = hvd.KVCache(model8b, max_seqs=1, n_pages=(gold["context_len"] + 96) // 16 + 8)
+    ctx = wt.zipf_context(wt.rng_for(*gold["context_seed"]), gold["context_len"], V)
+    kv.prefill(0, ctx)
+    c0, p0 = len(ctx) - 1, int(ctx[-1])
+    ids = np.asarray(gold["sample_ids"])
+    rep = Report()
+    for st in gold["steps"]:
+        tok, par = st["tokens"], st["parents"]
+        lg = torch.empty((len(tok) + 1, V), dtype=torch.float32, device="cuda")
+        a, n, paths = kv.verify_tree([0], [c0], [(tok, par)], logits=lg)
+        kv.truncate(0, c0, p0)
+        L = lg.cpu().numpy()
+        err = float(np.abs(L[:, ids] - np.asarray(st["sample_logits"])).max())
+        top = np.asarray(st["top_ids"])
+        err = max(err, max(float(np.abs(L[r, top[r]] - np.asarray(st["top_logits"][r])).max())
+                           for r in range(L.shape[0])))
+        rep.max_err = max(rep.max_err, err)
+        assert err <= LOGIT_TOL, f"logit error {err:.3e}"
+        tie = np.asarray(st["margin"]) < TIE_MARGIN
+        g_gpu = L.argmax(1)
+        rep.rows += L.shape[0]
+        rep.excused += int(tie.sum())
+        assert not ((g_gpu != np.asarray(st["argmax"])) & ~tie).any()
+        assert paths[0] == oracle.tree_accept(g_gpu, np.asarray(tok), np.asarray(par))
+        on_path = [0] + [j + 1 for j in st["path"]]
+        if not tie[on_path].any():
+            assert paths[0] == st["path"] and int(n[0]) == st["next"]
+        print(f"{len(tok)} nodes: path {paths[0]} (oracle {st['path']}) {rep}", flush=True)
