@@ -261,6 +261,71 @@ def leg_tree_drafts(model, reps):
             "kernel_families_ms": fam}
 
 
+def leg_hvd_loop(model, reps):
+    """Hybrid Verified Decoding (Alg. 1) around the verify step on the 8B
+    shape: an agentic-style 2048-token prompt (64-token segments copied from
+    16 bases with 20% mutation), 256 new tokens; the payoff MLP is trained on
+    the replay (App. B) of the greedy trace of another such prompt.  Reports
+    verification cycles per 1K tokens and tokens/s for plain greedy steps,
+    for verifying every cache draft (the suffix-cache baseline) and for the
+    payoff-guided selection (tau = 6; the model drafter proposes nothing),
+    for a fresh request and for a retried one (an identical earlier request
+    in the cache warmup, Alg. 1).  Random weights give the target no reason
+    to repeat its prompt, so a fresh request finds few cache drafts."""
+    import paper_2606_01019_amd as hvd
+    from paper_2606_01019_amd import hvd_loop as hl
+    from workloads import tokens as wt
+    cfg = model.cfg
+    n, n_new = 2048, 256
+    kv = hvd.KVCache(model, max_seqs=2, n_pages=2 * ((n + n_new + 160) // 16 + 8))
+
+    def greedy(sid, prompt, m):
+        kv.prefill(sid, prompt)
+        out = []
+        t = time.perf_counter()
+        for _ in range(m):
+            c, _, _ = kv.seq_info(sid)
+            _, nx = kv.verify([sid], [c], [np.zeros(0, np.int32)])
+            kv.commit([sid])
+            out.append(int(nx[0]))
+        dt = time.perf_counter() - t
+        kv.seq_free(sid)
+        return out, dt
+
+    # predictor: App. B replay of another request's greedy trace, once with
+    # no warmup (fresh request) and once with an identical earlier request
+    # in the cache (a retried request), so it sees short and long payoffs
+    train_prompt = wt.segment_context(wt.rng_for("context", 7, 1), n, cfg.vocab)
+    trace, _ = greedy(1, train_prompt, n_new)
+    full = list(train_prompt) + trace
+    X1, y1 = hl.replay_labels(full, n)
+    X2, y2 = hl.replay_labels(full, n, cache_streams=[full])
+    X, y = np.concatenate([X1, X2]), np.concatenate([y1, y2])
+    g = hl.PayoffMLP()
+    g.fit(X, y)
+    prompt = wt.segment_context(wt.rng_for("context", 7, 2), n, cfg.vocab)
+    ref, t_greedy = greedy(1, prompt, n_new)
+    res = {"greedy": {"cycles_per_1k": 1000.0, "tokens_per_s": n_new / t_greedy}}
+    always = lambda phi: np.full(len(phi), np.inf)
+    for name, pred, warm in (("fresh_suffix_cache_always", always, []), ("fresh_hvd", g, []),
+                             ("retry_suffix_cache_always", always, [list(prompt) + ref]),
+                             ("retry_hvd", g, [list(prompt) + ref])):
+        dec = hl.HybridVerifiedDecoder(kv, 0, pred, warmup_streams=warm)
+        out, st = dec.generate(prompt, n_new)
+        kv.seq_free(0)
+        res[name] = {"cycles_per_1k": st.cycles_per_1k, "tokens_per_s": st.generated / st.decode_s,
+                     "cache_verifies": st.cache_steps,
+                     "mean_cache_accepted": float(np.mean(st.cache_accepted)) if st.cache_accepted else 0.0,
+                     "tokens_equal_to_greedy": int(next((i for i, (a, b) in enumerate(zip(out, ref)) if a != b),
+                                                        len(ref)))}
+    kv.close()
+    res["workload"] = (f"8B shape, batch 1, agentic-style prompt of {n} tokens, {n_new} new tokens; fresh: empty "
+                       f"cache warmup; retry: the cache holds an identical earlier request; payoff MLP trained on "
+                       f"{len(y)} replayed cache drafts of another request")
+    res["retry_speedup_vs_greedy"] = res["retry_hvd"]["tokens_per_s"] / res["greedy"]["tokens_per_s"]
+    return res
+
+
 def leg_mixed_batch(model, reps):
     """32 sequences, contexts 1024..8192 over the paged cache, half model
     chains k = 8 (geometric 0.4), half cache drafts k in 16..64 (uniform)."""
@@ -441,7 +506,7 @@ def main():
     ap.add_argument("--ctx", type=int, default=2048)
     ap.add_argument("--layers", type=int, default=0, help="override depth (0 = full 32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workloads", default="long_context,tree_drafts,mixed_batch,multistep_32b",
+    ap.add_argument("--workloads", default="long_context,tree_drafts,hvd_loop,mixed_batch,multistep_32b",
                     help="extra workloads reported beside the headline (comma list, '' for none)")
     ap.add_argument("--reps", type=int, default=5, help="repeats per timed step of the extra workloads")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -573,6 +638,8 @@ def main():
             extra[leg] = leg_long_context(model, args.reps)
         elif leg == "tree_drafts":
             extra[leg] = leg_tree_drafts(model, args.reps)
+        elif leg == "hvd_loop":
+            extra[leg] = leg_hvd_loop(model, args.reps)
         elif leg == "mixed_batch":
             extra[leg] = leg_mixed_batch(model, args.reps)
         elif leg == "multistep_32b":
