@@ -326,6 +326,74 @@ def leg_hvd_loop(model, reps):
     return res
 
 
+def leg_async_loop(model, reps):
+    """Device-resident verify loop (hvd_async_*) beside the host-driven loop
+    (hvd_verify + hvd_commit per step) on the headline shape: 8B, batch 1,
+    context 2048 Zipf tokens, fixed draft lengths k.  Both draft from the
+    same token stream (the greedy continuation with tokens replaced at rate
+    0.3: geometric acceptance) at the current position, the host loop on the
+    host, the device loop with the library's copy drafter inside each
+    step's graph; the device loop is enqueued whole and waited for once."""
+    import torch
+    import paper_2606_01019_amd as hvd
+    from workloads import tokens as wt
+    cfg = model.cfg
+    n, steps, warm = 2048, 48, 4
+    ks = (4, 8, 16)
+    kv = hvd.KVCache(model, max_seqs=1, n_pages=(n + (steps + warm) * (max(ks) + 1) + 64) // 16 + 8)
+    kv.prefill(0, wt.zipf_context(wt.rng_for("context", 2), n, cfg.vocab))
+    c0, p0, _ = kv.seq_info(0)
+    greedy = []
+    for _ in range((steps + warm) * (max(ks) + 1) + 1):
+        c, _, _ = kv.seq_info(0)
+        _, nx = kv.verify([0], [c], [np.zeros(0, np.int32)])
+        kv.commit([0])
+        greedy.append(int(nx[0]))
+    kv.truncate(0, c0, p0)
+    ref = wt.corrupt_stream(wt.rng_for("draft", 9), greedy, 0.3, cfg.vocab)
+    ref_t = torch.tensor(ref[None, :], device="cuda")
+    res = {}
+    for k in ks:
+        def draft_at(c):
+            j = np.arange(c + 1, c + 1 + k) - (c0 + 1)
+            return np.where(j < len(ref), ref[np.minimum(j, len(ref) - 1)], -1).astype(np.int32)
+
+        # host-driven loop
+        acc_h = []
+        for i in range(warm + steps):
+            if i == warm:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+            c, _, _ = kv.seq_info(0)
+            a, _ = kv.verify([0], [c], [draft_at(c)])
+            kv.commit([0])
+            if i >= warm:
+                acc_h.append(int(a[0]))
+        torch.cuda.synchronize()
+        t_host = time.perf_counter() - t0
+        kv.truncate(0, c0, p0)
+        # device-resident loop: the same steps enqueued at once
+        loop = kv.async_loop([0], [c0], [k], warm + steps, ref=ref_t, ref_start=[c0 + 1])
+        loop.step(warm)
+        kv.stream.synchronize()
+        t0 = time.perf_counter()
+        loop.step(steps)
+        loop.end()
+        t_dev = time.perf_counter() - t0
+        hist = loop.history.cpu().numpy()[warm:warm + steps, 0]
+        acc_d = [int(x) for x in hist[:, 0]]
+        kv.truncate(0, c0, p0)
+        same = next((i for i, (x, y) in enumerate(zip(acc_h, acc_d)) if x != y), steps)
+        res[f"k{k}"] = {"host_loop_ms_per_step": t_host / steps * 1e3, "device_loop_ms_per_step": t_dev / steps * 1e3,
+                        "host_loop_tokens_per_s": sum(a + 1 for a in acc_h) / t_host,
+                        "device_loop_tokens_per_s": sum(a + 1 for a in acc_d) / t_dev,
+                        "mean_accepted": float(np.mean(acc_d)), "steps_equal_to_host_loop": same}
+    kv.close()
+    res["workload"] = (f"8B shape, batch 1, context {n} Zipf(1.1) tokens, {steps} timed steps (after {warm}) per k, "
+                       f"drafts copied from the greedy continuation with tokens replaced at rate 0.3")
+    return res
+
+
 def leg_mixed_batch(model, reps):
     """32 sequences, contexts 1024..8192 over the paged cache, half model
     chains k = 8 (geometric 0.4), half cache drafts k in 16..64 (uniform)."""
@@ -506,7 +574,7 @@ def main():
     ap.add_argument("--ctx", type=int, default=2048)
     ap.add_argument("--layers", type=int, default=0, help="override depth (0 = full 32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workloads", default="long_context,tree_drafts,hvd_loop,mixed_batch,multistep_32b",
+    ap.add_argument("--workloads", default="long_context,tree_drafts,hvd_loop,async_loop,mixed_batch,multistep_32b",
                     help="extra workloads reported beside the headline (comma list, '' for none)")
     ap.add_argument("--reps", type=int, default=5, help="repeats per timed step of the extra workloads")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -640,6 +708,8 @@ def main():
             extra[leg] = leg_tree_drafts(model, args.reps)
         elif leg == "hvd_loop":
             extra[leg] = leg_hvd_loop(model, args.reps)
+        elif leg == "async_loop":
+            extra[leg] = leg_async_loop(model, args.reps)
         elif leg == "mixed_batch":
             extra[leg] = leg_mixed_batch(model, args.reps)
         elif leg == "multistep_32b":

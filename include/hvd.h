@@ -163,6 +163,49 @@ hvd_status hvd_verify_tree(hvd_model m, hvd_kv kv, int32_t batch, const int32_t*
 hvd_status hvd_commit(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_ids,
                       const int32_t* keep_lens);
 
+/* Device-resident verify loop: Alg. 1's Verify followed by the commit of
+ * the whole accepted block (append z_t with keep = a_t), repeated on the GPU
+ * with the drafts read from device memory and no host round trip per step.
+ * Each step is one replay of a HIP graph captured here, so a drafter running
+ * on the GPU (writing `drafts` on the same stream between steps) can feed
+ * verification directly, and the host only enqueues.
+ *
+ * hvd_async_begin opens a loop of at most max_steps >= 1 steps over `batch`
+ * sequences with fixed draft lengths draft_lens[b] in [0, max_draft]
+ * (ctx_lens as in hvd_verify).  It reserves the pages of the longest
+ * possible outcome, ctx_b + max_steps * (k_b + 1) + 1 positions
+ * (HVD_ERR_OOM if the pool cannot; HVD_ERR_RANGE past the rotary table), and
+ * while the loop is open every other call on these sequences is
+ * HVD_ERR_STATE.  Caller-owned DEVICE buffers (int32, kept alive until
+ * hvd_async_end):
+ *   drafts  [sum k_b]   draft tokens of step s, packed in batch order; read
+ *                       by every step (may be NULL when every k_b = 0).  A
+ *                       token outside [0, vocab) is never accepted.
+ *   state   [2 batch + 1]  ctx[b], pending token[b], steps done; written
+ *                       here, then advanced by every step on the device.
+ *   history [max_steps][batch][2]  (accepted a_b, next token) of each step.
+ * Copy drafter (optional, the cache drafts of section 3.2 in their simplest
+ * device form): with ref_tokens (DEVICE, [batch][ref_len]) non-NULL, each
+ * step first fills sequence b's drafts with the stream tokens at positions
+ * ctx_b + 1 .. ctx_b + k_b, where ref_tokens[b][j] stands at position
+ * ref_start[b] + j (ref_start: host, [batch]) and positions outside the
+ * stream give -1; the drafts buffer then receives them too.
+ * hvd_async_step enqueues n_steps >= 0 steps and returns without waiting
+ * (HVD_ERR_RANGE past max_steps in total).  hvd_async_end waits for them,
+ * takes ctx and the pending token from `state` into the library's sequence
+ * state, releases the pages past each new end and frees the loop (also on
+ * error: then the sequences keep their state from before the loop).
+ * steps_done (nullable) receives the number of steps run.  The results
+ * equal those of hvd_verify + hvd_commit with the same drafts, up to the
+ * rounding of attention sums split at other chunk boundaries. */
+typedef struct hvd_async_s* hvd_async;
+hvd_status hvd_async_begin(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_ids,
+                           const int32_t* ctx_lens, const int32_t* draft_lens, int32_t max_steps,
+                           int32_t* drafts, int32_t* state, int32_t* history, const int32_t* ref_tokens,
+                           int32_t ref_len, const int32_t* ref_start, hvd_async* out);
+hvd_status hvd_async_step(hvd_async loop, int32_t n_steps);
+hvd_status hvd_async_end(hvd_async loop, int32_t* steps_done);
+
 /* Roll sequence seq_id back to an earlier committed length: 0 <= new_ctx_len
  * <= ctx_len, pending_token is the committed token at position new_ctx_len.
  * Cancels an uncommitted verify. */

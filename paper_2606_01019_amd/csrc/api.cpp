@@ -568,6 +568,8 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
     it.g = u.g; it.c = c; it.nch = nch; it.rg = u.rg; it.part = part;
     it.p_begin = c * chunk;
     it.p_end = std::min(s.ctx + s.k + 1, (c + 1) * chunk);
+    it.pad1 = u.b;                // for a device-side re-plan at another ctx:
+    it.pad2 = u.keys - s.ctx - 1;  // sequence, last row index of the unit
     // pages of the first kAttnChunk positions; entries past the chunk's end
     // repeat its first page (the kernel loads them unconditionally)
     const std::vector<int32_t>& pg = hs.seq(s.slot).pages;
@@ -628,8 +630,26 @@ struct TreeRows {
   std::vector<int32_t> parent;
 };
 
+// A device-resident loop's step, captured instead of run: the metadata
+// (planned for the longest context the loop reaches) goes once to a device
+// block of the loop's own, and the captured launches start with the
+// device-side re-plan and end with the on-device commit.
+struct AsyncCap {
+  int32_t* drafts = nullptr;
+  int32_t* state = nullptr;
+  int32_t* hist = nullptr;
+  int hist_cap = 0;
+  const int32_t* ref = nullptr;
+  int ref_len = 0;
+  std::vector<int32_t> ref_start;  // [B]
+  std::vector<int32_t> page_off;   // [B + 1]
+  std::vector<int32_t> pages;      // reserved pages, concatenated
+  int32_t* meta = nullptr;         // out: device metadata block (hipMalloc)
+  hipGraphExec_t graph = nullptr;  // out
+};
+
 hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<RowMeta> rows, bool lm_head,
-                   float* logits, const TreeRows* tree = nullptr) {
+                   float* logits, const TreeRows* tree = nullptr, AsyncCap* acap = nullptr) {
   // each row's pool slot: page * kPage + offset (the QKV epilogue writes K/V there)
   for (RowMeta& r : rows) r.kvs = k->hs->seq(r.slot).pages[(size_t)(r.kvs / kPage)] * kPage + r.kvs % kPage;
   hvd_model_s* m = k->m;
@@ -668,8 +688,13 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     plan.heads.resize(n_heads, none);
   }
 
-  // pack metadata: header | rows | seqs | items | heads | updates
-  int32_t* h = k->meta_host;
+  // pack metadata: header | rows | seqs | items | heads | updates (a
+  // device-resident loop adds its static copies after them)
+  std::vector<int32_t> ameta;
+  if (acap)
+    ameta.resize(16 + 4 * (size_t)M + sizeof(SeqMeta) / 4 * 2 * (size_t)B + 64 * (n_items + n_heads) +
+                 3 * (size_t)M + 3 * last.size() + M + 2 * B + 1 + acap->pages.size() + 80);
+  int32_t* h = acap ? ameta.data() : k->meta_host;
   size_t off = 0;
   auto put = [&](const void* src, size_t ints) {
     if (ints) std::memcpy(h + off, src, ints * 4);
@@ -679,7 +704,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   };
   const size_t need_ints = 16 + 4 * (size_t)M + sizeof(SeqMeta) / 4 * (size_t)B + 32 * (n_items + n_heads) +
                            3 * (size_t)M + 3 * last.size() + 40;
-  if (need_ints > k->meta_ints) {
+  if (!acap && need_ints > k->meta_ints) {
     k->hs->take_updates();
     return set_err(HVD_ERR_OOM, "metadata buffer too small");
   }
@@ -704,19 +729,70 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     upd.push_back(kv.second);
   }
   const size_t o_upd = put(upd.data(), upd.size());
-  HIP_TRY(hipMemcpyAsync(k->meta_dev, h, off * 4, hipMemcpyHostToDevice, s));
-  const RowMeta* d_rows = (const RowMeta*)(k->meta_dev + o_rows);
-  const SeqMeta* d_seqs = (const SeqMeta*)(k->meta_dev + o_seqs);
-  const AttnItem* d_items = (const AttnItem*)(k->meta_dev + o_items);
-  const AttnItem* d_heads = (const AttnItem*)(k->meta_dev + o_heads);
-  const uint64_t* d_mask = tree ? (const uint64_t*)(k->meta_dev + o_mask) : nullptr;
-  const int32_t* d_parent = tree ? k->meta_dev + o_parent : nullptr;
+  size_t o_sitems = 0, o_sheads = 0, o_sseqs = 0, o_rowseq = 0, o_pgoff = 0, o_pages = 0, o_rstart = 0;
+  if (acap) {
+    o_sitems = put(plan.items.data(), sizeof(AttnItem) / 4 * n_items);
+    o_sheads = put(plan.heads.data(), sizeof(AttnItem) / 4 * n_heads);
+    o_sseqs = put(seqs.data(), sizeof(SeqMeta) / 4 * (size_t)B);
+    std::vector<int32_t> row_seq(M);
+    for (int b = 0; b < B; ++b)
+      for (int i = 0; i <= seqs[b].k; ++i) row_seq[seqs[b].cu + i] = b;
+    o_rowseq = put(row_seq.data(), M);
+    o_pgoff = put(acap->page_off.data(), B + 1);
+    o_pages = put(acap->pages.data(), acap->pages.size());
+    o_rstart = put(acap->ref_start.data(), B);
+    if (off > ameta.size()) return set_err(HVD_ERR_OOM, "loop metadata block too small");
+    if (hipMalloc((void**)&acap->meta, off * 4) != hipSuccess) {
+      acap->meta = nullptr;
+      return set_err(HVD_ERR_OOM, "hipMalloc of the loop metadata failed");
+    }
+  }
+  int32_t* const meta_dev = acap ? acap->meta : k->meta_dev;
+  HIP_TRY(hipMemcpyAsync(meta_dev, h, off * 4, hipMemcpyHostToDevice, s));
+  if (acap) {
+    // the page-table updates are applied once, here; the replays carry none
+    // (replaying them could undo later updates of other sequences)
+    static const int32_t zero = 0;
+    HIP_TRY(launch_pt_update(meta_dev + o_upd, meta_dev, k->pt, k->pt_stride, s));
+    HIP_TRY(hipMemcpyAsync(meta_dev, &zero, 4, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));  // the staging vector goes out of scope
+  }
+  const RowMeta* d_rows = (const RowMeta*)(meta_dev + o_rows);
+  const SeqMeta* d_seqs = (const SeqMeta*)(meta_dev + o_seqs);
+  const AttnItem* d_items = (const AttnItem*)(meta_dev + o_items);
+  const AttnItem* d_heads = (const AttnItem*)(meta_dev + o_heads);
+  const uint64_t* d_mask = tree ? (const uint64_t*)(meta_dev + o_mask) : nullptr;
+  const int32_t* d_parent = tree ? meta_dev + o_parent : nullptr;
 
   // ---------------------------------------------------------------- launches
   // Everything below only enqueues kernels whose arguments are fixed by
   // the GraphKey fields: captured once per shape into
   // a HIP graph and replayed (eager while profiling or with graphs off).
   auto launch_all = [&]() -> hvd_status {
+  if (acap) {
+    AsyncPlanArgs p{};
+    p.state = acap->state;
+    p.drafts = acap->drafts;
+    p.ref = acap->ref;
+    p.ref_len = acap->ref_len;
+    p.ref_start = meta_dev + o_rstart;
+    p.seq_static = (const SeqMeta*)(meta_dev + o_sseqs);
+    p.page_off = meta_dev + o_pgoff;
+    p.pages = meta_dev + o_pages;
+    p.row_seq = meta_dev + o_rowseq;
+    p.rows = (RowMeta*)(meta_dev + o_rows);
+    p.seqs = (SeqMeta*)(meta_dev + o_seqs);
+    p.items_static = (const AttnItem*)(meta_dev + o_sitems);
+    p.items = (AttnItem*)(meta_dev + o_items);
+    p.n_items = (int)n_items;
+    p.heads_static = (const AttnItem*)(meta_dev + o_sheads);
+    p.heads = (AttnItem*)(meta_dev + o_heads);
+    p.n_heads = (int)n_heads;
+    p.chunk = plan.chunk;
+    p.M = M;
+    p.B = B;
+    HIP_TRY(launch_async_plan(p, s));
+  }
   {
     EmbedArgs e{};
     e.E = m->embed;
@@ -730,10 +806,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     e.Nlo = k->Nlo;
     e.ss_out = k->ss;
     e.MTtot = MT;
-    e.upd = k->meta_dev + o_upd;
-    e.n_upd = k->meta_dev;  // header[0]
+    e.upd = meta_dev + o_upd;
+    e.n_upd = meta_dev;  // header[0]
     e.pt = k->pt;
     e.pt_stride = k->pt_stride;
+    e.V = c.vocab;
     ProfScope ps(k, PF_OTHER, 0.0);
     HIP_TRY(launch_embed(e, s));
   }
@@ -955,6 +1032,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     ac.counter = k->counter;
     ac.tree_parent = d_parent;
     ac.path = k->out + 2 * B;
+    if (acap) {
+      ac.astate = acap->state;
+      ac.hist = acap->hist;
+      ac.hist_cap = acap->hist_cap;
+    }
     {
       ProfScope ps(k, PF_OTHER, 0.0);
       HIP_TRY(launch_accept(ac, s));
@@ -979,6 +1061,28 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   return HVD_OK;
   };  // launch_all
 
+  if (acap) {
+    // captured once; the loop replays it (no profiling events inside)
+    const bool prof = k->prof;
+    k->prof = false;
+    hipGraph_t g = nullptr;
+    HIP_TRY(hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
+    const hvd_status st = launch_all();
+    const hipError_t ec = hipStreamEndCapture(s, &g);
+    k->prof = prof;
+    if (st != HVD_OK) {
+      if (g) (void)hipGraphDestroy(g);
+      return st;
+    }
+    if (ec != hipSuccess) return set_err(HVD_ERR_DEVICE, std::string("graph capture: ") + hipGetErrorString(ec));
+    const hipError_t ei = hipGraphInstantiate(&acap->graph, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (ei != hipSuccess) {
+      acap->graph = nullptr;
+      return set_err(HVD_ERR_DEVICE, std::string("graph instantiate: ") + hipGetErrorString(ei));
+    }
+    return HVD_OK;
+  }
   if (k->prof || !k->use_graphs) {
     if (hvd_status st = launch_all(); st != HVD_OK) return st;
   } else {
@@ -1146,6 +1250,125 @@ extern "C" hvd_status hvd_verify_tree(hvd_model m, hvd_kv k, int32_t batch, cons
   }
   k->hs->finish_verify(batch, seq_ids, path_tokens.data(), acc.data(), accepted_len, next_token);
   return HVD_OK;
+}
+
+// ------------------------------------------------------------ device-resident loop
+
+struct hvd_async_s {
+  hvd_kv_s* k = nullptr;
+  std::vector<int32_t> ids;
+  int32_t* state = nullptr;  // caller's: ctx[B], pending[B], steps done
+  int max_steps = 0, launched = 0;
+  int32_t* meta = nullptr;
+  hipGraphExec_t graph = nullptr;
+};
+
+extern "C" hvd_status hvd_async_begin(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids,
+                                      const int32_t* ctx_lens, const int32_t* draft_lens, int32_t max_steps,
+                                      int32_t* drafts, int32_t* state, int32_t* history, const int32_t* ref_tokens,
+                                      int32_t ref_len, const int32_t* ref_start, hvd_async* out) {
+  if (!m || !k) return set_err(HVD_ERR_ARG, "null handle");
+  if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
+  if (!out || !state || !history) return set_err(HVD_ERR_ARG, "null state, history or out");
+  if (ref_tokens && (ref_len < 1 || !ref_start)) return set_err(HVD_ERR_ARG, "copy drafter needs ref_len >= 1 and ref_start");
+  if (hvd_status st = from_host(k->hs->begin_async(batch, seq_ids, ctx_lens, draft_lens, max_steps), k); st != HVD_OK)
+    return st;
+  std::vector<int32_t> ctx0(batch), pend0(batch);
+  int64_t sum_k = 0;
+  for (int b = 0; b < batch; ++b) {
+    ctx0[b] = k->hs->seq(seq_ids[b]).ctx;
+    pend0[b] = k->hs->seq(seq_ids[b]).pending;
+    sum_k += draft_lens[b];
+  }
+  auto undo = [&](hvd_status st) {
+    k->hs->end_async(batch, seq_ids, ctx0.data(), pend0.data());
+    return st;
+  };
+  if (sum_k > 0 && !drafts) return undo(set_err(HVD_ERR_ARG, "null drafts buffer"));
+  // the step is planned at the longest context the loop reaches (every
+  // draft accepted until the last step); rows are rebuilt on the device
+  AsyncCap cap;
+  cap.drafts = drafts;
+  cap.state = state;
+  cap.hist = history;
+  cap.hist_cap = max_steps;
+  cap.ref = ref_tokens;
+  cap.ref_len = ref_tokens ? ref_len : 0;
+  std::vector<SeqMeta> seqs(batch);
+  std::vector<RowMeta> rows;
+  cap.page_off.push_back(0);
+  for (int b = 0; b < batch; ++b) {
+    const SeqSlot& sl = k->hs->seq(seq_ids[b]);
+    const int kk = draft_lens[b];
+    const int ctx_max = sl.ctx + (max_steps - 1) * (kk + 1);
+    seqs[b] = {seq_ids[b], ctx_max, kk, (int32_t)rows.size()};
+    for (int i = 0; i <= kk; ++i) rows.push_back({0, seq_ids[b], ctx_max + i, ctx_max + i});
+    cap.pages.insert(cap.pages.end(), sl.pages.begin(), sl.pages.end());
+    cap.page_off.push_back((int32_t)cap.pages.size());
+    cap.ref_start.push_back(ref_tokens ? ref_start[b] : 0);
+  }
+  std::vector<int32_t> st0(2 * (size_t)batch + 1, 0);
+  for (int b = 0; b < batch; ++b) {
+    st0[b] = ctx0[b];
+    st0[batch + b] = pend0[b];
+  }
+  if (hipMemcpyAsync(state, st0.data(), st0.size() * 4, hipMemcpyHostToDevice, k->stream) != hipSuccess ||
+      hipStreamSynchronize(k->stream) != hipSuccess)
+    return undo(set_err(HVD_ERR_DEVICE, "loop state upload failed"));
+  if (hvd_status st = forward(k, seqs, rows, true, nullptr, nullptr, &cap); st != HVD_OK) {
+    if (cap.graph) (void)hipGraphExecDestroy(cap.graph);
+    if (cap.meta) (void)hipFree(cap.meta);
+    return undo(st);
+  }
+  auto* a = new hvd_async_s();
+  a->k = k;
+  a->ids.assign(seq_ids, seq_ids + batch);
+  a->state = state;
+  a->max_steps = max_steps;
+  a->meta = cap.meta;
+  a->graph = cap.graph;
+  *out = a;
+  return HVD_OK;
+}
+
+extern "C" hvd_status hvd_async_step(hvd_async a, int32_t n_steps) {
+  if (!a) return set_err(HVD_ERR_ARG, "null handle");
+  if (n_steps < 0) return set_err(HVD_ERR_ARG, "n_steps must be >= 0");
+  if ((int64_t)a->launched + n_steps > a->max_steps) return set_err(HVD_ERR_RANGE, "more steps than the loop reserved");
+  for (int i = 0; i < n_steps; ++i) {
+    HIP_TRY(hipGraphLaunch(a->graph, a->k->stream));
+    ++a->launched;
+  }
+  return HVD_OK;
+}
+
+extern "C" hvd_status hvd_async_end(hvd_async a, int32_t* steps_done) {
+  if (!a) return set_err(HVD_ERR_ARG, "null handle");
+  hvd_kv_s* k = a->k;
+  const int B = (int)a->ids.size();
+  std::vector<int32_t> st(2 * (size_t)B + 1);
+  hvd_status ret = HVD_OK;
+  if (hipMemcpyAsync(st.data(), a->state, st.size() * 4, hipMemcpyDeviceToHost, k->stream) != hipSuccess ||
+      hipStreamSynchronize(k->stream) != hipSuccess) {
+    ret = set_err(HVD_ERR_DEVICE, "loop state readback failed");
+  } else if (st[2 * B] != a->launched) {
+    ret = set_err(HVD_ERR_STATE, "the device step count disagrees with the steps launched");
+  }
+  if (ret == HVD_OK) {
+    k->hs->end_async(B, a->ids.data(), st.data(), st.data() + B);
+  } else {  // unknown device state: the sequences leave the loop at their start
+    std::vector<int32_t> c0(B), p0(B);
+    for (int b = 0; b < B; ++b) {
+      c0[b] = k->hs->seq(a->ids[b]).ctx;
+      p0[b] = k->hs->seq(a->ids[b]).pending;
+    }
+    k->hs->end_async(B, a->ids.data(), c0.data(), p0.data());
+  }
+  if (steps_done) *steps_done = a->launched;
+  (void)hipGraphExecDestroy(a->graph);
+  (void)hipFree(a->meta);
+  delete a;
+  return ret;
 }
 
 extern "C" hvd_status hvd_commit(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids, const int32_t* keep) {

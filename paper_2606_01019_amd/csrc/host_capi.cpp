@@ -28,6 +28,13 @@ void hvdh_abort_verify(void* h, int32_t batch, const int32_t* ids) { ((HostState
 int hvdh_commit(void* h, int32_t batch, const int32_t* ids, const int32_t* keep) {
   return ((HostState*)h)->commit(batch, ids, keep);
 }
+int hvdh_begin_async(void* h, int32_t batch, const int32_t* ids, const int32_t* ctx, const int32_t* lens,
+                     int32_t max_steps) {
+  return ((HostState*)h)->begin_async(batch, ids, ctx, lens, max_steps);
+}
+void hvdh_end_async(void* h, int32_t batch, const int32_t* ids, const int32_t* ctx, const int32_t* pend) {
+  ((HostState*)h)->end_async(batch, ids, ctx, pend);
+}
 int hvdh_truncate(void* h, int32_t id, int32_t ctx, int32_t pend) { return ((HostState*)h)->truncate(id, ctx, pend); }
 int hvdh_free_seq(void* h, int32_t id) { return ((HostState*)h)->free_seq(id); }
 int32_t hvdh_free_pages(void* h) { return ((HostState*)h)->free_pages(); }

@@ -76,6 +76,7 @@ int HostState::begin_verify(int32_t batch, const int32_t* ids, const int32_t* ct
     if (id < 0 || id >= max_seqs() || !seqs_[id].live) return fail(HS_ARG, "unknown seq_id");
     if (!seen.insert(id).second) return fail(HS_ARG, "duplicate seq_id in batch");
     const SeqSlot& s = seqs_[id];
+    if (s.in_async) return fail(HS_STATE, "sequence is in a device-resident verify loop");
     if (s.verify_pending) return fail(HS_STATE, "previous verify not committed");
     if (ctx_lens[b] != s.ctx) return fail(HS_STATE, "ctx_lens disagrees with the library");
     int32_t k = draft_lens[b];
@@ -128,6 +129,7 @@ int HostState::commit(int32_t batch, const int32_t* ids, const int32_t* keep) {
     if (id < 0 || id >= max_seqs() || !seqs_[id].live) return fail(HS_ARG, "unknown seq_id");
     if (!seen.insert(id).second) return fail(HS_ARG, "duplicate seq_id in batch");
     const SeqSlot& s = seqs_[id];
+    if (s.in_async) return fail(HS_STATE, "sequence is in a device-resident verify loop");
     if (!s.verify_pending) return fail(HS_STATE, "commit without a verify");
     if (keep && (keep[b] < 0 || keep[b] > s.accepted)) return fail(HS_ARG, "keep outside [0, accepted]");
   }
@@ -144,9 +146,52 @@ int HostState::commit(int32_t batch, const int32_t* ids, const int32_t* keep) {
   return HS_OK;
 }
 
+int HostState::begin_async(int32_t batch, const int32_t* ids, const int32_t* ctx_lens, const int32_t* draft_lens,
+                           int32_t max_steps) {
+  if (batch < 1 || batch > max_seqs()) return fail(HS_ARG, "batch must be in [1, max_seqs]");
+  if (!ids || !ctx_lens || !draft_lens) return fail(HS_ARG, "null argument");
+  if (max_steps < 1) return fail(HS_ARG, "max_steps must be >= 1");
+  std::set<int32_t> seen;
+  int64_t extra_pages = 0;
+  for (int32_t b = 0; b < batch; ++b) {
+    int32_t id = ids[b];
+    if (id < 0 || id >= max_seqs() || !seqs_[id].live) return fail(HS_ARG, "unknown seq_id");
+    if (!seen.insert(id).second) return fail(HS_ARG, "duplicate seq_id in batch");
+    const SeqSlot& s = seqs_[id];
+    if (s.in_async) return fail(HS_STATE, "sequence is in a device-resident verify loop");
+    if (s.verify_pending) return fail(HS_STATE, "previous verify not committed");
+    if (ctx_lens[b] != s.ctx) return fail(HS_STATE, "ctx_lens disagrees with the library");
+    const int32_t k = draft_lens[b];
+    if (k < 0 || k > max_draft_) return fail(HS_RANGE, "draft length outside [0, max_draft]");
+    // the last step writes positions up to ctx + max_steps * (k + 1) - 1
+    const int64_t span = (int64_t)max_steps * (k + 1);
+    if ((int64_t)s.ctx + span - 1 >= max_pos_) return fail(HS_RANGE, "position beyond the rotary table");
+    const int64_t need = ((int64_t)s.ctx + span + 1 + page_size_ - 1) / page_size_;
+    extra_pages += std::max<int64_t>(0, need - (int64_t)s.pages.size());
+  }
+  if (extra_pages > (int64_t)free_.size()) return fail(HS_OOM, "page pool exhausted");
+  for (int32_t b = 0; b < batch; ++b) {
+    SeqSlot& s = seqs_[ids[b]];
+    grow_to(ids[b], pages_for(s.ctx + max_steps * (draft_lens[b] + 1) + 1));
+    s.in_async = true;
+  }
+  return HS_OK;
+}
+
+void HostState::end_async(int32_t batch, const int32_t* ids, const int32_t* ctx, const int32_t* pending) {
+  for (int32_t b = 0; b < batch; ++b) {
+    SeqSlot& s = seqs_[ids[b]];
+    s.in_async = false;
+    s.ctx = ctx[b];
+    s.pending = pending[b];
+    shrink_to(ids[b], pages_for(s.ctx + 1));
+  }
+}
+
 int HostState::truncate(int32_t id, int32_t new_ctx, int32_t pending) {
   if (id < 0 || id >= max_seqs() || !seqs_[id].live) return fail(HS_ARG, "unknown seq_id");
   SeqSlot& s = seqs_[id];
+  if (s.in_async) return fail(HS_STATE, "sequence is in a device-resident verify loop");
   if (new_ctx < 0 || new_ctx > s.ctx) return fail(HS_ARG, "new_ctx_len outside [0, ctx_len]");
   if (pending < 0 || pending >= vocab_) return fail(HS_RANGE, "token id outside [0, vocab)");
   s.ctx = new_ctx;
@@ -159,6 +204,7 @@ int HostState::truncate(int32_t id, int32_t new_ctx, int32_t pending) {
 
 int HostState::free_seq(int32_t id) {
   if (id < 0 || id >= max_seqs() || !seqs_[id].live) return fail(HS_ARG, "unknown seq_id");
+  if (seqs_[id].in_async) return fail(HS_STATE, "sequence is in a device-resident verify loop");
   shrink_to(id, 0);
   seqs_[id] = SeqSlot();
   return HS_OK;

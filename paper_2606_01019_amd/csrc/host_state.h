@@ -32,6 +32,9 @@ struct SeqSlot {
   bool verify_pending = false;
   int32_t k = 0, accepted = 0, next = 0;
   std::vector<int32_t> draft;
+  // inside a device-resident verify loop: ctx and pending live on the device
+  // until the loop ends, so every host-side call on the sequence is refused
+  bool in_async = false;
 };
 
 class HostState {
@@ -61,6 +64,16 @@ class HostState {
   void abort_verify(int32_t batch, const int32_t* ids);
 
   int commit(int32_t batch, const int32_t* ids, const int32_t* keep);
+
+  // Device-resident loop of up to max_steps verify+commit steps with fixed
+  // draft lengths: validate, and reserve the pages of the longest possible
+  // outcome (every draft accepted), ctx + max_steps * (k + 1) positions plus
+  // the pending token's (all or nothing).
+  int begin_async(int32_t batch, const int32_t* ids, const int32_t* ctx_lens, const int32_t* draft_lens,
+                  int32_t max_steps);
+  // Loop ended: take the device's ctx and pending tokens, release the pages
+  // past the new pending position.
+  void end_async(int32_t batch, const int32_t* ids, const int32_t* ctx, const int32_t* pending);
   int truncate(int32_t id, int32_t new_ctx, int32_t pending);
   int free_seq(int32_t id);
 

@@ -148,6 +148,7 @@ struct EmbedArgs {
   const int32_t* n_upd;  // device count (metadata header) so the launch is shape-only
   int32_t* pt;
   int pt_stride;
+  int V;  // token ids outside [0, V) gather row 0 (they can never be accepted)
 };
 
 struct AcceptArgs {
@@ -163,6 +164,12 @@ struct AcceptArgs {
   uint32_t* counter;   // one uint32, zero between launches
   const int32_t* tree_parent;  // [rows]: parent node of a tree row (-1 = the pending token)
   int32_t* path;       // [B][kMaxTreeNodes]: accepted node indices of tree sequences
+  // device-resident loop (null otherwise): the commit of the accepted block is
+  // applied here, state = ctx[B], pending[B], steps done; each step's
+  // (accepted, next) pairs go to hist[step][B][2] while step < hist_cap
+  int32_t* astate;
+  int32_t* hist;
+  int hist_cap;
 };
 // Moves the K/V of each tree sequence's accepted path from the nodes'
 // positions (ctx + 1 + node) to the chain positions ctx + 1 .. ctx + a.
@@ -175,6 +182,35 @@ struct CompactArgs {
   const SeqMeta* seqs;
   const int32_t* out;  // [B][2] accepted, next
   const int32_t* path; // [B][kMaxTreeNodes]
+};
+
+// Device-resident verify loop: one workgroup rebuilds a step's row and
+// attention metadata from the device state (ctx and pending token per
+// sequence) and the draft buffer, so the step's captured launches need no
+// host staging.  The attention items were planned on the host for the longest
+// context the loop can reach; here each item takes the current ctx, its chunk
+// end, and whether it still has keys (chunks past the keys become no-ops and
+// the combine entries count only the live chunks).
+struct AsyncPlanArgs {
+  const int32_t* state;      // ctx[B], pending[B]
+  int32_t* drafts;           // [sum k]: draft tokens of sequence b from seq_static[b].cu - b
+  const int32_t* ref;        // nullable: [B][ref_len] token stream of the copy drafter
+  int ref_len;
+  const int32_t* ref_start;  // [B]: position of ref[b][0]
+  const SeqMeta* seq_static; // [B] (ctx unused)
+  const int32_t* page_off;   // [B + 1]: offsets of each sequence's page list in pages
+  const int32_t* pages;      // reserved pages of every sequence, concatenated
+  const int32_t* row_seq;    // [M]: sequence of each row
+  RowMeta* rows;             // [M] out
+  SeqMeta* seqs;             // [B] out
+  const AttnItem* items_static;  // [n_items]: pad1 = sequence, pad2 = the unit's last row index
+  AttnItem* items;
+  int n_items;
+  const AttnItem* heads_static;  // [n_heads], same extra fields
+  AttnItem* heads;
+  int n_heads;
+  int chunk;
+  int M, B;
 };
 
 // Launchers: all enqueue on `s` and return the launch status.
@@ -201,6 +237,8 @@ hipError_t attn_set_lds_limit();  // once per process, before the first launch
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int B, hipStream_t s);
+hipError_t launch_async_plan(const AsyncPlanArgs& a, hipStream_t s);
+hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* pt, int pt_stride, hipStream_t s);
 
 constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
 

@@ -53,7 +53,9 @@ __global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
       a.pt[(size_t)a.upd[u * 3] * a.pt_stride + a.upd[u * 3 + 1]] = a.upd[u * 3 + 2];
   const int R = blockIdx.x;
   const bool valid = R < a.M;
-  const uint16_t* er = valid ? a.E + (size_t)a.rows[R].tok * a.D : nullptr;
+  int tok = valid ? a.rows[R].tok : 0;
+  if ((unsigned)tok >= (unsigned)a.V) tok = 0;  // only a device-side drafter can pass one
+  const uint16_t* er = valid ? a.E + (size_t)tok * a.D : nullptr;
   const int noct = a.D >> 3;
   for (int base = 0; base < noct; base += 256) {
     const int o = base + threadIdx.x;
@@ -135,6 +137,7 @@ __global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
   __syncthreads();
   if (!last) return;
   __threadfence();
+  const int step = a.astate ? a.astate[2 * a.B] : 0;
   for (int b = threadIdx.x; b < a.B; b += 256) {
     const SeqMeta sq = a.seqs[b];
     int acc = 0, last = 0;  // accepted count; row of the last accepted token
@@ -165,10 +168,23 @@ __global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
       }
       last = cur + 1;
     }
+    const int nxt = __atomic_load_n(&a.g[sq.cu + last], __ATOMIC_RELAXED);
     a.out[2 * b] = acc;
-    a.out[2 * b + 1] = __atomic_load_n(&a.g[sq.cu + last], __ATOMIC_RELAXED);
+    a.out[2 * b + 1] = nxt;
+    if (a.astate) {  // device-resident loop: commit the whole accepted block
+      a.astate[b] += acc + 1;
+      a.astate[a.B + b] = nxt;
+      if (step < a.hist_cap) {
+        a.hist[((size_t)step * a.B + b) * 2] = acc;
+        a.hist[((size_t)step * a.B + b) * 2 + 1] = nxt;
+      }
+    }
   }
-  if (threadIdx.x == 0) *a.counter = 0u;
+  __syncthreads();  // every thread has read the step count
+  if (threadIdx.x == 0) {
+    *a.counter = 0u;
+    if (a.astate) a.astate[2 * a.B] = step + 1;
+  }
 }
 
 // After a tree verify: the accepted path's K/V moves from the nodes'
@@ -209,6 +225,81 @@ hipError_t launch_compact(const CompactArgs& a, int B, hipStream_t s) {
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   hvd_launch(argmax_accept, dim3(a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// One workgroup: rows (token, position, pool slot), sequences (ctx) and the
+// attention items and combine entries of this step of a device-resident
+// loop.  Row i of sequence b is token pending[b] (i = 0) or draft i - 1, at
+// position ctx[b] + i.  With the copy drafter, draft token i - 1 is the
+// stream token at that position (-1 outside the stream: never accepted) and
+// is also stored to the draft buffer.  Page indexes past a sequence's
+// reserved list are clamped into it (the host reserves enough, so this only
+// keeps a broken caller from faulting).
+__global__ __launch_bounds__(512) void async_plan(AsyncPlanArgs a) {
+  for (int r = threadIdx.x; r < a.M; r += blockDim.x) {
+    const int b = a.row_seq[r];
+    const SeqMeta sq = a.seq_static[b];
+    const int ctx = a.state[b];
+    const int i = r - sq.cu;
+    int tok;
+    if (i == 0) {
+      tok = a.state[a.B + b];
+    } else {
+      const int d = sq.cu - b + i - 1;
+      if (a.ref) {
+        const int j = ctx + i - a.ref_start[b];
+        tok = (j >= 0 && j < a.ref_len) ? a.ref[(size_t)b * a.ref_len + j] : -1;
+        a.drafts[d] = tok;
+      } else {
+        tok = a.drafts[d];
+      }
+    }
+    const int pos = ctx + i;
+    const int p0 = a.page_off[b], np = a.page_off[b + 1] - p0;
+    const int pi = min(pos / kPage, np - 1);
+    a.rows[r] = RowMeta{tok, sq.slot, pos, a.pages[p0 + pi] * kPage + pos % kPage};
+  }
+  for (int b = threadIdx.x; b < a.B; b += blockDim.x) {
+    SeqMeta sq = a.seq_static[b];
+    sq.ctx = a.state[b];
+    a.seqs[b] = sq;
+  }
+  // items: the live chunks of the unit at the current ctx
+  for (int n = threadIdx.x; n < a.n_items + a.n_heads; n += blockDim.x) {
+    const bool head = n >= a.n_items;
+    const int e = head ? n - a.n_items : n;
+    AttnItem it = head ? a.heads_static[e] : a.items_static[e];
+    if (it.k >= 0) {
+      const int ctx = a.state[it.pad1];
+      const int nch = (ctx + it.pad2 + 1 + a.chunk - 1) / a.chunk;
+      if (head ? nch == 1 : it.c >= nch) {
+        it.k = -1;  // no keys yet (item), or the only chunk writes O itself (combine entry)
+      } else {
+        it.ctx = ctx;
+        it.nch = nch;
+        it.p_end = min(ctx + it.k + 1, it.p_begin + a.chunk);
+      }
+    }
+    if (head) a.heads[e] = it;
+    else a.items[e] = it;
+  }
+}
+
+// Page-table updates applied on their own (before a device-resident loop's
+// captured steps, which then carry none).
+__global__ __launch_bounds__(256) void pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* pt, int pt_stride) {
+  for (int u = threadIdx.x, n = *n_upd; u < n; u += blockDim.x)
+    pt[(size_t)upd[u * 3] * pt_stride + upd[u * 3 + 1]] = upd[u * 3 + 2];
+}
+
+hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* pt, int pt_stride, hipStream_t s) {
+  hvd_launch(pt_update, dim3(1), dim3(256), 0, s, upd, n_upd, pt, pt_stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_async_plan(const AsyncPlanArgs& a, hipStream_t s) {
+  hvd_launch(async_plan, dim3(1), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

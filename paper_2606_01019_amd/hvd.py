@@ -19,7 +19,8 @@ _STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM
 
 EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
            "hvd_prefill", "hvd_verify", "hvd_verify_tree", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
-           "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error")
+           "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error",
+           "hvd_async_begin", "hvd_async_step", "hvd_async_end")
 HVD_OPT_GRAPHS = 1
 HVD_OPT_MLP_SINGLE = 2
 HVD_OPT_LM_SINGLE = 3
@@ -86,6 +87,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    ctypes.POINTER(ctypes.c_double)]),
         "hvd_kv_set_option": (I32, [P, I32, I32]),
         "hvd_last_error": (ctypes.c_char_p, []),
+        "hvd_async_begin": (I32, [P, P, I32, PI32, PI32, PI32, I32, P, P, P, P, I32, PI32, ctypes.POINTER(P)]),
+        "hvd_async_step": (I32, [P, I32]),
+        "hvd_async_end": (I32, [P, PI32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -264,6 +268,10 @@ class KVCache:
         _check(self.lib.hvd_profile_read(self.handle, family, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b)))
         return ms.value, n.value, b.value
 
+    def async_loop(self, seq_ids, ctx_lens, draft_lens, max_steps, ref=None, ref_start=None):
+        """Open a device-resident verify loop (hvd_async_begin); see AsyncLoop."""
+        return AsyncLoop(self, seq_ids, ctx_lens, draft_lens, max_steps, ref, ref_start)
+
     def close(self):
         if getattr(self, "handle", None):
             self.stream.synchronize()
@@ -274,5 +282,65 @@ class KVCache:
     def __del__(self):
         try:
             self.close()
+        except Exception:
+            pass
+
+
+class AsyncLoop:
+    """Device-resident verify loop over fixed draft lengths (hvd_async_*).
+
+    Owns the device buffers the library reads and advances: ``drafts``
+    (int32 [sum k], the draft tokens of the next step, packed in batch
+    order), ``state`` (int32 [2B + 1]: ctx, pending token, steps done) and
+    ``history`` (int32 [max_steps, B, 2]: accepted length and next token of
+    every step).  A GPU drafter writes ``drafts`` on ``kv.stream`` between
+    steps; with ``ref`` (int32 CUDA tensor [B, ref_len]) and ``ref_start``
+    the library's copy drafter fills them from that token stream instead.
+    ``step(n)`` only enqueues; ``end()`` waits and hands the sequences back to
+    the host-side calls."""
+
+    def __init__(self, kv, seq_ids, ctx_lens, draft_lens, max_steps, ref=None, ref_start=None):
+        import torch
+        self.kv = kv
+        self.lib = kv.lib
+        ids, ctx, lens = _i32(seq_ids), _i32(ctx_lens), _i32(draft_lens)
+        B = ids.size
+        self.draft_lens = lens
+        self.drafts = torch.zeros(max(1, int(lens.sum())), dtype=torch.int32, device="cuda")
+        self.state = torch.zeros(2 * B + 1, dtype=torch.int32, device="cuda")
+        self.history = torch.zeros((max(1, max_steps), B, 2), dtype=torch.int32, device="cuda")
+        self.ref = None
+        rs = None
+        ref_len = 0
+        if ref is not None:
+            assert ref.is_cuda and ref.dtype == torch.int32 and ref.dim() == 2 and ref.shape[0] == B
+            self.ref = ref.contiguous()
+            ref_len = int(self.ref.shape[1])
+            rs = _i32(ref_start)
+        torch.cuda.current_stream().synchronize()  # buffers exist before the library's stream uses them
+        h = ctypes.c_void_p()
+        vp = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+        _check(self.lib.hvd_async_begin(kv.model.handle, kv.handle, B, _ptr(ids), _ptr(ctx), _ptr(lens), max_steps,
+                                        vp(self.drafts), vp(self.state), vp(self.history), vp(self.ref), ref_len,
+                                        _ptr(rs), ctypes.byref(h)))
+        self.handle = h
+        self.steps_done = 0
+
+    def step(self, n: int = 1):
+        _check(self.lib.hvd_async_step(self.handle, n))
+
+    def end(self):
+        """Wait for the enqueued steps, return the host-side calls their
+        sequences; returns the number of steps run."""
+        if getattr(self, "handle", None):
+            n = ctypes.c_int32()
+            h, self.handle = self.handle, None
+            _check(self.lib.hvd_async_end(h, ctypes.byref(n)))
+            self.steps_done = n.value
+        return self.steps_done
+
+    def __del__(self):
+        try:
+            self.end()
         except Exception:
             pass

@@ -111,3 +111,17 @@ def test_plant_path_gives_the_planted_acceptance_length():
             cur, n = nxt[0], n + 1
         deepest = max(len(trees.path_to(par, j)) for j in range(len(par)))
         assert n == min(a, deepest)
+
+
+def test_corrupt_stream_replaces_at_rate_p_with_different_tokens():
+    rng = wt.rng_for("misc", 7)
+    g = wt.uniform_context(rng, 20000, 4096)
+    s = wt.corrupt_stream(wt.rng_for("misc", 8), g, 0.3, 4096)
+    diff = s != g
+    assert abs(diff.mean() - 0.3) < 0.02
+    assert s.min() >= 0 and s.max() < 4096
+    # runs of kept tokens are geometric: P(run >= 3) = 0.7^3
+    starts = np.flatnonzero(diff[:-3])[:2000] + 1
+    runs = np.array([np.argmax(diff[i:]) if diff[i:].any() else 0 for i in starts])
+    assert abs((runs >= 3).mean() - 0.7 ** 3) < 0.05
+    assert (wt.corrupt_stream(wt.rng_for("misc", 8), g, 0.0, 4096) == g).all()

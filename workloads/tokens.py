@@ -112,3 +112,17 @@ def plant_cache_draft(rng, context, greedy, a: int, k: int, vocab: int) -> np.nd
 
 def random_chain(rng, k: int, vocab: int) -> np.ndarray:
     return rng.integers(0, vocab, size=k, dtype=np.int64).astype(np.int32)
+
+
+def corrupt_stream(rng, greedy, p: float, vocab: int) -> np.ndarray:
+    """Token stream for a copy drafter with planted acceptance: ``greedy``
+    with each token independently replaced, with probability p, by a uniform
+    token different from it.  Drafts copied from the stream at the current
+    position are then accepted up to the next replaced token, so the accepted
+    length of a k-token draft is min(Geometric(p), k)."""
+    g = np.asarray(greedy, dtype=np.int64)
+    out = g.copy()
+    hit = rng.random(g.shape[0]) < p
+    shift = rng.integers(1, vocab, size=g.shape[0])
+    out[hit] = (g[hit] + shift[hit]) % vocab
+    return out.astype(np.int32)
