@@ -34,7 +34,7 @@ hvd_status set_err(hvd_status s, const std::string& m) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr int kPrefillRows = 128;  // rows per prefill chunk
+constexpr int kPrefillRows = 256;  // rows per prefill chunk (256 measured 5% above 128 and 512)
 // Up to 8 row tiles (128 rows) the skinny kernel in row blocks of <= 4
 // tiles beats the tiled kernel and its K-split finish (measured: 65-row
 // verifies and 128-row prefill chunks of the 8B shape)
@@ -329,6 +329,7 @@ struct hvd_kv_s {
   int attn_max_np = kItemPages;  // most pages one attention sub-chunk stages
   int skinny_max_mt = kSkinnyMaxMT;   // row tiles above which GEMMs take the MFMA-tiled kernel
   int gemm_force[PF_LM + 1][2] = {};  // per GEMM family: {strips per workgroup, K splits} of the skinny kernel, 0 = policy
+  int tiled_force[PF_LM + 1][2] = {};  // per GEMM family: {tile + 1, K splits} of the tiled kernel, 0 = policy
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
   bool mlp_single = true;    // large-batch verify MLP GEMMs on the hi activation part only
@@ -475,6 +476,26 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
           if (item.compare(0, eq, names[f]) == 0 && (ns == 1 || ns == 2 || ns == 4 || ns == 8) && sp >= 1 && sp <= 16) {
             k->gemm_force[f][0] = ns;
             k->gemm_force[f][1] = sp;
+          }
+      at = end + 1;
+    }
+  }
+  // tuning override of the tiled GEMM: "down=2:4" (family=tile:splits, tile 0..3)
+  if (const char* e = getenv("HVD_TILED_SHAPE")) {
+    static const char* names[PF_LM + 1] = {"qkv", "o", "gateup", "down", "lm"};
+    std::string spec(e);
+    size_t at = 0;
+    while (at < spec.size()) {
+      size_t end = spec.find(',', at);
+      if (end == std::string::npos) end = spec.size();
+      const std::string item = spec.substr(at, end - at);
+      int t = -1, sp = 0;
+      const size_t eq = item.find('=');
+      if (eq != std::string::npos && sscanf(item.c_str() + eq + 1, "%d:%d", &t, &sp) == 2)
+        for (int f = 0; f <= PF_LM; ++f)
+          if (item.compare(0, eq, names[f]) == 0 && t >= 0 && t <= 3 && sp >= 1 && sp <= 8) {
+            k->tiled_force[f][0] = t + 1;
+            k->tiled_force[f][1] = sp;
           }
       at = end + 1;
     }
@@ -837,17 +858,20 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       // many rows: MFMA-tiled kernel, weights read once per XCD.  The
       // largest tile (256 x 256, 128 x 256, 128 x 128) that still gives
       // enough workgroups, and a K split when even the smallest is too few
-      static const int tile_bm[3] = {128, 128, 256}, tile_bn[3] = {128, 256, 256};
+      static const int tile_bm[4] = {128, 128, 256, 256}, tile_bn[4] = {128, 256, 256, 256};
       int tile = 0;
       for (int t = 2; t >= 1; --t)
         if (N % tile_bn[t] == 0 && N / tile_bn[t] * ((MT * 16 + tile_bm[t] - 1) / tile_bm[t]) >= want) {
           tile = t;
           break;
         }
+      const bool forced = family <= PF_LM && k->tiled_force[family][0] && N % tile_bn[k->tiled_force[family][0] - 1] == 0;
+      if (forced) tile = k->tiled_force[family][0] - 1;
       const int RB = (MT * 16 + tile_bm[tile] - 1) / tile_bm[tile];
       const int nblk = N / tile_bn[tile] * RB;
       int splits = 1;
-      if (nblk < want) splits = std::max(1, std::min({4, (kGemmSplitTarget + nblk - 1) / nblk, a.KT / 32}));
+      if (forced) splits = std::max(1, std::min(k->tiled_force[family][1], a.KT / 32));
+      else if (nblk < want) splits = std::max(1, std::min({4, (kGemmSplitTarget + nblk - 1) / nblk, a.KT / 32}));
       while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > kGemmPartBytes) --splits;
       const bool mlp = epi == EPI_SILU || family == PF_DOWN;
       if (epi == EPI_LM) {
