@@ -86,3 +86,36 @@ def test_mid_batched_decode_loop(mid):
                          else oracle.commit(states[s], results[s]))
             assert kv.seq_info(s)[:2] == (states[s].ctx, states[s].pending)
     print(rep)
+
+
+def test_mid_maximum_rows_ragged_contexts(mid):
+    """The largest verify a handle of 32 sequences takes: every sequence
+    drafts max_draft = 64 tokens (2080 rows: MFMA-tiled GEMMs, two attention
+    row groups per kv head), over ragged contexts from the degenerate empty
+    cache (a one-token prompt) to 700 tokens."""
+    import paper_2606_01019_amd as hvd
+    torch, om, gm = mid
+    B, k = 32, MID.max_draft
+    lens = [1, 2, 17, 31] + [int(x) for x in wt.rng_for("misc", 70).integers(40, 700, size=B - 4)]
+    kv = hvd.KVCache(gm, max_seqs=B, n_pages=sum((L + k + 16) // 16 + 1 for L in lens) + 8)
+    states, drafts, results = [], [], []
+    drng = wt.rng_for("draft", 70)
+    for s, L in enumerate(lens):
+        c = wt.uniform_context(wt.rng_for("context", 70 + s), L, MID.vocab)
+        st = oracle.prefill(om, c)
+        kv.prefill(s, c)
+        g, _ = oracle.greedy_decode(om, st, 9)
+        full = np.concatenate([g, wt.random_chain(drng, k + 1 - len(g), MID.vocab)])
+        d = wt.plant_chain(drng, full, int(drng.integers(0, 9)), k, MID.vocab)
+        states.append(st)
+        drafts.append(d)
+        results.append(oracle.verify(om, st, d))
+    print(f"{B} sequences, {B * (k + 1)} rows, contexts {min(lens) - 1}..{max(lens) - 1}", flush=True)
+    a, n, lg = _verify(torch, kv, list(range(B)), [st.ctx for st in states], drafts)
+    rep = Report()
+    for s in range(B):
+        check_step(rep, results[s], lg[s * (k + 1):(s + 1) * (k + 1)], int(a[s]), int(n[s]), drafts[s])
+    kv.commit(list(range(B)))
+    for s in range(B):
+        assert kv.seq_info(s)[0] == states[s].ctx + int(a[s]) + 1
+    print(rep)
