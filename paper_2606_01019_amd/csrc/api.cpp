@@ -44,6 +44,7 @@ constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (o
 constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
 constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
+constexpr int kCUs = 256;                     // compute units of the MI355X
 constexpr int kAttnRows = 128;     // query rows per attention work item
 constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items)
 constexpr size_t kMaxGraphs = 64;  // cached step graphs per KV handle
@@ -855,23 +856,26 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.part = k->gemm_part;
     const int want = k->gemm_min_blocks;
     if (MT > k->skinny_max_mt && N % 128 == 0) {
-      // many rows: MFMA-tiled kernel, weights read once per XCD.  The
-      // largest tile (256 x 256, 128 x 256, 128 x 128) that still gives
-      // enough workgroups, and a K split when even the smallest is too few
+      // many rows: MFMA-tiled kernel, weights read once per XCD.  Of the
+      // tiles that give at least one workgroup per CU, 256 x 256 unless the
+      // 128-row tile pads the rows less (the padded rows' MFMA work is
+      // wasted: 848 rows run as 1024 or as 896); else 128 x 128, with a K
+      // split when even that leaves CUs idle (measured at 848 rows: down and
+      // O 8% faster split two ways at 224 workgroups)
       static const int tile_bm[4] = {128, 128, 256, 256}, tile_bn[4] = {128, 256, 256, 256};
+      const int want_t = std::max(want, kCUs);
+      auto rb_of = [&](int t) { return (MT * 16 + tile_bm[t] - 1) / tile_bm[t]; };
+      auto fits = [&](int t) { return N % tile_bn[t] == 0 && N / tile_bn[t] * rb_of(t) >= want_t; };
       int tile = 0;
-      for (int t = 2; t >= 1; --t)
-        if (N % tile_bn[t] == 0 && N / tile_bn[t] * ((MT * 16 + tile_bm[t] - 1) / tile_bm[t]) >= want) {
-          tile = t;
-          break;
-        }
+      if (fits(2) && !(fits(1) && rb_of(1) * 128 < rb_of(2) * 256)) tile = 2;
+      else if (fits(1)) tile = 1;
       const bool forced = family <= PF_LM && k->tiled_force[family][0] && N % tile_bn[k->tiled_force[family][0] - 1] == 0;
       if (forced) tile = k->tiled_force[family][0] - 1;
       const int RB = (MT * 16 + tile_bm[tile] - 1) / tile_bm[tile];
       const int nblk = N / tile_bn[tile] * RB;
       int splits = 1;
       if (forced) splits = std::max(1, std::min(k->tiled_force[family][1], a.KT / 32));
-      else if (nblk < want) splits = std::max(1, std::min({4, (kGemmSplitTarget + nblk - 1) / nblk, a.KT / 32}));
+      else if (nblk < want_t) splits = std::max(1, std::min({4, (want_t + nblk - 1) / nblk, a.KT / 32}));
       while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > kGemmPartBytes) --splits;
       const bool mlp = epi == EPI_SILU || family == PF_DOWN;
       if (epi == EPI_LM) {
