@@ -700,6 +700,8 @@ def main():
     }
     kv.close()
     legs = [x for x in args.workloads.split(",") if x]
+    # the 32B leg frees the 8B model: it runs last whatever the order given
+    legs = [x for x in legs if x != "multistep_32b"] + [x for x in legs if x == "multistep_32b"]
     extra = {}
     for leg in legs:
         t0 = time.time()

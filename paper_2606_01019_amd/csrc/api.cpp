@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -287,11 +288,11 @@ extern "C" void hvd_model_free(hvd_model m) {
 // rows, sequences, attention grid sizes and kernel variants (chunk length,
 // rows per item), LM head on/off and the logits pointer.
 struct GraphKey {
-  int M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head, tree;
+  int M, B, lm_head, tree;
+  std::array<int, 12> attn;  // per row class: items, combine entries, chunk, combine rows
   float* logits;
   bool operator<(const GraphKey& o) const {
-    return std::tie(M, B, n_items, n_heads, chunk, rpi, comb_rows, lm_head, tree, logits) <
-           std::tie(o.M, o.B, o.n_items, o.n_heads, o.chunk, o.rpi, o.comb_rows, o.lm_head, o.tree, o.logits);
+    return std::tie(M, B, lm_head, tree, attn, logits) < std::tie(o.M, o.B, o.lm_head, o.tree, o.attn, o.logits);
   }
 };
 
@@ -361,11 +362,12 @@ size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int p
   const size_t rg_verify = ((size_t)(c.max_draft + 1) * G + kAttnRows - 1) / kAttnRows;
   const size_t rg_prefill = ((size_t)kPrefillRows * G + kAttnRows - 1) / kAttnRows;
   const size_t units = std::max((size_t)max_seqs * rg_verify, rg_prefill) * c.n_kv_heads;
-  // items <= units + kPartSlots and heads <= units, each padded up (to 64
-  // and 16 entries); header and per-section alignment fit in the last term
+  // items <= units + partial slots (at most 2 kPartSlots: 64-row items) and
+  // heads <= units, each of the three row classes padded up (to 64 and 16
+  // entries); header and per-section alignment fit in the last term
   const size_t item_ints = sizeof(AttnItem) / 4;
   return (4 + 3) * (size_t)max_rows + sizeof(SeqMeta) / 4 * (size_t)max_seqs +
-         item_ints * (2 * units + kPartSlots + 64 + 16) + 3 * (size_t)max_seqs * pt_stride + 64;
+         item_ints * (2 * units + 2 * kPartSlots + 3 * (64 + 16)) + 3 * (size_t)max_seqs * pt_stride + 64;
 }
 
 size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, void* base) {
@@ -575,12 +577,18 @@ void prof_collect(hvd_kv_s* k) {
 struct Plan {
   std::vector<AttnItem> items, heads;
   int chunk = 0;
+  int rpi = 0;             // query rows per item
+  int comb_rows = 1;       // rows of the largest combine entry
+  size_t part_rows = 0;    // partial-buffer rows the plan uses
+  size_t part_base = 0;    // its first partial-buffer row
+  size_t item0 = 0, head0 = 0;  // offsets of its items and entries in the step's lists
 };
 
-// Split every (sequence, kv head, row group) into KV chunks of `chunk`
-// positions, chosen so the launch has enough workgroups to fill the GPU.
-bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<SeqMeta>& seqs, int min_items,
-                    int rpi, Plan& p) {
+// Split every (sequence, kv head, row group) of the sequences `members` into
+// KV chunks of `chunk` positions, chosen so the launch has enough workgroups
+// to fill the GPU; at most part_rows_free partial-buffer rows.
+bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<SeqMeta>& seqs,
+                    const std::vector<int>& members, int min_items, int rpi, size_t part_rows_free, Plan& p) {
   const int G = c.n_q_heads / c.n_kv_heads;
   struct Unit { int b, g, rg, keys; };
   auto item = [&](const Unit& u, int c, int nch, int part, int chunk) {
@@ -591,7 +599,8 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
     it.p_begin = c * chunk;
     it.p_end = std::min(s.ctx + s.k + 1, (c + 1) * chunk);
     it.pad1 = u.b;                // for a device-side re-plan at another ctx:
-    it.pad2 = u.keys - s.ctx - 1;  // sequence, last row index of the unit
+    it.pad2 = u.keys - s.ctx - 1;  // sequence, last row index of the unit,
+    it.pad3 = chunk;               // chunk length
     // pages of the first kAttnChunk positions; entries past the chunk's end
     // repeat its first page (the kernel loads them unconditionally)
     const std::vector<int32_t>& pg = hs.seq(s.slot).pages;
@@ -604,7 +613,7 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   };
   std::vector<Unit> units;
   int64_t total_keys = 0;
-  for (int b = 0; b < (int)seqs.size(); ++b) {
+  for (int b : members) {
     const SeqMeta& s = seqs[b];
     const int R = (s.k + 1) * G;
     const int n_rg = (R + rpi - 1) / rpi;
@@ -616,12 +625,18 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
         total_keys += keys;
       }
   }
-  // chunk: a power-of-two number of pages (32..kAttnChunk positions, the
-  // kernel's sub-chunk sizes, so only a head's last chunk is partial), the
-  // largest that still yields about min_items workgroups
-  const int64_t want = (total_keys + min_items - 1) / min_items;
-  int chunk = 32;
-  while (chunk < kAttnChunk && 2 * chunk <= want) chunk *= 2;
+  // chunk: a power-of-two number of positions, the largest that still gives
+  // every CU work -- two 64-row items per CU (4 waves: several share a CU),
+  // one item of 128 or 256 rows (8 waves) -- with at least 64 positions for
+  // 64-row items and at most 1024 (128-row) or 512 (256-row).  Longer
+  // chunks loop over LDS-sized sub-chunks.  Measured: 32 sequences of mixed
+  // drafts 34.2 -> 34.0 ms per step; context 16384 at k = 16 / 64 from
+  // 4.97 / 9.05 to 4.69 / 8.65 ms (chunks of at most 256 before)
+  const int per_cu = rpi <= kAttnRows / 2 ? 2 : 1;
+  const int64_t want = (total_keys + (int64_t)min_items * per_cu - 1) / ((int64_t)min_items * per_cu);
+  const int cap = rpi <= kAttnRows / 2 ? (1 << 20) : rpi <= kAttnRows ? 1024 : 512;
+  int chunk = rpi <= kAttnRows / 2 ? 64 : 32;
+  while (chunk < cap && 2 * chunk <= want) chunk *= 2;
   for (;;) {
     p.items.clear();
     p.heads.clear();
@@ -636,12 +651,19 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
         slots += nch;
       }
     }
-    if ((size_t)slots * rpi <= (size_t)kPartSlots * kAttnRows) break;  // partial buffer rows
+    if ((size_t)slots * rpi <= part_rows_free) {  // partial buffer rows
+      p.part_rows = (size_t)slots * rpi;
+      break;
+    }
     if (chunk >= (1 << 20)) return false;
     // longer chunks: multiples of kAttnChunk above it (looped in LDS-sized pieces)
     chunk = chunk < kAttnChunk ? std::min(kAttnChunk, chunk * 2) : chunk * 2;
   }
   p.chunk = chunk;
+  p.rpi = rpi;
+  int max_r = 1;
+  for (int b : members) max_r = std::max(max_r, (seqs[b].k + 1) * G);
+  p.comb_rows = std::min(rpi, max_r);
   return true;
 }
 
@@ -684,31 +706,49 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   const int D = c.d_model, F = c.ffn_dim, dh = c.head_dim, qd = c.n_q_heads * dh, kvd = c.n_kv_heads * dh;
   const int G = c.n_q_heads / c.n_kv_heads;
 
-  Plan plan;
-  // query rows per item: 64 (one 4-wave tile set), 128, or 256 (head dim
-  // 128) when a kv head has more, so each key is read once per item
-  int max_rows = 0;
-  for (const SeqMeta& sq : seqs) max_rows = std::max(max_rows, (sq.k + 1) * (c.n_q_heads / c.n_kv_heads));
-  const int rpi = max_rows <= kAttnRows / 2 ? kAttnRows / 2
-                  : (max_rows > kAttnRows && c.head_dim == 128) ? 2 * kAttnRows : kAttnRows;
-  const int comb_rows = std::max(1, std::min(rpi, max_rows));  // rows of the largest combine entry
-  if (!plan_attention(c, *k->hs, seqs, k->attn_min_items, rpi, plan)) return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
+  // Attention row classes: each sequence's (k + 1) * group query rows per kv
+  // head go to items of 64, 128 or 256 rows (256 for head dim 128 only;
+  // longer row sets take several row groups), one launch per class, so a
+  // long draft does not put every short one on the large kernel.
+  static const int kClassRows[3] = {kAttnRows / 2, kAttnRows, 2 * kAttnRows};
+  std::vector<int> members[3];
+  for (int b = 0; b < B; ++b) {
+    const int R = (seqs[b].k + 1) * G;
+    members[R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2].push_back(b);
+  }
+  Plan plans[3];
+  std::vector<AttnItem> items_all, heads_all;
+  std::array<int, 12> attn_key{};
+  size_t part_used = 0;
+  for (int cl = 0; cl < 3; ++cl) {
+    if (members[cl].empty()) continue;
+    Plan& pl = plans[cl];
+    if (!plan_attention(c, *k->hs, seqs, members[cl], k->attn_min_items, kClassRows[cl],
+                        (size_t)kPartSlots * kAttnRows - part_used, pl))
+      return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
+    pl.part_base = part_used;
+    part_used += pl.part_rows;
+    // Pad the grids to buckets (no-op items have k = -1) so the launch
+    // sequence depends only on (rows, sequences, buckets): one cached HIP
+    // graph per such shape.
+    AttnItem none{};
+    none.k = -1;
+    pl.items.resize((pl.items.size() + 63) / 64 * 64, none);
+    pl.heads.resize((pl.heads.size() + 15) / 16 * 16, none);
+    pl.item0 = items_all.size();
+    pl.head0 = heads_all.size();
+    items_all.insert(items_all.end(), pl.items.begin(), pl.items.end());
+    heads_all.insert(heads_all.end(), pl.heads.begin(), pl.heads.end());
+    attn_key[4 * cl] = (int)pl.items.size();
+    attn_key[4 * cl + 1] = (int)pl.heads.size();
+    attn_key[4 * cl + 2] = pl.chunk;
+    attn_key[4 * cl + 3] = pl.comb_rows;
+  }
+  const size_t n_items = items_all.size(), n_heads = heads_all.size();
   std::vector<PageUpdate> upd_raw = k->hs->take_updates();
   // keep the last update of each (slot, index): they are applied in parallel
   std::map<std::pair<int, int>, int> last;
   for (auto& u : upd_raw) last[{u.slot, u.index}] = u.page;
-
-  // Pad the attention grids to buckets (no-op items have k = -1) so the
-  // launch sequence depends only on (rows, sequences, buckets): one cached
-  // HIP graph per such shape.
-  const size_t n_items = (plan.items.size() + 63) / 64 * 64;
-  const size_t n_heads = (plan.heads.size() + 15) / 16 * 16;
-  {
-    AttnItem none{};
-    none.k = -1;
-    plan.items.resize(n_items, none);
-    plan.heads.resize(n_heads, none);
-  }
 
   // pack metadata: header | rows | seqs | items | heads | updates (a
   // device-resident loop adds its static copies after them)
@@ -734,8 +774,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   put(header, 16);
   const size_t o_rows = put(rows.data(), 4 * (size_t)M);
   const size_t o_seqs = put(seqs.data(), sizeof(SeqMeta) / 4 * (size_t)B);
-  const size_t o_items = put(plan.items.data(), sizeof(AttnItem) / 4 * n_items);
-  const size_t o_heads = put(plan.heads.data(), sizeof(AttnItem) / 4 * n_heads);
+  const size_t o_items = put(items_all.data(), sizeof(AttnItem) / 4 * n_items);
+  const size_t o_heads = put(heads_all.data(), sizeof(AttnItem) / 4 * n_heads);
   // tree rows (fixed size per M, before the variable-length updates so every
   // offset a captured graph holds depends on the graph key only)
   off = (off + 7) / 8 * 8;  // 8-byte alignment of the masks
@@ -753,8 +793,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   const size_t o_upd = put(upd.data(), upd.size());
   size_t o_sitems = 0, o_sheads = 0, o_sseqs = 0, o_rowseq = 0, o_pgoff = 0, o_pages = 0, o_rstart = 0;
   if (acap) {
-    o_sitems = put(plan.items.data(), sizeof(AttnItem) / 4 * n_items);
-    o_sheads = put(plan.heads.data(), sizeof(AttnItem) / 4 * n_heads);
+    o_sitems = put(items_all.data(), sizeof(AttnItem) / 4 * n_items);
+    o_sheads = put(heads_all.data(), sizeof(AttnItem) / 4 * n_heads);
     o_sseqs = put(seqs.data(), sizeof(SeqMeta) / 4 * (size_t)B);
     std::vector<int32_t> row_seq(M);
     for (int b = 0; b < B; ++b)
@@ -810,7 +850,6 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     p.heads_static = (const AttnItem*)(meta_dev + o_sheads);
     p.heads = (AttnItem*)(meta_dev + o_heads);
     p.n_heads = (int)n_heads;
-    p.chunk = plan.chunk;
     p.M = M;
     p.B = B;
     HIP_TRY(launch_async_plan(p, s));
@@ -924,8 +963,9 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, !single, s));
     return HVD_OK;
   };
-  double kv_bytes = 0;
-  for (auto& sq : seqs) kv_bytes += (double)(sq.ctx + sq.k + 1) * kvd * 2 * 2;
+  double kv_bytes_cl[3] = {0, 0, 0};  // KV bytes each attention launch reads
+  for (int cl = 0; cl < 3; ++cl)
+    for (int b : members[cl]) kv_bytes_cl[cl] += (double)(seqs[b].ctx + seqs[b].k + 1) * kvd * 2 * 2;
 
   for (int l = 0; l < c.n_layers; ++l) {
     const LayerW& L = m->layers[l];
@@ -968,29 +1008,35 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.Ohi = k->Ohi;
       a.Olo = k->Olo;
       a.MTtot = MT;
-      a.part_o = k->part_o;
-      a.part_ml = k->part_ml;
       a.tree_mask = d_mask;
-      {
-        ProfScope ps(k, PF_ATTN, kv_bytes);
-        HIP_TRY(launch_attn(a, (int)plan.items.size(), plan.chunk, rpi, k->attn_max_np, s));
+      // one launch per row class, then the combine passes
+      for (int cl = 0; cl < 3; ++cl) {
+        const Plan& pl = plans[cl];
+        if (pl.items.empty()) continue;
+        a.items = d_items + pl.item0;
+        a.part_o = k->part_o + pl.part_base * dh;
+        a.part_ml = k->part_ml + pl.part_base * 2;
+        ProfScope ps(k, PF_ATTN, kv_bytes_cl[cl]);
+        HIP_TRY(launch_attn(a, (int)pl.items.size(), pl.chunk, pl.rpi, k->attn_max_np, s));
       }
-      if (!plan.heads.empty()) {
+      for (int cl = 0; cl < 3; ++cl) {
+        const Plan& pl = plans[cl];
+        if (pl.heads.empty()) continue;
         CombineArgs cb{};
-        cb.heads = d_heads;
+        cb.heads = d_heads + pl.head0;
         cb.Hq = c.n_q_heads;
         cb.Hkv = c.n_kv_heads;
         cb.dh = dh;
         cb.group = G;
-        cb.part_o = k->part_o;
-        cb.part_ml = k->part_ml;
+        cb.part_o = k->part_o + pl.part_base * dh;
+        cb.part_ml = k->part_ml + pl.part_base * 2;
         cb.Ohi = k->Ohi;
         cb.Olo = k->Olo;
         cb.MTtot = MT;
-        cb.rpi = rpi;
-        cb.max_rows = comb_rows;
+        cb.rpi = pl.rpi;
+        cb.max_rows = pl.comb_rows;
         ProfScope ps(k, PF_COMBINE, 0.0);
-        HIP_TRY(launch_combine(cb, (int)plan.heads.size(), s));
+        HIP_TRY(launch_combine(cb, (int)pl.heads.size(), s));
       }
     }
     {
@@ -1114,8 +1160,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   if (k->prof || !k->use_graphs) {
     if (hvd_status st = launch_all(); st != HVD_OK) return st;
   } else {
-    const GraphKey key{M, B, (int)n_items, (int)n_heads, plan.chunk, rpi, comb_rows, lm_head ? 1 : 0,
-                       tree ? 1 : 0, logits};
+    const GraphKey key{M, B, lm_head ? 1 : 0, tree ? 1 : 0, attn_key, logits};
     auto it = k->graphs.find(key);
     if (it == k->graphs.end()) {
       if (k->graphs.size() >= kMaxGraphs) {

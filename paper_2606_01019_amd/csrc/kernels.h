@@ -203,13 +203,12 @@ struct AsyncPlanArgs {
   const int32_t* row_seq;    // [M]: sequence of each row
   RowMeta* rows;             // [M] out
   SeqMeta* seqs;             // [B] out
-  const AttnItem* items_static;  // [n_items]: pad1 = sequence, pad2 = the unit's last row index
-  AttnItem* items;
+  const AttnItem* items_static;  // [n_items]: pad1 = sequence, pad2 = the unit's last row index,
+  AttnItem* items;               //   pad3 = its plan's chunk length
   int n_items;
   const AttnItem* heads_static;  // [n_heads], same extra fields
   AttnItem* heads;
   int n_heads;
-  int chunk;
   int M, B;
 };
 

@@ -272,13 +272,13 @@ __global__ __launch_bounds__(512) void async_plan(AsyncPlanArgs a) {
     AttnItem it = head ? a.heads_static[e] : a.items_static[e];
     if (it.k >= 0) {
       const int ctx = a.state[it.pad1];
-      const int nch = (ctx + it.pad2 + 1 + a.chunk - 1) / a.chunk;
+      const int nch = (ctx + it.pad2 + 1 + it.pad3 - 1) / it.pad3;  // pad3: the plan's chunk length
       if (head ? nch == 1 : it.c >= nch) {
         it.k = -1;  // no keys yet (item), or the only chunk writes O itself (combine entry)
       } else {
         it.ctx = ctx;
         it.nch = nch;
-        it.p_end = min(ctx + it.k + 1, it.p_begin + a.chunk);
+        it.p_end = min(ctx + it.k + 1, it.p_begin + it.pad3);
       }
     }
     if (head) a.heads[e] = it;
