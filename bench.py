@@ -591,8 +591,8 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n * 4}))
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the verify step of one "
-              f"sequence batch does not shard across GPUs in this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library runs the verify "
+              f"step of a sequence batch on one GPU and has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
 
     import torch
