@@ -176,8 +176,8 @@ hvd_status hvd_commit(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_
  * possible outcome, ctx_b + max_steps * (k_b + 1) + 1 positions
  * (HVD_ERR_OOM if the pool cannot; HVD_ERR_RANGE past the rotary table), and
  * while the loop is open every other call on these sequences is
- * HVD_ERR_STATE.  Caller-owned DEVICE buffers (int32, kept alive until
- * hvd_async_end):
+ * HVD_ERR_STATE.  The model and KV handles must outlive the loop.
+ * Caller-owned DEVICE buffers (int32, kept alive until hvd_async_end):
  *   drafts  [sum k_b]   draft tokens of step s, packed in batch order; read
  *                       by every step (may be NULL when every k_b = 0).  A
  *                       token outside [0, vocab) is never accepted.
