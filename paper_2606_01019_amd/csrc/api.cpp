@@ -35,7 +35,7 @@ hvd_status set_err(hvd_status s, const std::string& m) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr int kPrefillRows = 256;  // rows per prefill chunk (256 measured 5% above 128 and 512)
+constexpr int kPrefillRows = 512;  // rows per prefill chunk (measured: 512 above 256 and 1024)
 // Up to 8 row tiles (128 rows) the skinny kernel in row blocks of <= 4
 // tiles beats the tiled kernel and its K-split finish (measured: 65-row
 // verifies and 128-row prefill chunks of the 8B shape)
