@@ -3,7 +3,8 @@ paths the tiny decoder does not: 8 q / 2 kv heads of 128 (group 4), rotary
 theta 5e5, weight-streaming GEMMs with 2 and 4 strips per workgroup, the
 pipelined K loop with its tail, the K split with its finish pass (down
 projection, K = 8192), split-KV attention with the combine pass, prefill
-blocks of 64 rows, and 1 to 5 row tiles per verify (k = 0 .. 64)."""
+in 512-row chunks with a ragged tail, 1 to 5 row tiles per verify
+(k = 0 .. 64), and the largest batch a 32-sequence handle takes."""
 
 import numpy as np
 import pytest
