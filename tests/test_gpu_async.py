@@ -263,3 +263,48 @@ def test_async_loop_errors_and_lock(torch_cuda, tiny):
     a, n = kv.verify([0], [ctx_after], [[1, 2]])  # the sequence is back under host control
     kv.commit([0])
     kv.close()
+
+
+def test_async_loop_interleaved_with_host_verifies(torch_cuda, tiny):
+    """A device-resident loop on one sequence while the host verifies and
+    commits another on the same handle between its steps (shared workspace,
+    page-table updates of the other sequence, cached step graphs on): both
+    streams follow the oracle."""
+    torch = torch_cuda
+    import paper_2606_01019_amd as hvd
+    om, gm = tiny
+    V = TINY.vocab
+    kv = hvd.KVCache(gm, max_seqs=2, n_pages=256)
+    kv.set_graphs(True)
+    ctx0 = wt.uniform_context(wt.rng_for("context", 350), 300, V)
+    ctx1 = wt.uniform_context(wt.rng_for("context", 351), 200, V)
+    st0, st1 = oracle.prefill(om, ctx0), oracle.prefill(om, ctx1)
+    kv.prefill(0, ctx0)
+    kv.prefill(1, ctx1)
+    k, steps = 4, 6
+    G = greedy(om, st0, steps * (k + 1) + 1)
+    ref = wt.corrupt_stream(wt.rng_for("draft", 350), G, 0.3, V)
+    loop = kv.async_loop([0], [st0.ctx], [k], steps, ref=torch.tensor(ref[None, :], device="cuda"),
+                         ref_start=[st0.ctx + 1])
+    f0, rep1 = Follow(om), Report()
+    drng = wt.rng_for("draft", 351)
+    for s in range(steps):
+        loop.step(1)
+        # the host-driven sequence, between the loop's steps
+        g = greedy(om, st1, 7)
+        d = wt.plant_chain(drng, g, wt.geometric_accept(drng, 0.4, 6), 6, V)
+        res = oracle.verify(om, st1, d)
+        lg = torch.empty((7, V), dtype=torch.float32, device="cuda")
+        a, n = kv.verify([1], [st1.ctx], [d], logits=lg)
+        kv.commit([1])
+        div = check_step(rep1, res, lg.cpu().numpy().astype(np.float64), int(a[0]), int(n[0]), d)
+        st1 = oracle_commit_as(st1, res, int(a[0]), int(n[0])) if div else oracle.commit(st1, res)
+    assert loop.end() == steps
+    hist = loop.history.cpu().numpy()
+    draft_at = ref_drafter(ref, st0.ctx + 1, k)
+    for s in range(steps):
+        st0 = f0.step(st0, draft_at(st0.ctx), int(hist[s, 0, 0]), int(hist[s, 0, 1]))
+    check_after_loop(torch, om, kv, 0, st0, f0.rep)
+    assert kv.seq_info(1)[:2] == (st1.ctx, st1.pending)
+    print(f"loop: {f0}; host-driven: {rep1}")
+    kv.close()
