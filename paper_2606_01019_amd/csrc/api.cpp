@@ -331,6 +331,7 @@ struct hvd_kv_s {
   int attn_max_np = kItemPages;  // most pages one attention sub-chunk stages
   int skinny_max_mt = kSkinnyMaxMT;   // row tiles above which GEMMs take the MFMA-tiled kernel
   int gemm_force[PF_LM + 1][2] = {};  // per GEMM family: {strips per workgroup, K splits} of the skinny kernel, 0 = policy
+  bool ns8_mt3 = true;  // 8-strip skinny blocks at three single-pass row tiles
   int tiled_force[PF_LM + 1][2] = {};  // per GEMM family: {tile + 1, K splits} of the tiled kernel, 0 = policy
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
@@ -463,6 +464,7 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   if (const char* e = getenv("HVD_ATTN_MAX_NP")) k->attn_max_np = std::max(2, std::min(kItemPages, atoi(e)));
   if (const char* e = getenv("HVD_GRAPHS")) k->use_graphs = atoi(e) != 0;
   if (const char* e = getenv("HVD_SKINNY_MAX_MT")) k->skinny_max_mt = std::max(1, std::min(64, atoi(e)));
+  if (const char* e = getenv("HVD_NS8_MT3")) k->ns8_mt3 = atoi(e) != 0;
   // tuning override of the skinny GEMM shape: "qkv=2:1,o=1:1" (family=strips:splits)
   if (const char* e = getenv("HVD_GEMM_SHAPE")) {
     static const char* names[PF_LM + 1] = {"qkv", "o", "gateup", "down", "lm"};
@@ -927,8 +929,13 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       return HVD_OK;
     }
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
+    // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
+    const bool single = lm_head && MT > 2 &&
+                        ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
     int ns = 4, splits = 1;
-    if (mt_block == 2 && N % 128 == 0 && nb8 >= want) {
+    // 8 strips per workgroup halve the activation fragments per weight byte:
+    // two row tiles, or three on the single-pass activation (LDS bounds it)
+    if ((mt_block == 2 || (mt_block == 3 && single && k->ns8_mt3)) && N % 128 == 0 && nb8 >= want) {
       ns = 8;
     } else if (nb4 >= want) {
       ns = 4;
@@ -957,9 +964,6 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.n_part = lm_parts;
     }
     ProfScope ps(k, family, (double)N * K * 2.0);
-    // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
-    const bool single = lm_head && MT > 2 &&
-                        ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
     HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, !single, s));
     return HVD_OK;
   };

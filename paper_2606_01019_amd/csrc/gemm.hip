@@ -611,7 +611,15 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
     case 2: launch_one<2, NS, EPI, true>(a, splits, mblocks, s); break;
     case 3:
     case 4:
-      if constexpr (NS <= 4) {  // 8-strip blocks only up to 2 row tiles (LDS)
+      if constexpr (NS == 8) {  // 8-strip blocks: 3 row tiles, single pass only (LDS)
+        if constexpr (kSingle) {
+          if (mt == 3 && !hi_lo) {
+            launch_one<3, 8, EPI, false>(a, splits, mblocks, s);
+            break;
+          }
+        }
+        return hipErrorInvalidValue;
+      } else if constexpr (NS <= 4) {
         if (kSingle && !hi_lo) {
           if constexpr (kSingle) {
             if (mt == 3) launch_one<3, NS, EPI, false>(a, splits, mblocks, s);
@@ -623,8 +631,6 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
           launch_one<4, NS, EPI, true>(a, splits, mblocks, s);
         }
         break;
-      } else {
-        return hipErrorInvalidValue;
       }
     default: return hipErrorInvalidValue;
   }
