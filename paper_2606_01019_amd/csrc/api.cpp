@@ -331,7 +331,7 @@ struct hvd_kv_s {
   int attn_max_np = kItemPages;  // most pages one attention sub-chunk stages
   int skinny_max_mt = kSkinnyMaxMT;   // row tiles above which GEMMs take the MFMA-tiled kernel
   int gemm_force[PF_LM + 1][2] = {};  // per GEMM family: {strips per workgroup, K splits} of the skinny kernel, 0 = policy
-  bool ns8_mt3 = true;  // 8-strip skinny blocks at three single-pass row tiles
+  bool ns8_mt3 = true;  // 8-strip skinny blocks at three and four single-pass row tiles
   int tiled_force[PF_LM + 1][2] = {};  // per GEMM family: {tile + 1, K splits} of the tiled kernel, 0 = policy
   float* gemm_part = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
@@ -934,8 +934,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
                         ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
     int ns = 4, splits = 1;
     // 8 strips per workgroup halve the activation fragments per weight byte:
-    // two row tiles, or three on the single-pass activation (LDS bounds it)
-    if ((mt_block == 2 || (mt_block == 3 && single && k->ns8_mt3)) && N % 128 == 0 && nb8 >= want) {
+    // two row tiles, or three and four on the single-pass activation
+    if ((mt_block == 2 || (mt_block >= 3 && single && k->ns8_mt3)) && N % 128 == 0 && nb8 >= want) {
       ns = 8;
     } else if (nb4 >= want) {
       ns = 4;

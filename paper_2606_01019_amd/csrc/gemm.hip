@@ -402,7 +402,11 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   constexpr int ROWS = MT * 16;
   constexpr int COLS = NS * 16;
 
-  __shared__ float red[4][NS][MT][256];
+  // the cross-wave reduction takes NH passes over the strips (two for 8
+  // strips x 4 row tiles, whose full buffer would not fit the LDS)
+  constexpr int NH = (NS == 8 && MT == 4) ? 2 : 1;
+  constexpr int NSH = NS / NH;
+  __shared__ float red[4][NSH][MT][256];
   __shared__ float tile[ROWS][COLS + 1];
   __shared__ EpiPre<MT, NS, EPI> pre;
 
@@ -506,31 +510,36 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   if constexpr (!EpiRegs<MT, NS, EPI>::EARLY_ROPE) epi_issue_rope<MT, NS, EPI>(a, er, cb);
   epi_commit_rope<MT, NS, EPI>(a, er, pre, mt0, mcount);
 
-  // ---- reduce the 8 K ranges through LDS in two rounds (fixed order)
-  if (wave >= 4) {
+  // ---- reduce the 8 K ranges through LDS in two rounds (fixed order), in
+  // NH passes over the strips
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+  for (int h = 0; h < NH; ++h) {
+    if (h) __syncthreads();  // the previous pass has read red
+    if (wave >= 4) {
 #pragma unroll
-      for (int n = 0; n < NS; ++n)
+      for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) red[wave - 4][n][m][lane * 4 + i] = acc[m][n][i];
-  }
-  __syncthreads();
-  if (wave < 4) {
+        for (int n = 0; n < NSH; ++n)
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+          for (int i = 0; i < 4; ++i) red[wave - 4][n][m][lane * 4 + i] = acc[m][h * NSH + n][i];
+    }
+    __syncthreads();
+    if (wave < 4) {
 #pragma unroll
-      for (int n = 0; n < NS; ++n)
+      for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) red[wave][n][m][lane * 4 + i] += acc[m][n][i];
-  }
-  __syncthreads();
-  for (int e = tid; e < NS * MT * 256; e += 512) {
-    const int n = e / (MT * 256), rem = e % (MT * 256);
-    const int m = rem / 256, li = rem % 256;
-    const int ln = li >> 2, i = li & 3;
-    const float v = (red[0][n][m][li] + red[1][n][m][li]) + (red[2][n][m][li] + red[3][n][m][li]);
-    tile[m * 16 + (ln >> 4) * 4 + i][n * 16 + (ln & 15)] = v;
+        for (int n = 0; n < NSH; ++n)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) red[wave][n][m][lane * 4 + i] += acc[m][h * NSH + n][i];
+    }
+    __syncthreads();
+    for (int e = tid; e < NSH * MT * 256; e += 512) {
+      const int n = e / (MT * 256), rem = e % (MT * 256);
+      const int m = rem / 256, li = rem % 256;
+      const int ln = li >> 2, i = li & 3;
+      const float v = (red[0][n][m][li] + red[1][n][m][li]) + (red[2][n][m][li] + red[3][n][m][li]);
+      tile[m * 16 + (ln >> 4) * 4 + i][(h * NSH + n) * 16 + (ln & 15)] = v;
+    }
   }
   __syncthreads();
 
@@ -611,10 +620,11 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
     case 2: launch_one<2, NS, EPI, true>(a, splits, mblocks, s); break;
     case 3:
     case 4:
-      if constexpr (NS == 8) {  // 8-strip blocks: 3 row tiles, single pass only (LDS)
+      if constexpr (NS == 8) {  // 8-strip blocks at 3-4 row tiles: single pass only (LDS)
         if constexpr (kSingle) {
-          if (mt == 3 && !hi_lo) {
-            launch_one<3, 8, EPI, false>(a, splits, mblocks, s);
+          if (!hi_lo) {
+            if (mt == 3) launch_one<3, 8, EPI, false>(a, splits, mblocks, s);
+            else launch_one<4, 8, EPI, false>(a, splits, mblocks, s);
             break;
           }
         }
