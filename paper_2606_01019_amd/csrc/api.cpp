@@ -35,7 +35,16 @@ hvd_status set_err(hvd_status s, const std::string& m) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr int kPrefillRows = 512;  // rows per prefill chunk (measured: 512 above 256 and 1024)
+// Prefill chunk: rows whose query rows per kv head (rows x group) come to
+// 2048, between 128 and 512 rows (measured: 512 rows for the 8B shape,
+// group 4, above 256 and 1024; 256 for the 32B shape, group 8, above 512).
+// HVD_PREFILL_ROWS overrides it for sweeps.
+int prefill_rows(const hvd_config& c) {
+  static const int forced = getenv("HVD_PREFILL_ROWS") ? atoi(getenv("HVD_PREFILL_ROWS")) : 0;
+  if (forced >= 16) return forced / 16 * 16;
+  const int G = c.n_q_heads / c.n_kv_heads;
+  return std::max(128, std::min(512, 2048 / G));
+}
 // Up to 8 row tiles (128 rows) the skinny kernel in row blocks of <= 4
 // tiles beats the tiled kernel and its K-split finish (measured: 65-row
 // verifies and 128-row prefill chunks of the 8B shape)
@@ -361,7 +370,7 @@ namespace {
 size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int pt_stride) {
   const int G = c.n_q_heads / c.n_kv_heads;
   const size_t rg_verify = ((size_t)(c.max_draft + 1) * G + kAttnRows - 1) / kAttnRows;
-  const size_t rg_prefill = ((size_t)kPrefillRows * G + kAttnRows - 1) / kAttnRows;
+  const size_t rg_prefill = ((size_t)prefill_rows(c) * G + kAttnRows - 1) / kAttnRows;
   const size_t units = std::max((size_t)max_seqs * rg_verify, rg_prefill) * c.n_kv_heads;
   // items <= units + partial slots (at most 2 kPartSlots: 64-row items) and
   // heads <= units, each of the three row classes padded up (to 64 and 16
@@ -379,7 +388,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->pool = cv.take<_Float16>(k->layer_stride * c.n_layers);
   k->pt_stride = (c.max_pos + kPage) / kPage + 1;
   k->pt = cv.take<int32_t>((size_t)max_seqs * k->pt_stride);
-  k->max_rows = std::max(max_seqs * (c.max_draft + 1), kPrefillRows);
+  k->max_rows = std::max(max_seqs * (c.max_draft + 1), prefill_rows(c));
   k->MTmax = (k->max_rows + 15) / 16;
   const size_t Mp = (size_t)k->MTmax * 16;
   k->X = cv.take<float>(Mp * D);
@@ -1208,8 +1217,9 @@ extern "C" hvd_status hvd_prefill(hvd_model m, hvd_kv k, int32_t seq_id, const i
   if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
   if (hvd_status st = from_host(k->hs->begin_prefill(seq_id, tokens, n), k); st != HVD_OK) return st;
   const int body = n - 1;
-  for (int s0 = 0; s0 < body; s0 += kPrefillRows) {
-    const int cnt = std::min(kPrefillRows, body - s0);
+  const int chunk_rows = prefill_rows(m->cfg);
+  for (int s0 = 0; s0 < body; s0 += chunk_rows) {
+    const int cnt = std::min(chunk_rows, body - s0);
     std::vector<SeqMeta> seqs{{seq_id, s0, cnt - 1, 0}};
     std::vector<RowMeta> rows(cnt);
     for (int i = 0; i < cnt; ++i) rows[i] = {tokens[s0 + i], seq_id, s0 + i, s0 + i};
