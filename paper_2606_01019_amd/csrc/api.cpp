@@ -602,13 +602,13 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
                     const std::vector<int>& members, int min_items, int rpi, size_t part_rows_free, Plan& p) {
   const int G = c.n_q_heads / c.n_kv_heads;
   struct Unit { int b, g, rg, keys; };
-  auto item = [&](const Unit& u, int c, int nch, int part, int chunk) {
+  auto item = [&](const Unit& u, int ci, int nch, int part, int chunk) {
     const SeqMeta& s = seqs[u.b];
     AttnItem it{};
     it.slot = s.slot; it.ctx = s.ctx; it.k = s.k; it.cu = s.cu; it.tree = s.tree;
-    it.g = u.g; it.c = c; it.nch = nch; it.rg = u.rg; it.part = part;
-    it.p_begin = c * chunk;
-    it.p_end = std::min(s.ctx + s.k + 1, (c + 1) * chunk);
+    it.g = u.g; it.c = ci; it.nch = nch; it.rg = u.rg; it.part = part;
+    it.p_begin = ci * chunk;
+    it.p_end = std::min(s.ctx + s.k + 1, (ci + 1) * chunk);
     it.pad1 = u.b;                // for a device-side re-plan at another ctx:
     it.pad2 = u.keys - s.ctx - 1;  // sequence, last row index of the unit,
     it.pad3 = chunk;               // chunk length
@@ -641,8 +641,9 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   // one item of 128 or 256 rows (8 waves) -- with at least 64 positions for
   // 64-row items and at most 1024 (128-row) or 512 (256-row).  Longer
   // chunks loop over LDS-sized sub-chunks.  Measured: 32 sequences of mixed
-  // drafts 34.2 -> 34.0 ms per step; context 16384 at k = 16 / 64 from
-  // 4.97 / 9.05 to 4.69 / 8.65 ms (chunks of at most 256 before)
+  // drafts 34.2 -> 33.2 ms per step; context 16384 at k = 16 / 64 from
+  // 4.98 / 9.04 to 4.71 / 8.70 ms (chunks of at most 256 before); more
+  // workgroups per CU (384 or 512 targets) measured slower
   const int per_cu = rpi <= kAttnRows / 2 ? 2 : 1;
   const int64_t want = (total_keys + (int64_t)min_items * per_cu - 1) / ((int64_t)min_items * per_cu);
   const int cap = rpi <= kAttnRows / 2 ? (1 << 20) : rpi <= kAttnRows ? 1024 : 512;
