@@ -58,6 +58,12 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
   constexpr int LPP = 4 * DH / NT;      // 16-byte loads per thread per page (K and V: 4*DH units)
   static_assert(NP >= 2 && NP <= kItemPages && (NP & (NP - 1)) == 0, "pages per sub-chunk");
   static_assert(LPP >= 1 && LPP * NT == 4 * DH, "page units per thread");
+  // Sub-chunks of up to 4 pages are double-buffered in LDS: a sub-chunk is
+  // staged into the buffer its predecessor's predecessor used, which every
+  // wave has finished reading once it passed the previous staging barrier,
+  // so one barrier per sub-chunk suffices.
+  constexpr bool DB = NP <= 4;
+  constexpr int BUF_BYTES = CH * DH * 2 * 2;       // K and V of one sub-chunk
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16* sK = (_Float16*)smem;                  // [CH][DH], segment-swizzled
   _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], 8-byte-unit-swizzled
@@ -147,9 +153,16 @@ __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_at
   // wait for the next sub-chunk's loads.
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 
+  int nbuf = 0;
   for (int sub = p_begin; sub < p_end; sub += CH) {
     const int n_pos = min(CH, p_end - sub);
-    if (sub != p_begin) __syncthreads();  // previous sub-chunk fully consumed
+    if constexpr (DB) {
+      sK = (_Float16*)(smem + nbuf * BUF_BYTES);
+      sV = (_Float16*)(smem + nbuf * BUF_BYTES + CH * DH * 2);
+      nbuf ^= 1;
+    } else {
+      if (sub != p_begin) __syncthreads();  // previous sub-chunk fully consumed
+    }
 #pragma unroll
     for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -437,7 +450,8 @@ int attn_pages_per_sub(int chunk) {
   return np;
 }
 
-size_t attn_lds_bytes(int dh, int np) { return (size_t)np * kPage * dh * 2 * 2; }
+// K and V of one sub-chunk, twice for the double-buffered sub-chunks (<= 4 pages)
+size_t attn_lds_bytes(int dh, int np) { return (size_t)np * kPage * dh * 2 * 2 * (np <= 4 ? 2 : 1); }
 
 template <int DH, int NW, int TPW>
 static hipError_t launch_attn_dh(const AttnArgs& a, int n_items, int np, hipStream_t s) {
