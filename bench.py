@@ -313,21 +313,39 @@ def leg_hvd_loop(model, reps):
     ref, t_greedy = greedy(1, prompt, n_new)
     res = {"greedy": {"cycles_per_1k": 1000.0, "tokens_per_s": n_new / t_greedy}}
     always = lambda phi: np.full(len(phi), np.inf)
+    same = lambda x, y: int(next((i for i, (a, b) in enumerate(zip(x, y)) if a != b), min(len(x), len(y))))
+
+    # The retried request's cache holds the response an earlier run of the same
+    # decoder gave: starting from the greedy stream, rerun the retry until its
+    # output repeats (a near tie that a long verify resolves differently from a
+    # one-row step changes the response once, then it is stable)
+    earlier, rounds = ref, 0
+    while rounds < 4:
+        dec = hl.HybridVerifiedDecoder(kv, 0, g, warmup_streams=[list(prompt) + earlier])
+        out, _ = dec.generate(prompt, n_new)
+        kv.seq_free(0)
+        rounds += 1
+        if out == earlier:
+            break
+        earlier = out
     for name, pred, warm in (("fresh_suffix_cache_always", always, []), ("fresh_hvd", g, []),
-                             ("retry_suffix_cache_always", always, [list(prompt) + ref]),
-                             ("retry_hvd", g, [list(prompt) + ref])):
+                             ("retry_suffix_cache_always", always, [list(prompt) + earlier]),
+                             ("retry_hvd", g, [list(prompt) + earlier])):
         dec = hl.HybridVerifiedDecoder(kv, 0, pred, warmup_streams=warm)
         out, st = dec.generate(prompt, n_new)
         kv.seq_free(0)
         res[name] = {"cycles_per_1k": st.cycles_per_1k, "tokens_per_s": st.generated / st.decode_s,
                      "cache_verifies": st.cache_steps,
                      "mean_cache_accepted": float(np.mean(st.cache_accepted)) if st.cache_accepted else 0.0,
-                     "tokens_equal_to_greedy": int(next((i for i, (a, b) in enumerate(zip(out, ref)) if a != b),
-                                                        len(ref)))}
+                     "tokens_equal_to_greedy": same(out, ref)}
+        if warm:
+            res[name]["tokens_equal_to_earlier_response"] = same(out, earlier)
+    res["earlier_response"] = {"reruns": rounds, "tokens_equal_to_greedy": same(earlier, ref)}
     kv.close()
     res["workload"] = (f"8B shape, batch 1, agentic-style prompt of {n} tokens, {n_new} new tokens, verifies with "
                        f"fp16 hi+lo activations at every row count; fresh: empty "
-                       f"cache warmup; retry: the cache holds an identical earlier request; payoff MLP trained on "
+                       f"cache warmup; retry: the cache holds the decoder's own response to the same request from an "
+                       f"earlier run; payoff MLP trained on "
                        f"{len(y)} replayed cache drafts of another request")
     res["retry_speedup_vs_greedy"] = res["retry_hvd"]["tokens_per_s"] / res["greedy"]["tokens_per_s"]
     return res
