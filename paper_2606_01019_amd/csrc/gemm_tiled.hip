@@ -81,12 +81,35 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
   const int wave = threadIdx.x >> 6;
   const int wy = wave / WX, wx = wave % WX;
   const int lhi = lane >> 5, lc = lane & 31;
+  // Residual inputs are read one group of 4 rows ahead of the stores, and the
+  // gains once: a load issued after a store waits for that store before its
+  // value can be used.
+  constexpr bool XR = EPI == EPI_RESID;
+  float xq[2][XR ? 4 : 1][XR ? WN : 1];
+  auto load_x = [&](int g, float (&dst)[XR ? 4 : 1][XR ? WN : 1]) {
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int R = row_w + 32 * (g >> 2) + 8 * (g & 3) + 4 * lhi + rr;
+#pragma unroll
+      for (int j = 0; j < WN; ++j) dst[rr][j] = R < a.M ? a.X[(size_t)R * a.D + col_w + 32 * j + lc] : 0.f;
+    }
+  };
+  float gn[XR ? WN : 1];  // next layer's norm gain at this lane's columns
+  if constexpr (XR) {
+#pragma unroll
+    for (int j = 0; j < WN; ++j) gn[j] = a.gain_next[col_w + 32 * j + lc];
+    load_x(0, xq[0]);
+  }
 #pragma unroll
   for (int i = 0; i < WM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int R = row_w + 32 * i + 8 * (r >> 2) + 4 * lhi + (r & 3);
       const bool rok = R < a.M;
+      if constexpr (XR) {
+        const int g = 4 * i + (r >> 2);
+        if ((r & 3) == 0 && g + 1 < 4 * WM) load_x(g + 1, xq[(g + 1) & 1]);
+      }
       const float ir = (EPI != EPI_RESID && rok) ? inv_rms[R] : 1.f;
       if constexpr (EPI == EPI_QKV) {
         RowMeta rm{0, 0, 0, 0};
@@ -127,11 +150,10 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
           const int C = col_w + 32 * j + lc;
           float x = 0.f;
           if (rok) {
-            float* xp = a.X + (size_t)R * a.D + C;
-            x = *xp + acc[i][j][r];
-            *xp = x;
+            x = xq[(r >> 2) & 1][r & 3][j] + acc[i][j][r];
+            a.X[(size_t)R * a.D + C] = x;
             uint16_t hi, lo;
-            split_f16(x * a.gain_next[C], hi, lo);
+            split_f16(x * gn[j], hi, lo);
             const size_t off = afrag_off(R, C, a.MTtot);
             a.Nhi[off] = hi;
             a.Nlo[off] = lo;
