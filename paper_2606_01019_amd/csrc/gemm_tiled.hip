@@ -27,6 +27,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace hvd {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -71,6 +73,14 @@ __device__ __forceinline__ TileCoord tile_coord(int id, int total, int RB, int C
   return t;
 }
 
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 // Epilogue on the accumulators of one wave.  rows/cols are global indices of
 // the wave's sub-tile origin.  inv_rms: per-row inverse RMS (NORM GEMMs).
 template <int WY, int WX, int WM, int WN, int EPI>
@@ -100,21 +110,64 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
     for (int j = 0; j < WN; ++j) gn[j] = a.gain_next[col_w + 32 * j + lc];
     load_x(0, xq[0]);
   }
+  // Per-row inputs (inverse RMS; position and KV slot for QKV): lane lc reads
+  // row lc of each 32-row tile once, and the rows are handed out by shuffles.
+  constexpr bool RQ = EPI == EPI_QKV;
+  float irl[WM];
+  int posl[RQ ? WM : 1], kvsl[RQ ? WM : 1];
 #pragma unroll
   for (int i = 0; i < WM; ++i) {
+    const int R = row_w + 32 * i + lc;
+    const bool ok = R < a.M;
+    irl[i] = (EPI != EPI_RESID && ok) ? inv_rms[R] : 1.f;
+    if constexpr (RQ) {
+      posl[i] = ok ? a.rows[R].pos : 0;
+      kvsl[i] = ok ? a.rows[R].kvs : 0;
+    }
+  }
+  // QKV: rotary (cos, sin) pairs one group of 4 rows ahead of the stores.
+  // Wider wave tiles read them at the store instead: with the prefetch the
+  // row-tile loop is no longer unrolled and the accumulators go to scratch.
+  constexpr bool PCS = RQ && WN <= 2;
+  float2 csq[2][PCS ? 4 : 1][PCS ? WN : 1];
+  auto load_cs = [&](int g, float2 (&dst)[PCS ? 4 : 1][PCS ? WN : 1]) {
+    const int half = a.dh >> 1;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int t = 8 * (g & 3) + 4 * lhi + rr;
+      const int pos = __shfl(posl[g >> 2], t);
+      const bool rok = row_w + 32 * (g >> 2) + t < a.M;
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int C = col_w + 32 * j + lc;
+        dst[rr][j] = float2{1.f, 0.f};
+        if (rok && C < a.q_cols + a.kv_cols) {
+          const int base = C < a.q_cols ? 0 : a.q_cols;
+          dst[rr][j] = a.rope[(size_t)pos * half + (((C - base) % a.dh) >> 1)];
+        }
+      }
+    }
+  };
+  if constexpr (PCS) load_cs(0, csq[0]);
+  // the row-tile index is a compile-time constant, so the accumulators are
+  // never indexed at run time (a rolled loop would move them to scratch)
+  static_for<0, WM>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int R = row_w + 32 * i + 8 * (r >> 2) + 4 * lhi + (r & 3);
       const bool rok = R < a.M;
+      const int t = 8 * (r >> 2) + 4 * lhi + (r & 3);  // row within the 32-row tile
+      const int g = 4 * i + (r >> 2);
       if constexpr (XR) {
-        const int g = 4 * i + (r >> 2);
         if ((r & 3) == 0 && g + 1 < 4 * WM) load_x(g + 1, xq[(g + 1) & 1]);
       }
-      const float ir = (EPI != EPI_RESID && rok) ? inv_rms[R] : 1.f;
+      if constexpr (PCS) {
+        if ((r & 3) == 0 && g + 1 < 4 * WM) load_cs(g + 1, csq[(g + 1) & 1]);
+      }
+      const float ir = __shfl(irl[i], t);
       if constexpr (EPI == EPI_QKV) {
-        RowMeta rm{0, 0, 0, 0};
-        if (rok) rm = a.rows[R];
-        const int half = a.dh >> 1;
+        const int kvs = __shfl(kvsl[i], t);
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
           const int C = col_w + 32 * j + lc;
@@ -125,23 +178,28 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
             if ((C & 1) == 0) {
               const int base = C < a.q_cols ? 0 : a.q_cols;
               const int dp = (C - base) % a.dh;
-              const float2 cs = a.rope[(size_t)rm.pos * half + (dp >> 1)];
+              float2 cs;
+              if constexpr (PCS) {
+                cs = csq[(r >> 2) & 1][r & 3][j];
+              } else {
+                cs = a.rope[(size_t)__shfl(posl[i], t) * (a.dh >> 1) + (dp >> 1)];
+              }
               const float o0 = v * cs.x - pv * cs.y;
               const float o1 = pv * cs.x + v * cs.y;
               const uint32_t packed = (uint32_t)f2h(o0) | ((uint32_t)f2h(o1) << 16);
               if (C < a.q_cols) {
                 *(uint32_t*)(a.Q + (size_t)R * a.q_cols + C) = packed;
               } else {
-                const int g = (C - base) / a.dh;
-                *(uint32_t*)(a.kv + (size_t)(rm.kvs / kPage) * a.page_stride +
-                             ((size_t)g * kPage + (rm.kvs & (kPage - 1))) * a.dh + dp) = packed;
+                const int hg = (C - base) / a.dh;
+                *(uint32_t*)(a.kv + (size_t)(kvs / kPage) * a.page_stride +
+                             ((size_t)hg * kPage + (kvs & (kPage - 1))) * a.dh + dp) = packed;
               }
             }
           } else {
             const int cv = C - a.q_cols - a.kv_cols;
-            const int g = cv / a.dh, d = cv % a.dh;
-            a.kv[(size_t)(rm.kvs / kPage) * a.page_stride + (size_t)a.Hkv * kPage * a.dh +
-                 ((size_t)g * a.dh + d) * kPage + (rm.kvs & (kPage - 1))] = (_Float16)v;
+            const int hg = cv / a.dh, d = cv % a.dh;
+            a.kv[(size_t)(kvs / kPage) * a.page_stride + (size_t)a.Hkv * kPage * a.dh +
+                 ((size_t)hg * a.dh + d) * kPage + (kvs & (kPage - 1))] = (_Float16)v;
           }
         }
       } else if constexpr (EPI == EPI_RESID) {
@@ -212,7 +270,7 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
         }
       }
     }
-  }
+  });
   if constexpr (EPI == EPI_LM) {
     __syncthreads();
     // merge the column parts (lower columns first) and publish
