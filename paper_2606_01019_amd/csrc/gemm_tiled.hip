@@ -167,7 +167,10 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
       }
       const float ir = __shfl(irl[i], t);
       if constexpr (EPI == EPI_QKV) {
+        // shuffles run on every lane: a shuffle under the branches below would
+        // read lanes that are switched off
         const int kvs = __shfl(kvsl[i], t);
+        const int pos = PCS ? 0 : __shfl(posl[i], t);
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
           const int C = col_w + 32 * j + lc;
@@ -182,7 +185,7 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
               if constexpr (PCS) {
                 cs = csq[(r >> 2) & 1][r & 3][j];
               } else {
-                cs = a.rope[(size_t)__shfl(posl[i], t) * (a.dh >> 1) + (dp >> 1)];
+                cs = a.rope[(size_t)pos * (a.dh >> 1) + (dp >> 1)];
               }
               const float o0 = v * cs.x - pv * cs.y;
               const float o1 = pv * cs.x + v * cs.y;
