@@ -126,8 +126,8 @@ __device__ __forceinline__ void tiled_epilogue(const GemmArgs& a, const f32x16 (
     }
   }
   // QKV: rotary (cos, sin) pairs one group of 4 rows ahead of the stores.
-  // Wider wave tiles read them at the store instead: with the prefetch the
-  // row-tile loop is no longer unrolled and the accumulators go to scratch.
+  // Wave tiles of 128 columns read them at the store instead: two groups of
+  // pairs would take 64 more registers beside 128 or 256 accumulators.
   constexpr bool PCS = RQ && WN <= 2;
   float2 csq[2][PCS ? 4 : 1][PCS ? WN : 1];
   auto load_cs = [&](int g, float2 (&dst)[PCS ? 4 : 1][PCS ? WN : 1]) {
