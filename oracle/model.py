@@ -51,6 +51,10 @@ class OracleModel:
             self._conv[name] = arr
         return arr
 
+    def linear(self, h: np.ndarray, name: str) -> np.ndarray:
+        """h @ W^T for the [out, in] weight ``name`` (a plain matrix product)."""
+        return h @ self.w(name).T
+
 
 # ------------------------------------------------------------------ layers
 
@@ -119,23 +123,23 @@ def forward(model: OracleModel, K_cache, V_cache, tokens, positions, want_logits
     for l in range(c.n_layers):
         p = f"layers.{l}."
         h = rms_norm(x, model.w(p + "attn_norm"), c.rms_eps)
-        q = (h @ model.w(p + "wq").T).reshape(n, c.n_q_heads, c.head_dim)
-        k = (h @ model.w(p + "wk").T).reshape(n, c.n_kv_heads, c.head_dim)
-        v = (h @ model.w(p + "wv").T).reshape(n, c.n_kv_heads, c.head_dim)
+        q = model.linear(h, p + "wq").reshape(n, c.n_q_heads, c.head_dim)
+        k = model.linear(h, p + "wk").reshape(n, c.n_kv_heads, c.head_dim)
+        v = model.linear(h, p + "wv").reshape(n, c.n_kv_heads, c.head_dim)
         q = rotary(q, positions, c.rope_theta)
         k = rotary(k, positions, c.rope_theta)
         Kc = k if K_cache is None or K_cache[l] is None else np.concatenate([K_cache[l], k], axis=0)
         Vc = v if V_cache is None or V_cache[l] is None else np.concatenate([V_cache[l], v], axis=0)
         o = attend(q, Kc, Vc, positions).reshape(n, c.q_dim)
-        x = x + o @ model.w(p + "wo").T
+        x = x + model.linear(o, p + "wo")
         h2 = rms_norm(x, model.w(p + "mlp_norm"), c.rms_eps)
-        a = silu(h2 @ model.w(p + "wg").T) * (h2 @ model.w(p + "wu").T)
-        x = x + a @ model.w(p + "wd").T
+        a = silu(model.linear(h2, p + "wg")) * model.linear(h2, p + "wu")
+        x = x + model.linear(a, p + "wd")
         new_k.append(k)
         new_v.append(v)
     logits = None
     if want_logits:
-        logits = rms_norm(x, model.w("final_norm"), c.rms_eps) @ model.w("lm_head").T
+        logits = model.linear(rms_norm(x, model.w("final_norm"), c.rms_eps), "lm_head")
     return logits, new_k, new_v
 
 
@@ -333,21 +337,21 @@ def forward_tree(model: OracleModel, K_cache, V_cache, tokens, positions, row_al
     for l in range(c.n_layers):
         p = f"layers.{l}."
         h = rms_norm(x, model.w(p + "attn_norm"), c.rms_eps)
-        q = (h @ model.w(p + "wq").T).reshape(n, c.n_q_heads, c.head_dim)
-        k = (h @ model.w(p + "wk").T).reshape(n, c.n_kv_heads, c.head_dim)
-        v = (h @ model.w(p + "wv").T).reshape(n, c.n_kv_heads, c.head_dim)
+        q = model.linear(h, p + "wq").reshape(n, c.n_q_heads, c.head_dim)
+        k = model.linear(h, p + "wk").reshape(n, c.n_kv_heads, c.head_dim)
+        v = model.linear(h, p + "wv").reshape(n, c.n_kv_heads, c.head_dim)
         q = rotary(q, positions, c.rope_theta)
         k = rotary(k, positions, c.rope_theta)
         Kc = k if ctx == 0 else np.concatenate([K_cache[l], k], axis=0)
         Vc = v if ctx == 0 else np.concatenate([V_cache[l], v], axis=0)
         o = attend_masked(q, Kc, Vc, allowed).reshape(n, c.q_dim)
-        x = x + o @ model.w(p + "wo").T
+        x = x + model.linear(o, p + "wo")
         h2 = rms_norm(x, model.w(p + "mlp_norm"), c.rms_eps)
-        a = silu(h2 @ model.w(p + "wg").T) * (h2 @ model.w(p + "wu").T)
-        x = x + a @ model.w(p + "wd").T
+        a = silu(model.linear(h2, p + "wg")) * model.linear(h2, p + "wu")
+        x = x + model.linear(a, p + "wd")
         new_k.append(k)
         new_v.append(v)
-    logits = rms_norm(x, model.w("final_norm"), c.rms_eps) @ model.w("lm_head").T
+    logits = model.linear(rms_norm(x, model.w("final_norm"), c.rms_eps), "lm_head")
     return logits, new_k, new_v
 
 

@@ -11,7 +11,7 @@ The 8B- and 32B-shaped references use the oracle in float32 (the float64
 path of the same code would need twice the memory and time); a reduced-depth
 pin (tests/test_oracle_precision.py) bounds the float32/float64 difference.
 
-Usage: python tests/golden/make_golden.py cfg2 [cfg3 cfg4 cfg5 tree2]
+Usage: python tests/golden/make_golden.py cfg2 [cfg3 cfg4 cfg5 tree2 cfg5_full] [--spill DIR]
 """
 
 import json
@@ -238,9 +238,151 @@ def case_tree2():
             "oracle_dtype": "float32"}
 
 
+# ---------------------------------------------------------------- full depth
+
+FULL_ROW_STEP = 2.0 ** -11  # logits stored as int16 multiples of this (|error| <= 2.5e-4)
+
+
+def quantize_rows(rows):
+    """Full logit rows stored compactly: int16 multiples of FULL_ROW_STEP
+    (range +-16; the script refuses logits outside it)."""
+    rows = np.asarray(rows, dtype=np.float64)
+    assert np.abs(rows).max() < 32767 * FULL_ROW_STEP, "logit outside the stored range"
+    return np.round(rows / FULL_ROW_STEP).astype(np.int16)
+
+
+class SpillStore:
+    """Canonical tensors (bf16 bits) of a model too large for the host's
+    memory: the norms, embedding, LM head and the first ``resident`` layers
+    stay in memory; the other layers' matrices go once to raw files in
+    ``spill_dir`` and are read back on every use (or, without a directory,
+    are re-drawn from their seeds on every use)."""
+
+    def __init__(self, cfg, resident, spill_dir=None, seed=42):
+        from concurrent.futures import ThreadPoolExecutor
+        from workloads.weights import canonical_tensors, default_threads, make_tensor
+        self.cfg, self.seed, self.spill_dir = cfg, seed, spill_dir
+        self.mem, self.files = {}, {}
+        self._make = make_tensor
+        self._pool = ThreadPoolExecutor(max_workers=default_threads())
+        for name, shape, layer, kind in canonical_tensors(cfg):
+            if layer < resident or kind == "norm":
+                self.mem[name] = make_tensor(cfg, name, seed=seed, pool=self._pool)
+                continue
+            if spill_dir is None:
+                self.files[name] = (None, shape)
+                continue
+            path = os.path.join(spill_dir, f"{cfg.name}.{name}.bf16")
+            nbytes = int(np.prod(shape)) * 2
+            if not (os.path.exists(path) and os.path.getsize(path) == nbytes):
+                make_tensor(cfg, name, seed=seed, pool=self._pool).tofile(path + ".tmp")
+                os.replace(path + ".tmp", path)
+            self.files[name] = (path, shape)
+        log(f"{cfg.name}: {len(self.mem)} tensors in memory, {len(self.files)} streamed")
+
+    def __getitem__(self, name):
+        if name in self.mem:
+            return self.mem[name]
+        path, shape = self.files[name]
+        if path is None:
+            return self._make(self.cfg, name, seed=self.seed, pool=self._pool)
+        return np.fromfile(path, dtype=np.uint16).reshape(shape)
+
+    def keys(self):
+        return list(self.mem) + list(self.files)
+
+
+def _save_progress(ckpt, b, st, steps, rows):
+    tmp = f"{ckpt}/cfg5f_seq{b}"
+    np.save(tmp + "_K.npy.tmp.npy", np.stack(st.K))
+    np.save(tmp + "_V.npy.tmp.npy", np.stack(st.V))
+    np.savez(tmp + "_rows.tmp.npz", **rows)
+    with open(tmp + ".json.tmp", "w") as f:
+        json.dump({"tokens": [int(t) for t in st.tokens], "steps": steps}, f)
+    os.replace(tmp + "_K.npy.tmp.npy", tmp + "_K.npy")
+    os.replace(tmp + "_V.npy.tmp.npy", tmp + "_V.npy")
+    os.replace(tmp + "_rows.tmp.npz", tmp + "_rows.npz")
+    os.replace(tmp + ".json.tmp", tmp + ".json")
+
+
+def _load_progress(ckpt, b):
+    from oracle.model import SeqState
+    base = f"{ckpt}/cfg5f_seq{b}"
+    if ckpt is None or not os.path.exists(base + ".json"):
+        return None
+    with open(base + ".json") as f:
+        meta = json.load(f)
+    K, V = np.load(base + "_K.npy"), np.load(base + "_V.npy")
+    rows = dict(np.load(base + "_rows.npz"))
+    st = SeqState(tokens=meta["tokens"], K=[K[l] for l in range(K.shape[0])], V=[V[l] for l in range(V.shape[0])])
+    return st, meta["steps"], rows
+
+
+CFG5F_SEQS = (0, 1)
+
+
+def case_cfg5_full(spill=None, n_steps=4, resident=38):
+    """Workload 5 at its full depth (64 layers of the 32B shape): sequences 0
+    and 1 over the first n_steps verify + commit steps, from a float32
+    oracle that streams the weights (oracle/streamed.py).  Besides the
+    compact record, rows 0 and k of every verify are kept whole (int16
+    multiples of FULL_ROW_STEP) in cfg5_full_rows.npz."""
+    from oracle.streamed import StreamedOracleModel
+    cfg = SHAPE_32B
+    plans = batches.multistep_plan()
+    store = SpillStore(cfg, resident, spill)
+    m = StreamedOracleModel(cfg, store)
+    ids = sample_ids(cfg.vocab)
+    out, all_rows = [], {}
+    for b in CFG5F_SEQS:
+        ctx = batches.multistep_context(b, 8192, cfg.vocab)
+        got = _load_progress(spill, b)
+        if got is None:
+            log(f"cfg5_full: seq {b} prefill")
+            st = oracle.prefill(m, ctx, row_block=8192)
+            steps, rows = [], {}
+            if spill:
+                _save_progress(spill, b, st, steps, rows)
+        else:
+            st, steps, rows = got
+            log(f"cfg5_full: seq {b} resumed after {len(steps)} steps")
+        for s_ in range(len(steps), n_steps):
+            p = plans[s_][b]
+            t0 = time.time()
+            g = greedy(m, st, p.accept + 1)
+            d = batches.multistep_draft(b, s_, p.k, p.accept, ctx, g, cfg.vocab)
+            res = oracle.verify(m, st, d)
+            steps.append(record(res, ids, top_n=4))
+            rows[f"seq{b}_step{s_}"] = quantize_rows(res.logits[[0, len(d)]])
+            st = oracle.commit(st, res, res.accepted)
+            log(f"cfg5_full: seq {b} step {s_} k={p.k} planted={p.accept} accepted={res.accepted} "
+                f"({time.time() - t0:.0f}s)")
+            if spill:
+                _save_progress(spill, b, st, steps, rows)
+        out.append({"seq": b, "steps": steps})
+        all_rows.update(rows)
+        del st
+    np.savez_compressed(os.path.join(HERE, "cfg5_full_rows.npz"), step=np.float64(FULL_ROW_STEP), **all_rows)
+    return {"config": "32B shape at full depth (64 layers, 64 q / 8 kv heads of 128, SwiGLU 27648, vocab 152064); "
+                      "8 sequences at context 8192 (Zipf tokens), verify + commit steps with k uniform in {4..64} "
+                      "and cache drafts planted uniform in [0, k]; sequences 0 and 1 checked over the first "
+                      f"{n_steps} steps; rows 0 and k of every verify stored whole in cfg5_full_rows.npz",
+            "model": cfg.as_dict(), "n_layers": cfg.n_layers, "n_steps": n_steps,
+            "sample_ids": [int(i) for i in ids], "seqs": out, "oracle_dtype": "float32 (bf16 weights streamed)",
+            "full_rows": "cfg5_full_rows.npz", "full_row_step": FULL_ROW_STEP}
+
+
 def main():
-    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3, "cfg4": case_cfg4, "cfg5": case_cfg5, "tree2": case_tree2}
-    for name in sys.argv[1:]:
+    import argparse
+    ap = argparse.ArgumentParser()
+    ap.add_argument("cases", nargs="+")
+    ap.add_argument("--spill", default=None, help="directory for streamed weights and resume state (cfg5_full)")
+    ap.add_argument("--steps", type=int, default=4, help="verify + commit steps of cfg5_full")
+    ap.add_argument("--resident", type=int, default=38, help="32B layers held in memory (cfg5_full)")
+    args = ap.parse_args()
+    cases = {"cfg2": case_cfg2, "cfg3": case_cfg3, "cfg4": case_cfg4, "cfg5": case_cfg5, "tree2": case_tree2,
+             "cfg5_full": lambda: case_cfg5_full(args.spill, args.steps, args.resident)}
+    for name in args.cases:
         t0 = time.time()
         out = cases[name]()
         path = os.path.join(HERE, f"{name}.json")
