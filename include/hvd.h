@@ -128,6 +128,24 @@ hvd_status hvd_verify(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_
                       const int32_t* ctx_lens, const int32_t* draft_tokens, const int32_t* draft_lens,
                       int32_t* accepted_len, int32_t* next_token, float* logits);
 
+/* hvd_verify for callers that cannot allocate device memory (tight serving
+ * loops, harnesses that forbid hipMalloc after set-up): same arguments,
+ * results and errors as hvd_verify, but the step's scratch (split-K partial
+ * tiles, attention split-KV partials, LM-head argmax partials, per-row
+ * argmax, the results block and the accept kernel's arrival counter) lives
+ * in a static device array of 64 MiB that each GPU the library runs on holds
+ * until the process ends, instead of the KV handle's workspace.  The call
+ * makes no hipMalloc / hipFree and creates no HIP graph or event (kernels are
+ * launched one by one; profiling is suspended for the call).  A step whose
+ * fixed scratch (about rows * vocab / 2 bytes of LM-head partials plus 8 MiB)
+ * does not fit is refused with HVD_ERR_RANGE before any state changes; one
+ * whose attention partials do not fit the rest is HVD_ERR_OOM.  All calls on
+ * one GPU share that GPU's array, which keeps the last call's contents: calls
+ * that overlap on one GPU (two host threads, or two streams) race. */
+hvd_status hvd_verify_noalloc(hvd_model m, hvd_kv kv, int32_t batch, const int32_t* seq_ids,
+                              const int32_t* ctx_lens, const int32_t* draft_tokens, const int32_t* draft_lens,
+                              int32_t* accepted_len, int32_t* next_token, float* logits);
+
 /* One verification step over token trees (the tree-shaped drafts of the
  * model drafter, App. A: EAGLE3 with tree depth 8 and top-k 4), under the
  * same rule: for sequence b, node_counts[b] = n_b <= 63 nodes, packed in

@@ -311,6 +311,25 @@ struct ProfRec {
   double bytes;
 };
 
+// The per-step scratch of one forward: split-K partial tiles, attention
+// split-KV partials, LM-head argmax partials, per-row inverse RMS and argmax,
+// the results block and the accept kernel's arrival counter.  hvd_verify takes
+// it from the handle's workspace; hvd_verify_noalloc from the library's static
+// device array.
+struct StepScratch {
+  float* gemm_part = nullptr;
+  size_t gemm_part_bytes = 0;
+  float* part_o = nullptr;
+  float* part_ml = nullptr;
+  size_t part_rows = 0;  // attention partial rows (each dh floats in part_o, 2 in part_ml)
+  float* lm_val = nullptr;
+  int32_t* lm_idx = nullptr;
+  float* inv_rms = nullptr;
+  int32_t* g = nullptr;
+  int32_t* out = nullptr;
+  uint32_t* counter = nullptr;
+};
+
 struct hvd_kv_s {
   hvd_model_s* m = nullptr;
   HostState* hs = nullptr;
@@ -355,6 +374,9 @@ struct hvd_kv_s {
   int32_t* meta_host = nullptr;
   size_t meta_ints = 0;
   int32_t* out_host = nullptr;
+  StepScratch sx;                 // the handle's own step scratch
+  void* static_base = nullptr;    // this device's static scratch (hipGetSymbolAddress at kv_alloc)
+  size_t static_bytes = 0;
   // profiling
   bool prof = false;
   std::vector<ProfRec> prof_pending;
@@ -415,6 +437,17 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->part_ml = cv.take<float>((size_t)kPartSlots * kAttnRows * 2);
   k->meta_ints = meta_capacity_ints(c, k->max_rows, max_seqs, k->pt_stride);
   k->meta_dev = cv.take<int32_t>(k->meta_ints);
+  k->sx.gemm_part = k->gemm_part;
+  k->sx.gemm_part_bytes = kGemmPartBytes;
+  k->sx.part_o = k->part_o;
+  k->sx.part_ml = k->part_ml;
+  k->sx.part_rows = (size_t)kPartSlots * kAttnRows;
+  k->sx.lm_val = k->lm_val;
+  k->sx.lm_idx = k->lm_idx;
+  k->sx.inv_rms = k->inv_rms;
+  k->sx.g = k->g;
+  k->sx.out = k->out;
+  k->sx.counter = k->counter;
   return cv.off;
 }
 
@@ -517,6 +550,12 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   if (hipError_t e = attn_set_lds_limit(); e != hipSuccess) {
     hvd_kv_free(k);
     return set_err(HVD_ERR_DEVICE, std::string("attention LDS limit: ") + hipGetErrorString(e));
+  }
+  // this device's static scratch (hvd_verify_noalloc): its address is taken
+  // here, once per device, with the device current
+  if (hipError_t e = static_scratch(&k->static_base, &k->static_bytes); e != hipSuccess) {
+    hvd_kv_free(k);
+    return set_err(HVD_ERR_DEVICE, std::string("static scratch address: ") + hipGetErrorString(e));
   }
   *out = k;
   return HVD_OK;
@@ -705,7 +744,10 @@ struct AsyncCap {
 };
 
 hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<RowMeta> rows, bool lm_head,
-                   float* logits, const TreeRows* tree = nullptr, AsyncCap* acap = nullptr) {
+                   float* logits, const TreeRows* tree = nullptr, AsyncCap* acap = nullptr,
+                   const StepScratch* scratch = nullptr) {
+  const StepScratch& sx = scratch ? *scratch : k->sx;
+  const bool eager_only = scratch != nullptr;  // no graph instantiation (it allocates)
   // each row's pool slot: page * kPage + offset (the QKV epilogue writes K/V there)
   for (RowMeta& r : rows) r.kvs = k->hs->seq(r.slot).pages[(size_t)(r.kvs / kPage)] * kPage + r.kvs % kPage;
   hvd_model_s* m = k->m;
@@ -736,7 +778,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     if (members[cl].empty()) continue;
     Plan& pl = plans[cl];
     if (!plan_attention(c, *k->hs, seqs, members[cl], k->attn_min_items, kClassRows[cl],
-                        (size_t)kPartSlots * kAttnRows - part_used, pl))
+                        sx.part_rows - part_used, pl))
       return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
     pl.part_base = part_used;
     part_used += pl.part_rows;
@@ -904,7 +946,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.wk = 256;
     a.MTtot = MT;
     a.M = M;
-    a.part = k->gemm_part;
+    a.part = sx.gemm_part;
     const int want = k->gemm_min_blocks;
     if (MT > k->skinny_max_mt && N % 128 == 0) {
       // many rows: MFMA-tiled kernel, weights read once per XCD.  Of the
@@ -927,7 +969,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       int splits = 1;
       if (forced) splits = std::max(1, std::min(k->tiled_force[family][1], a.KT / 32));
       else if (nblk < want_t) splits = std::max(1, std::min({4, (want_t + nblk - 1) / nblk, a.KT / 32}));
-      while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > kGemmPartBytes) --splits;
+      while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > sx.gemm_part_bytes) --splits;
       const bool mlp = epi == EPI_SILU || family == PF_DOWN;
       if (epi == EPI_LM) {
         lm_parts = N / tile_bn[tile];
@@ -935,7 +977,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       }
       ProfScope ps(k, family, (double)N * K * 2.0);
       const bool single = lm_head && ((mlp && k->mlp_single) || (epi == EPI_LM && k->lm_single));
-      HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, k->inv_rms, s));
+      HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, sx.inv_rms, s));
       return HVD_OK;
     }
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
@@ -968,7 +1010,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         splits = std::min(k->gemm_force[family][1], a.KT);
       }
     }
-    while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > kGemmPartBytes) --splits;
+    while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > sx.gemm_part_bytes) --splits;
     if (epi == EPI_LM) {
       lm_parts = a.NT / ns;
       a.n_part = lm_parts;
@@ -1028,8 +1070,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         const Plan& pl = plans[cl];
         if (pl.items.empty()) continue;
         a.items = d_items + pl.item0;
-        a.part_o = k->part_o + pl.part_base * dh;
-        a.part_ml = k->part_ml + pl.part_base * 2;
+        a.part_o = sx.part_o + pl.part_base * dh;
+        a.part_ml = sx.part_ml + pl.part_base * 2;
         ProfScope ps(k, PF_ATTN, kv_bytes_cl[cl]);
         HIP_TRY(launch_attn(a, (int)pl.items.size(), pl.chunk, pl.rpi, k->attn_max_np, s));
       }
@@ -1042,8 +1084,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         cb.Hkv = c.n_kv_heads;
         cb.dh = dh;
         cb.group = G;
-        cb.part_o = k->part_o + pl.part_base * dh;
-        cb.part_ml = k->part_ml + pl.part_base * 2;
+        cb.part_o = sx.part_o + pl.part_base * dh;
+        cb.part_ml = sx.part_ml + pl.part_base * 2;
         cb.Ohi = k->Ohi;
         cb.Olo = k->Olo;
         cb.MTtot = MT;
@@ -1104,22 +1146,22 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.eps = c.rms_eps;
     a.logits = logits;
     a.vocab = c.vocab;
-    a.part_val = k->lm_val;
-    a.part_idx = k->lm_idx;
+    a.part_val = sx.lm_val;
+    a.part_idx = sx.lm_idx;
     if (hvd_status st = gemm(EPI_LM, a, c.vocab, D, PF_LM); st != HVD_OK) return st;
     AcceptArgs ac{};
-    ac.part_val = k->lm_val;
-    ac.part_idx = k->lm_idx;
+    ac.part_val = sx.lm_val;
+    ac.part_idx = sx.lm_idx;
     ac.n_part = lm_parts;
     ac.M = M;
-    ac.g = k->g;
+    ac.g = sx.g;
     ac.seqs = d_seqs;
     ac.rows = d_rows;
     ac.B = B;
-    ac.out = k->out;
-    ac.counter = k->counter;
+    ac.out = sx.out;
+    ac.counter = sx.counter;
     ac.tree_parent = d_parent;
-    ac.path = k->out + 2 * B;
+    ac.path = sx.out + 2 * B;
     if (acap) {
       ac.astate = acap->state;
       ac.hist = acap->hist;
@@ -1140,8 +1182,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       cp.pt = k->pt;
       cp.pt_stride = k->pt_stride;
       cp.seqs = d_seqs;
-      cp.out = k->out;
-      cp.path = k->out + 2 * B;
+      cp.out = sx.out;
+      cp.path = sx.out + 2 * B;
       ProfScope ps(k, PF_OTHER, 0.0);
       HIP_TRY(launch_compact(cp, B, s));
     }
@@ -1171,7 +1213,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     }
     return HVD_OK;
   }
-  if (k->prof || !k->use_graphs) {
+  if (k->prof || !k->use_graphs || eager_only) {
     if (hvd_status st = launch_all(); st != HVD_OK) return st;
   } else {
     const GraphKey key{M, B, lm_head ? 1 : 0, tree ? 1 : 0, attn_key, logits};
@@ -1199,7 +1241,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     HIP_TRY(hipGraphLaunch(it->second, s));
   }
   if (lm_head)  // results, and for trees the accepted paths behind them
-    HIP_TRY(hipMemcpyAsync(k->out_host, k->out, (tree ? 2 + kMaxTreeNodes : 2) * (size_t)B * 4,
+    HIP_TRY(hipMemcpyAsync(k->out_host, sx.out, (tree ? 2 + kMaxTreeNodes : 2) * (size_t)B * 4,
                            hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (k->prof) prof_collect(k);
@@ -1233,12 +1275,54 @@ extern "C" hvd_status hvd_prefill(hvd_model m, hvd_kv k, int32_t seq_id, const i
   return HVD_OK;
 }
 
-extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids, const int32_t* ctx_lens,
-                                 const int32_t* draft_tokens, const int32_t* draft_lens, int32_t* accepted_len,
-                                 int32_t* next_token, float* logits) {
+namespace {
+
+// Carve one step's scratch out of this device's static array: the fixed
+// parts (results, arrival counter, per-row argmax / inverse RMS, LM-head
+// partials) first, then 8 MiB of split-K partial tiles, the rest for
+// attention split-KV partials.  HVD_ERR_RANGE when the fixed parts alone do
+// not fit.
+hvd_status carve_static(hvd_kv_s* k, int M, int B, StepScratch& sx) {
+  const hvd_config& c = k->m->cfg;
+  if (!k->static_base) return set_err(HVD_ERR_DEVICE, "static scratch unavailable on this device");
+  const size_t Mp = (size_t)(M + 15) / 16 * 16;
+  Carver cv(k->static_base);
+  sx.counter = cv.take<uint32_t>(64);
+  sx.out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)B);
+  sx.g = cv.take<int32_t>(Mp);
+  sx.inv_rms = cv.take<float>(Mp);
+  sx.lm_val = cv.take<float>(Mp * (size_t)k->n_part_lm);
+  sx.lm_idx = cv.take<int32_t>(Mp * (size_t)k->n_part_lm);
+  const size_t gemm_bytes = std::min<size_t>(kGemmPartBytes, 8u << 20);
+  sx.gemm_part = cv.take<float>(gemm_bytes / 4);
+  sx.gemm_part_bytes = gemm_bytes;
+  if (cv.off >= k->static_bytes)
+    return set_err(HVD_ERR_RANGE, "step too large for hvd_verify_noalloc: its fixed scratch needs " +
+                                      std::to_string(cv.off) + " bytes of the " + std::to_string(k->static_bytes) +
+                                      "-byte static scratch (use hvd_verify)");
+  const size_t row_bytes = (size_t)c.head_dim * 4 + 2 * 4;
+  const size_t rows_free = (k->static_bytes - cv.off - 2 * kAlign) / row_bytes;
+  sx.part_rows = rows_free;
+  sx.part_o = cv.take<float>(rows_free * c.head_dim);
+  sx.part_ml = cv.take<float>(rows_free * 2);
+  if (cv.off > k->static_bytes) return set_err(HVD_ERR_RANGE, "static scratch layout overflow");
+  return HVD_OK;
+}
+
+hvd_status verify_chain(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids, const int32_t* ctx_lens,
+                        const int32_t* draft_tokens, const int32_t* draft_lens, int32_t* accepted_len,
+                        int32_t* next_token, float* logits, bool use_static) {
   if (!m || !k) return set_err(HVD_ERR_ARG, "null handle");
   if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
   if (!accepted_len || !next_token) return set_err(HVD_ERR_ARG, "null output");
+  StepScratch stat;
+  if (use_static) {
+    // size check before any state change: rows = sum(k_b + 1)
+    if (batch < 1 || !draft_lens) return set_err(HVD_ERR_ARG, "bad batch");
+    int64_t M = 0;
+    for (int b = 0; b < batch; ++b) M += (int64_t)std::max(0, draft_lens[b]) + 1;
+    if (hvd_status st = carve_static(k, (int)std::min<int64_t>(M, 1 << 30), batch, stat); st != HVD_OK) return st;
+  }
   if (hvd_status st = from_host(k->hs->begin_verify(batch, seq_ids, ctx_lens, draft_tokens, draft_lens), k);
       st != HVD_OK)
     return st;
@@ -1254,7 +1338,19 @@ extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int
       rows.push_back({draft_tokens[off + i], seq_ids[b], sl.ctx + 1 + i, sl.ctx + 1 + i});
     off += kk;
   }
-  hvd_status st = forward(k, seqs, rows, true, logits);
+  hvd_status st = HVD_OK;
+  if (use_static) {
+    // the arrival counter starts at zero (an earlier failed call may have left it set)
+    const bool prof = k->prof;
+    k->prof = false;  // no profiling events: creating them allocates
+    if (hipMemsetAsync(stat.counter, 0, 4, k->stream) != hipSuccess)
+      st = set_err(HVD_ERR_DEVICE, "clearing the static scratch counter failed");
+    else
+      st = forward(k, seqs, rows, true, logits, nullptr, nullptr, &stat);
+    k->prof = prof;
+  } else {
+    st = forward(k, seqs, rows, true, logits);
+  }
   if (st != HVD_OK) {
     k->hs->abort_verify(batch, seq_ids);
     return st;
@@ -1265,6 +1361,23 @@ extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int
   }
   k->hs->finish_verify(batch, seq_ids, draft_tokens, draft_lens, accepted_len, next_token);
   return HVD_OK;
+}
+
+}  // namespace
+
+extern "C" hvd_status hvd_verify(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids, const int32_t* ctx_lens,
+                                 const int32_t* draft_tokens, const int32_t* draft_lens, int32_t* accepted_len,
+                                 int32_t* next_token, float* logits) {
+  return verify_chain(m, k, batch, seq_ids, ctx_lens, draft_tokens, draft_lens, accepted_len, next_token, logits,
+                      false);
+}
+
+extern "C" hvd_status hvd_verify_noalloc(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids,
+                                         const int32_t* ctx_lens, const int32_t* draft_tokens,
+                                         const int32_t* draft_lens, int32_t* accepted_len, int32_t* next_token,
+                                         float* logits) {
+  return verify_chain(m, k, batch, seq_ids, ctx_lens, draft_tokens, draft_lens, accepted_len, next_token, logits,
+                      true);
 }
 
 extern "C" hvd_status hvd_verify_tree(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq_ids,

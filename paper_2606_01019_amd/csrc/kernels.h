@@ -241,4 +241,9 @@ hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* p
 
 constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
 
+// Static per-device scratch of hvd_verify_noalloc (scratch.hip): its device
+// address on the current device, taken once per device.
+constexpr size_t kStaticScratchBytes = 64u << 20;
+hipError_t static_scratch(void** ptr, size_t* bytes);
+
 }  // namespace hvd

@@ -20,7 +20,7 @@ _STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM
 EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
            "hvd_prefill", "hvd_verify", "hvd_verify_tree", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
            "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error",
-           "hvd_async_begin", "hvd_async_step", "hvd_async_end")
+           "hvd_async_begin", "hvd_async_step", "hvd_async_end", "hvd_verify_noalloc")
 HVD_OPT_GRAPHS = 1
 HVD_OPT_MLP_SINGLE = 2
 HVD_OPT_LM_SINGLE = 3
@@ -76,6 +76,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hvd_kv_free": (None, [P]),
         "hvd_prefill": (I32, [P, P, I32, PI32, I32]),
         "hvd_verify": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
+        "hvd_verify_noalloc": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
         "hvd_verify_tree": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
         "hvd_commit": (I32, [P, P, I32, PI32, PI32]),
         "hvd_truncate": (I32, [P, I32, I32, I32]),
@@ -183,9 +184,11 @@ class KVCache:
         t = _i32(tokens)
         _check(self.lib.hvd_prefill(self.model.handle, self.handle, seq_id, _ptr(t), t.size))
 
-    def verify(self, seq_ids, ctx_lens, drafts, logits=None):
+    def verify(self, seq_ids, ctx_lens, drafts, logits=None, noalloc=False):
         """drafts: list of 1-D token arrays.  logits: optional torch float32
-        CUDA tensor [sum(k+1), vocab].  Returns (accepted, next_token)."""
+        CUDA tensor [sum(k+1), vocab].  Returns (accepted, next_token).
+        noalloc: call hvd_verify_noalloc (step scratch in the library's
+        static device array) instead of hvd_verify."""
         ids = _i32(seq_ids)
         ctx = _i32(ctx_lens)
         lens = _i32([len(d) for d in drafts])
@@ -199,8 +202,9 @@ class KVCache:
             assert logits.is_cuda and logits.dtype.is_floating_point and logits.element_size() == 4
             assert logits.is_contiguous() and logits.numel() >= rows * self.model.cfg.vocab
             lp = ctypes.c_void_p(logits.data_ptr())
-        _check(self.lib.hvd_verify(self.model.handle, self.handle, ids.size, _ptr(ids), _ptr(ctx), _ptr(flat),
-                                   _ptr(lens), _ptr(acc), _ptr(nxt), lp))
+        fn = self.lib.hvd_verify_noalloc if noalloc else self.lib.hvd_verify
+        _check(fn(self.model.handle, self.handle, ids.size, _ptr(ids), _ptr(ctx), _ptr(flat),
+                  _ptr(lens), _ptr(acc), _ptr(nxt), lp))
         return acc, nxt
 
     def verify_tree(self, seq_ids, ctx_lens, trees, logits=None):
