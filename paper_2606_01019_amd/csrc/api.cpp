@@ -53,6 +53,7 @@ constexpr int kGemmMinBlocks = 192;          // GEMM workgroups below which the 
 constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (one per CU)
 constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
 constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
+constexpr int kGemmCounters = 16384;          // split-K arrival counters (output blocks of one launch)
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
 constexpr int kCUs = 256;                     // compute units of the MI355X
 constexpr int kAttnRows = 128;     // query rows per attention work item
@@ -319,6 +320,7 @@ struct ProfRec {
 struct StepScratch {
   float* gemm_part = nullptr;
   size_t gemm_part_bytes = 0;
+  uint32_t* gemm_cnt = nullptr;  // split-K arrival counters (zero between launches)
   float* part_o = nullptr;
   float* part_ml = nullptr;
   size_t part_rows = 0;  // attention partial rows (each dh floats in part_o, 2 in part_ml)
@@ -362,6 +364,7 @@ struct hvd_kv_s {
   bool ns8_mt3 = true;  // 8-strip skinny blocks at three and four single-pass row tiles
   int tiled_force[PF_LM + 1][2] = {};  // per GEMM family: {tile + 1, K splits} of the tiled kernel, 0 = policy
   float* gemm_part = nullptr;
+  uint32_t* gemm_cnt = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
   bool mlp_single = true;    // large-batch verify MLP GEMMs on the hi activation part only
   bool lm_single = true;     // large-batch verify LM head on the hi activation part only
@@ -429,6 +432,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->lm_val = cv.take<float>(Mp * k->n_part_lm);
   k->lm_idx = cv.take<int32_t>(Mp * k->n_part_lm);
   k->gemm_part = cv.take<float>(kGemmPartBytes / 4);
+  k->gemm_cnt = cv.take<uint32_t>(kGemmCounters);
   k->inv_rms = cv.take<float>(Mp);
   k->g = cv.take<int32_t>(Mp);
   k->out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)max_seqs);  // [B][2] results, then [B][63] tree paths
@@ -439,6 +443,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->meta_dev = cv.take<int32_t>(k->meta_ints);
   k->sx.gemm_part = k->gemm_part;
   k->sx.gemm_part_bytes = kGemmPartBytes;
+  k->sx.gemm_cnt = k->gemm_cnt;
   k->sx.part_o = k->part_o;
   k->sx.part_ml = k->part_ml;
   k->sx.part_rows = (size_t)kPartSlots * kAttnRows;
@@ -947,6 +952,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     a.MTtot = MT;
     a.M = M;
     a.part = sx.gemm_part;
+    a.cnt = sx.gemm_cnt;
     const int want = k->gemm_min_blocks;
     if (MT > k->skinny_max_mt && N % 128 == 0) {
       // many rows: MFMA-tiled kernel, weights read once per XCD.  Of the
@@ -1011,6 +1017,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       }
     }
     while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > sx.gemm_part_bytes) --splits;
+    if (splits > 1 && (size_t)(a.NT / ns) * mblocks > (size_t)kGemmCounters) splits = 1;
     if (epi == EPI_LM) {
       lm_parts = a.NT / ns;
       a.n_part = lm_parts;
@@ -1288,6 +1295,7 @@ hvd_status carve_static(hvd_kv_s* k, int M, int B, StepScratch& sx) {
   const size_t Mp = (size_t)(M + 15) / 16 * 16;
   Carver cv(k->static_base);
   sx.counter = cv.take<uint32_t>(64);
+  sx.gemm_cnt = cv.take<uint32_t>(kGemmCounters);
   sx.out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)B);
   sx.g = cv.take<int32_t>(Mp);
   sx.inv_rms = cv.take<float>(Mp);
@@ -1343,7 +1351,10 @@ hvd_status verify_chain(hvd_model m, hvd_kv k, int32_t batch, const int32_t* seq
     // the arrival counter starts at zero (an earlier failed call may have left it set)
     const bool prof = k->prof;
     k->prof = false;  // no profiling events: creating them allocates
-    if (hipMemsetAsync(stat.counter, 0, 4, k->stream) != hipSuccess)
+    // counters start at zero (an earlier failed call may have left some set);
+    // the accept counter and the split-K counters are adjacent
+    if (hipMemsetAsync(stat.counter, 0, (size_t)((char*)(stat.gemm_cnt + kGemmCounters) - (char*)stat.counter),
+                       k->stream) != hipSuccess)
       st = set_err(HVD_ERR_DEVICE, "clearing the static scratch counter failed");
     else
       st = forward(k, seqs, rows, true, logits, nullptr, nullptr, &stat);

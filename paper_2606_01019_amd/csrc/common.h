@@ -52,6 +52,22 @@ __device__ __forceinline__ f32x4 mfma_f16(const f16x8& a, const f16x8& b, f32x4 
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
+// Device-scope (write-through / coherent) stores and loads.  The L2 caches
+// of the eight XCDs are not coherent with each other; data one workgroup
+// hands to a workgroup of another XCD inside the same kernel goes through
+// these (relaxed device-scope atomics: sc1 stores and loads, no cache-wide
+// write-back or invalidate).  The writer waits for its stores (vmcnt(0))
+// before it signals, and the reader loads only after seeing the signal.
+__device__ __forceinline__ void store_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_dev_u32(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_dev(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   return v;

@@ -20,9 +20,10 @@
 // first weight loads, so no dependent memory round trip is left for the end.
 // Partial sums are reduced through LDS in a fixed order.  When the column
 // blocks alone are too few to keep enough weight bytes in flight, K is also
-// split across workgroups (gridDim.y): each publishes its partial tile and a
-// second kernel sums the splits in order (deterministic; a kernel boundary is
-// cheaper here than device-scope release fences).  Fused epilogues:
+// split across workgroups (gridDim.y): each publishes its partial tile with
+// write-through stores and counts its arrival; the last split to arrive sums
+// all splits in split order (deterministic) and runs the epilogue, so a K
+// split costs no second kernel.  Fused epilogues:
 //   EPI_QKV   inverse-RMS row scale, rotary embedding on q and k (pairs are
 //             adjacent columns after the load-time permutation), q -> Q
 //             buffer, k/v -> paged fp16 KV cache;
@@ -544,71 +545,58 @@ __global__ __launch_bounds__(512, gemm_occupancy(MT)) void gemm_skinny(GemmArgs 
   __syncthreads();
 
   if (split) {
-    // K split across workgroups: publish the partial tile; gemm_finish sums
-    // the splits in order and runs the epilogue.
-    float* dst = a.part + ((size_t)(co.mb * gridDim.x + cb) * gridDim.y + co.split) * ROWS * COLS;
-    for (int e = tid; e < mcount * 16 * COLS; e += 512) dst[e] = tile[e / COLS][e % COLS];
-    return;
+    // K split across workgroups: publish this split's partial tile with
+    // device-scope (write-through) stores, then count arrivals; the last
+    // split of the (row block, column block) to arrive sums every split in
+    // split order (the same order whichever arrives last, so results are
+    // deterministic) and runs the epilogue.  No second kernel.
+    constexpr int EPT = (ROWS * COLS + 511) / 512;  // tile entries per thread
+    constexpr int SB = 8;                           // splits per batch of loads
+    __shared__ int last_split;
+    const int unit = co.mb * gridDim.x + cb;
+    const int n_el = mcount * 16 * COLS;
+    float* part = a.part + (size_t)unit * gridDim.y * ROWS * COLS;
+    float* dst = part + (size_t)co.split * ROWS * COLS;
+    for (int e = tid; e < n_el; e += 512) store_dev(dst + e, tile[e / COLS][e % COLS]);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's stores are done
+    __syncthreads();
+    if (tid == 0) last_split = atomicAdd(a.cnt + unit, 1u) == gridDim.y - 1u;
+    __syncthreads();
+    if (!last_split) return;
+    float v[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) v[i] = 0.f;
+    for (int q0 = 0; q0 < (int)gridDim.y; q0 += SB) {
+      float t[EPT][SB];
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+#pragma unroll
+        for (int q = 0; q < SB; ++q) {
+          const int el = tid + i * 512;
+          const int qq = q0 + q < (int)gridDim.y ? q0 + q : 0;
+          t[i][q] = load_dev(part + (size_t)qq * ROWS * COLS + (el < n_el ? el : 0));
+        }
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+#pragma unroll
+        for (int q = 0; q < SB; ++q)
+          if (q0 + q < (int)gridDim.y) v[i] += t[i][q];
+    }
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      const int el = tid + i * 512;
+      if (el < n_el) tile[el / COLS][el % COLS] = v[i];
+    }
+    if (tid == 0) store_dev_u32(a.cnt + unit, 0u);  // ready for the next launch
+    __syncthreads();
   }
-  gemm_epilogue<MT, NS, EPI>(a, tile, pre, cb, mt0, mcount);
-}
-
-// Second pass of a K-split GEMM: one workgroup per (column block, row block)
-// sums the splits' partial tiles in split order, then runs the epilogue.
-// All loads (epilogue inputs, then the partials, 8 splits per batch) are
-// requested before any is used.
-template <int MT, int NS, int EPI>
-__global__ __launch_bounds__(512) void gemm_finish(GemmArgs a, int splits) {
-  constexpr int ROWS = MT * 16;
-  constexpr int COLS = NS * 16;
-  constexpr int EPT = (ROWS * COLS + 511) / 512;  // tile entries per thread
-  constexpr int SB = 8;                           // splits per batch
-  __shared__ float tile[ROWS][COLS + 1];
-  __shared__ EpiPre<MT, NS, EPI> pre;
-  const int tid = threadIdx.x;
-  const int cb = blockIdx.x;
-  const int mt0 = blockIdx.z * MT;
-  const int mcount = min(MT, a.MTtot - mt0);
-  const int n_el = mcount * 16 * COLS;
-  const float* src = a.part + (size_t)(blockIdx.z * gridDim.x + cb) * splits * ROWS * COLS;
-  EpiRegs<MT, NS, EPI> er;
-  epi_issue<MT, NS, EPI>(a, er, cb, mt0, mcount);
-  float v[EPT];
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) v[i] = 0.f;
-  for (int q0 = 0; q0 < splits; q0 += SB) {
-    float t[EPT][SB];
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-#pragma unroll
-      for (int q = 0; q < SB; ++q) {
-        const int el = tid + i * 512;
-        t[i][q] = src[(size_t)(q0 + q < splits ? q0 + q : 0) * ROWS * COLS + (el < n_el ? el : 0)];
-      }
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-#pragma unroll
-      for (int q = 0; q < SB; ++q)
-        if (q0 + q < splits) v[i] += t[i][q];
-  }
-  epi_settle<MT, NS, EPI>(er);
-  epi_issue_rope<MT, NS, EPI>(a, er, cb);
-  epi_commit<MT, NS, EPI>(a, er, pre, cb, mt0, mcount);
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) {
-    const int el = tid + i * 512;
-    if (el < n_el) tile[el / COLS][el % COLS] = v[i];
-  }
-  epi_commit_rope<MT, NS, EPI>(a, er, pre, mt0, mcount);
-  __syncthreads();
   gemm_epilogue<MT, NS, EPI>(a, tile, pre, cb, mt0, mcount);
 }
 
 template <int MT, int NS, int EPI, bool HL>
 static void launch_one(const GemmArgs& a, int splits, int mblocks, hipStream_t s) {
-  const dim3 grid(a.NT / NS, splits, mblocks), fgrid(a.NT / NS, 1, mblocks);
+  const dim3 grid(a.NT / NS, splits, mblocks);
   hvd_launch((gemm_skinny<MT, NS, EPI, HL>), grid, dim3(512), 0, s, a);
-  if (splits > 1) hvd_launch((gemm_finish<MT, NS, EPI>), fgrid, dim3(512), 0, s, a, splits);
 }
 
 template <int NS, int EPI>

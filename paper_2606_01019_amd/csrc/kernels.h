@@ -100,8 +100,10 @@ struct GemmArgs {
   float* part_val;     // [M][n_part]
   int32_t* part_idx;
   int n_part;
-  // K split across workgroups: partial tiles [mblocks][NT/ns][splits][64*4*... rows][cols]
+  // K split across workgroups: partial tiles [mblocks][NT/ns][splits][rows][cols]
+  // and one arrival counter per (row block, column block), zero between launches
   float* part;
+  uint32_t* cnt;
 };
 
 struct AttnArgs {
@@ -217,7 +219,8 @@ hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst
                        hipStream_t s);
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 // ns: 16-column strips per workgroup (1, 2, 4; >= 2 for EPI_SILU); grid.x = NT / ns.
-// splits > 1 splits K across workgroups and adds the gemm_finish pass.
+// splits > 1 splits K across workgroups; the last split of each output block
+// to finish reduces (a.part, a.cnt).
 // hi_lo false: the hi activation part alone (honoured for the residual and
 // SiLU GEMMs at 3-4 row tiles; other shapes keep the pair)
 hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, bool hi_lo,
