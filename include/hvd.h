@@ -243,9 +243,10 @@ int32_t hvd_kv_free_pages(hvd_kv kv);
 /* Per-kernel timing: while enabled, every launch of a kernel family is
  * bracketed by HIP events on the handle's stream and its algorithmic HBM bytes
  * (weights streamed, KV read) are accumulated.  family: 0 = QKV GEMM,
- * 1 = O GEMM, 2 = gate/up GEMM, 3 = down GEMM, 4 = LM-head GEMM (a GEMM launch
- * includes its split-K finish pass when it has one), 5 = verify attention,
- * 6 = attention combine, 7 = everything else.  hvd_profile_read returns the
+ * 1 = O GEMM, 2 = gate/up GEMM, 3 = down GEMM, 4 = LM-head GEMM, 5 = verify
+ * attention, 6 = attention combine, 7 = everything else, 8 = the one-launch
+ * verify step (HVD_OPT_FLOW: the whole forward, its bytes the step's weights
+ * and K/V).  hvd_profile_read returns the
  * summed event time (ms), launch count and algorithmic bytes since the last
  * enable.  The events add a little time to every bracketed launch. */
 hvd_status hvd_profile_enable(hvd_kv kv, int32_t enable);
@@ -265,9 +266,25 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   Logit differences stay within the verify step's tolerance.
  * HVD_OPT_LM_SINGLE (default 1): likewise for the LM-head GEMM of verify
  *   forwards of more than 32 rows (its rounding error, ~1e-4 on the logits,
- *   is far below the tolerance); 0 keeps the pair. */
-enum { HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3 };
+ *   is far below the tolerance); 0 keeps the pair.
+ * HVD_OPT_FLOW (default 0): 1 runs verify steps of at most 32 rows (head dim
+ *   128, at most 128 query rows per kv head per sequence, chain drafts) as
+ *   one kernel launch in which each phase's workgroups request their weights
+ *   before waiting for the previous phase; 0 launches one kernel per GEMM /
+ *   attention pass (measured faster at batch 1).  Results agree within
+ *   rounding (the attention split may differ).
+ * HVD_OPT_FLOW_ITEMS (default 128): attention work items the one-launch step
+ *   aims for (longer KV chunks when fewer); a tuning knob. */
+enum { HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3, HVD_OPT_FLOW = 4, HVD_OPT_FLOW_ITEMS = 5 };
 hvd_status hvd_kv_set_option(hvd_kv kv, int32_t option, int32_t value);
+
+/* Diagnostics of the one-launch step (HVD_OPT_FLOW): while dev_buf (DEVICE,
+ * caller-owned, n_words uint64) is set, each such step whose workgroups fit
+ * (4 words each) writes, for workgroup w in launch order, words 4w..4w+3:
+ * its start, the time it found its inputs complete, its end (a 100 MHz
+ * constant-rate device clock) and the hardware id it ran on (XCD << 32 |
+ * HW_ID).  dev_buf NULL stops tracing.  Not needed for results. */
+hvd_status hvd_flow_trace(hvd_kv kv, uint64_t* dev_buf, int64_t n_words);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* hvd_last_error(void);

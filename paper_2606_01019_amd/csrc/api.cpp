@@ -54,6 +54,9 @@ constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (o
 constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
 constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
 constexpr int kGemmCounters = 16384;          // split-K arrival counters (output blocks of one launch)
+constexpr int kFlowCounterWords = 1 << 17;    // one-launch step: error word and per-layer counters
+constexpr int kFlowAttnItems = 128;           // attention items the one-launch step aims for
+constexpr int kFlowRows = 32;                 // rows of the one-launch step (two 16-row tiles)
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
 constexpr int kCUs = 256;                     // compute units of the MI355X
 constexpr int kAttnRows = 128;     // query rows per attention work item
@@ -61,7 +64,7 @@ constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items
 constexpr size_t kMaxGraphs = 64;  // cached step graphs per KV handle
 // profiling families: GEMM by role, attention, combine, everything else
 enum { PF_QKV = 0, PF_O = 1, PF_GATEUP = 2, PF_DOWN = 3, PF_LM = 4, PF_ATTN = 5, PF_COMBINE = 6, PF_OTHER = 7,
-       kProfFamilies = 8 };
+       PF_FLOW = 8, kProfFamilies = 9 };
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -321,6 +324,7 @@ struct StepScratch {
   float* gemm_part = nullptr;
   size_t gemm_part_bytes = 0;
   uint32_t* gemm_cnt = nullptr;  // split-K arrival counters (zero between launches)
+  uint32_t* flow_cnt = nullptr;  // one-launch step: error word, then per-layer counters (cleared each step)
   float* part_o = nullptr;
   float* part_ml = nullptr;
   size_t part_rows = 0;  // attention partial rows (each dh floats in part_o, 2 in part_ml)
@@ -378,6 +382,13 @@ struct hvd_kv_s {
   size_t meta_ints = 0;
   int32_t* out_host = nullptr;
   StepScratch sx;                 // the handle's own step scratch
+  bool use_flow = false;          // one-launch step (flow.hip) where the shape allows it (HVD_OPT_FLOW)
+  int flow_min_items = kFlowAttnItems;  // attention items the one-launch step aims for
+  FlowLayer* flow_layers = nullptr;     // [n_layers] (device)
+  std::vector<FlowLayer> flow_host;     // the same table on the host (filled by carve_kv)
+  uint64_t* flow_trace = nullptr;       // borrowed diagnostics buffer (hvd_flow_trace), or null
+  int64_t flow_trace_words = 0;
+  uint32_t* flow_cnt = nullptr;         // [kFlowCounterWords]: err word, then the step's counters
   void* static_base = nullptr;    // this device's static scratch (hipGetSymbolAddress at kv_alloc)
   size_t static_bytes = 0;
   // profiling
@@ -441,9 +452,38 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->part_ml = cv.take<float>((size_t)kPartSlots * kAttnRows * 2);
   k->meta_ints = meta_capacity_ints(c, k->max_rows, max_seqs, k->pt_stride);
   k->meta_dev = cv.take<int32_t>(k->meta_ints);
+  k->flow_layers = cv.take<FlowLayer>(c.n_layers);
+  k->flow_cnt = cv.take<uint32_t>(kFlowCounterWords);
+  // the one-launch step's per-layer activations (head dim 128 only), sized
+  // for its largest batch: kFlowRows rows
+  k->flow_host.assign(c.n_layers, FlowLayer{});
+  if (c.head_dim == 128) {
+    const size_t R = kFlowRows, fpad = (size_t)kGemmMaxMT * 512;
+    for (int l = 0; l < c.n_layers; ++l) {
+      FlowLayer& f = k->flow_host[l];
+      f.x_mid = cv.take<float>(R * D);
+      f.x_out = cv.take<float>(R * D);
+      f.n_mid_hi = cv.take<uint16_t>(R * D + fpad);
+      f.n_mid_lo = cv.take<uint16_t>(R * D + fpad);
+      f.n_out_hi = cv.take<uint16_t>(R * D + fpad);
+      f.n_out_lo = cv.take<uint16_t>(R * D + fpad);
+      f.ss_mid = cv.take<float>(R * (D / 16));
+      f.ss_out = cv.take<float>(R * (D / 16));
+      f.q = cv.take<_Float16>(R * qd);
+      f.o_hi = cv.take<uint16_t>(R * qd + fpad);
+      f.o_lo = cv.take<uint16_t>(R * qd + fpad);
+      f.a_hi = cv.take<uint16_t>(R * F + fpad);
+      f.a_lo = cv.take<uint16_t>(R * F + fpad);
+      f.x_in = l ? k->flow_host[l - 1].x_out : k->X;
+      f.n_in_hi = l ? k->flow_host[l - 1].n_out_hi : k->Nhi;
+      f.n_in_lo = l ? k->flow_host[l - 1].n_out_lo : k->Nlo;
+      f.ss_in = l ? k->flow_host[l - 1].ss_out : k->ss;
+    }
+  }
   k->sx.gemm_part = k->gemm_part;
   k->sx.gemm_part_bytes = kGemmPartBytes;
   k->sx.gemm_cnt = k->gemm_cnt;
+  k->sx.flow_cnt = k->flow_cnt;
   k->sx.part_o = k->part_o;
   k->sx.part_ml = k->part_ml;
   k->sx.part_rows = (size_t)kPartSlots * kAttnRows;
@@ -505,6 +545,29 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
     delete k;
     return set_err(HVD_ERR_DEVICE, "workspace clear failed");
   }
+  {
+    // the one-launch step's table of per-layer weights, gains and KV pools
+    std::vector<FlowLayer>& fl = k->flow_host;
+    for (int l = 0; l < c.n_layers; ++l) {
+      const LayerW& L = m->layers[l];
+      fl[l].qkv = (const uint4*)L.qkv;
+      fl[l].o = (const uint4*)L.o;
+      fl[l].gu = (const uint4*)L.gu;
+      fl[l].down = (const uint4*)L.down;
+      fl[l].g_attn = L.g_attn;
+      fl[l].g_mlp = L.g_mlp;
+      fl[l].kv = k->pool + (size_t)l * k->layer_stride;
+    }
+    if (hipMemcpyAsync(k->flow_layers, fl.data(), fl.size() * sizeof(FlowLayer), hipMemcpyHostToDevice, k->stream) !=
+            hipSuccess ||
+        hipStreamSynchronize(k->stream) != hipSuccess) {
+      (void)hipHostFree(k->meta_host);
+      (void)hipHostFree(k->out_host);
+      if (k->owned) (void)hipFree(k->base);
+      delete k;
+      return set_err(HVD_ERR_DEVICE, "layer table upload failed");
+    }
+  }
   k->hs = new HostState(max_seqs, n_pages, kPage, c.max_pos, c.max_draft, c.vocab);
   if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
@@ -556,6 +619,11 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
     hvd_kv_free(k);
     return set_err(HVD_ERR_DEVICE, std::string("attention LDS limit: ") + hipGetErrorString(e));
   }
+  if (hipError_t e = flow_set_lds_limit(); e != hipSuccess) {
+    hvd_kv_free(k);
+    return set_err(HVD_ERR_DEVICE, std::string("one-launch step LDS limit: ") + hipGetErrorString(e));
+  }
+
   // this device's static scratch (hvd_verify_noalloc): its address is taken
   // here, once per device, with the device current
   if (hipError_t e = static_scratch(&k->static_base, &k->static_bytes); e != hipSuccess) {
@@ -637,6 +705,7 @@ struct Plan {
   size_t part_rows = 0;    // partial-buffer rows the plan uses
   size_t part_base = 0;    // its first partial-buffer row
   size_t item0 = 0, head0 = 0;  // offsets of its items and entries in the step's lists
+  int n_items_real = 0, n_heads_real = 0;  // before grid padding
 };
 
 // Split every (sequence, kv head, row group) of the sequences `members` into
@@ -770,10 +839,15 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // longer row sets take several row groups), one launch per class, so a
   // long draft does not put every short one on the large kernel.
   static const int kClassRows[3] = {kAttnRows / 2, kAttnRows, 2 * kAttnRows};
+  // One-launch step (flow.hip): verify batches of at most two row tiles,
+  // head dim 128, every sequence's query rows per kv head in one 128-row
+  // attention item; chain drafts only, outside a device-resident loop.
+  bool flow = k->use_flow && lm_head && !tree && !acap && MT * 16 <= kFlowRows && dh == 128;
+  for (int b = 0; b < B && flow; ++b) flow = (seqs[b].k + 1) * G <= kAttnRows;
   std::vector<int> members[3];
   for (int b = 0; b < B; ++b) {
     const int R = (seqs[b].k + 1) * G;
-    members[R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2].push_back(b);
+    members[flow ? 1 : R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2].push_back(b);
   }
   Plan plans[3];
   std::vector<AttnItem> items_all, heads_all;
@@ -782,11 +856,23 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   for (int cl = 0; cl < 3; ++cl) {
     if (members[cl].empty()) continue;
     Plan& pl = plans[cl];
-    if (!plan_attention(c, *k->hs, seqs, members[cl], k->attn_min_items, kClassRows[cl],
+    if (!plan_attention(c, *k->hs, seqs, members[cl], flow ? k->flow_min_items : k->attn_min_items, kClassRows[cl],
                         sx.part_rows - part_used, pl))
       return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
     pl.part_base = part_used;
     part_used += pl.part_rows;
+    pl.n_items_real = (int)pl.items.size();
+    pl.n_heads_real = (int)pl.heads.size();
+    if (flow) {
+      // merge unit of each multi-chunk item: the index of its merge entry
+      std::map<int, int> unit_of_slot;
+      for (size_t h = 0; h < pl.heads.size(); ++h) {
+        pl.heads[h].pad4 = (int32_t)h;
+        unit_of_slot[pl.heads[h].part] = (int)h;
+      }
+      for (AttnItem& it : pl.items)
+        if (it.nch > 1) it.pad4 = unit_of_slot[it.part - it.c];
+    }
     // Pad the grids to buckets (no-op items have k = -1) so the launch
     // sequence depends only on (rows, sequences, buckets): one cached HIP
     // graph per such shape.
@@ -885,6 +971,212 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   const uint64_t* d_mask = tree ? (const uint64_t*)(meta_dev + o_mask) : nullptr;
   const int32_t* d_parent = tree ? meta_dev + o_parent : nullptr;
 
+  // skinny GEMMs: row blocks of at most kGemmMaxMT tiles, balanced
+  const int mblocks = (MT + kGemmMaxMT - 1) / kGemmMaxMT;
+  const int mt_block = (MT + mblocks - 1) / mblocks;
+  // Strips per workgroup and K splits of the weight-streaming GEMM (measured
+  // on the 8B verify shapes): 4 strips per workgroup when that alone gives
+  // enough workgroups (8 for two row tiles, which halves the activation
+  // fragments per weight byte); for long-K GEMMs 4 strips plus a K split;
+  // otherwise 2 strips, or for one row tile 1 strip when that fills the GPU;
+  // K-split if still too few.
+  auto skinny_shape = [&](int epi, int N, int K, int family, bool single, int& ns, int& splits) {
+    const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
+    const int KT = K / 32, NT = N / 16;
+    const int want = k->gemm_min_blocks;
+    ns = 4;
+    splits = 1;
+    // 8 strips per workgroup halve the activation fragments per weight byte:
+    // two row tiles, or three and four on the single-pass activation
+    if ((mt_block == 2 || (mt_block >= 3 && single && k->ns8_mt3)) && N % 128 == 0 && nb8 >= want) {
+      ns = 8;
+    } else if (nb4 >= want) {
+      ns = 4;
+    } else if (KT >= kGemmLongK) {
+      ns = 4;
+      splits = std::max(1, std::min((kGemmSplitTarget + nb4 - 1) / nb4, KT / 64));
+    } else if (nb2 >= want) {
+      ns = 2;
+    } else if (mt_block == 1 && epi != EPI_SILU && nb2 * 2 >= want) {
+      ns = 1;  // one strip per workgroup beats a K split plus its finish pass
+    } else {
+      ns = 2;
+      splits = std::max(1, std::min((kGemmSplitTarget + nb2 - 1) / nb2, KT / 64));
+    }
+    if (family <= PF_LM && k->gemm_force[family][0]) {
+      const int fns = k->gemm_force[family][0];
+      const bool ok = NT % fns == 0 && !(fns == 1 && epi == EPI_SILU) && !(fns == 8 && (mt_block > 2 || N % 128));
+      if (ok) {
+        ns = fns;
+        splits = std::min(k->gemm_force[family][1], KT);
+      }
+    }
+    while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > sx.gemm_part_bytes) --splits;
+    if (splits > 1 && (size_t)(NT / ns) * mblocks > (size_t)kGemmCounters) splits = 1;
+  };
+  // ---------------------------------------------------------------- one-launch step
+  // counter layout per layer: QKV groups, merge units, then four 8-way counters
+  const Plan& fpl = plans[1];
+  const int flow_cstride = flow ? (c.n_kv_heads + 7) / 8 * 8 + (fpl.n_heads_real + 7) / 8 * 8 + 32 : 0;
+  const int flow_words = flow ? 8 + c.n_layers * flow_cstride : 0;
+  if (flow && flow_words > kFlowCounterWords) flow = false;  // (not reached for the supported shapes)
+  auto launch_flow_step = [&]() -> hvd_status {
+    const int qd2 = qd + 2 * kvd;
+    FlowArgs f{};
+    f.layers = k->flow_layers;
+    f.L = c.n_layers;
+    f.g_final = m->g_final;
+    f.G = G;
+    f.dh = dh;
+    const int Ns[FG_N] = {qd2, D, 2 * F, D, c.vocab}, Ks[FG_N] = {D, qd, D, F, D};
+    const int epis[FG_N] = {EPI_QKV, EPI_RESID, EPI_SILU, EPI_RESID, EPI_LM};
+    const int fams[FG_N] = {PF_QKV, PF_O, PF_GATEUP, PF_DOWN, PF_LM};
+    for (int i = 0; i < FG_N; ++i) {
+      GemmArgs& a = f.g[i];
+      a.KT = Ks[i] / 32;
+      a.NT = Ns[i] / 16;
+      a.wg = (size_t)a.KT * 256;
+      a.wk = 256;
+      a.MTtot = MT;
+      a.M = M;
+      a.part = sx.gemm_part;
+      a.cnt = sx.gemm_cnt;
+      int ns = 4, splits = 1;
+      skinny_shape(epis[i], Ns[i], Ks[i], fams[i], false, ns, splits);
+      if (ns == 8) ns = 4;  // the one-launch step compiles 1, 2 and 4 strips
+      f.ns[i] = ns;
+      f.splits[i] = splits;
+      f.n_cb[i] = a.NT / ns;
+    }
+    {
+      GemmArgs& a = f.g[FG_QKV];
+      a.Ahi = (const uint4*)k->Nhi;
+      a.Alo = (const uint4*)k->Nlo;
+      a.ss = k->ss;
+      a.ss_n = D / 16;
+      a.inv_dim = 1.f / D;
+      a.eps = c.rms_eps;
+      a.Q = k->Q;
+      a.page_stride = k->page_stride;
+      a.q_cols = qd;
+      a.kv_cols = kvd;
+      a.Hkv = c.n_kv_heads;
+      a.dh = dh;
+      a.pt = k->pt;
+      a.pt_stride = k->pt_stride;
+      a.rows = d_rows;
+      a.rope = m->rope;
+    }
+    for (int i : {FG_O, FG_DOWN}) {
+      GemmArgs& a = f.g[i];
+      a.Ahi = (const uint4*)(i == FG_O ? k->Ohi : k->Ahi);
+      a.Alo = (const uint4*)(i == FG_O ? k->Olo : k->Alo);
+      a.X = k->X;
+      a.D = D;
+      a.Nhi = k->Nhi;
+      a.Nlo = k->Nlo;
+      a.ss_out = k->ss;
+    }
+    for (int i : {FG_GU, FG_LM}) {
+      GemmArgs& a = f.g[i];
+      a.Ahi = (const uint4*)k->Nhi;
+      a.Alo = (const uint4*)k->Nlo;
+      a.ss = k->ss;
+      a.ss_n = D / 16;
+      a.inv_dim = 1.f / D;
+      a.eps = c.rms_eps;
+    }
+    f.g[FG_GU].act_hi = k->Ahi;
+    f.g[FG_GU].act_lo = k->Alo;
+    f.g[FG_LM].W = (const uint4*)m->lm;  // (the layer GEMMs take W from the layer table)
+    f.g[FG_LM].logits = logits;
+    f.g[FG_LM].vocab = c.vocab;
+    f.g[FG_LM].part_val = sx.lm_val;
+    f.g[FG_LM].part_idx = sx.lm_idx;
+    f.g[FG_LM].n_part = f.n_cb[FG_LM];
+    // attention (one 128-row class) and its merge
+    AttnArgs& at = f.attn;
+    at.Q = k->Q;
+    at.page_stride = k->page_stride;
+    at.Hq = c.n_q_heads;
+    at.Hkv = c.n_kv_heads;
+    at.dh = dh;
+    at.group = G;
+    at.pt = k->pt;
+    at.pt_stride = k->pt_stride;
+    at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
+    at.Ohi = k->Ohi;
+    at.Olo = k->Olo;
+    at.MTtot = MT;
+    at.part_o = sx.part_o + fpl.part_base * dh;
+    at.part_ml = sx.part_ml + fpl.part_base * 2;
+    CombineArgs& cb = f.comb;
+    cb.heads = d_heads + fpl.head0;
+    cb.Hq = c.n_q_heads;
+    cb.Hkv = c.n_kv_heads;
+    cb.dh = dh;
+    cb.group = G;
+    cb.part_o = at.part_o;
+    cb.part_ml = at.part_ml;
+    cb.Ohi = k->Ohi;
+    cb.Olo = k->Olo;
+    cb.MTtot = MT;
+    cb.rpi = fpl.rpi;
+    cb.max_rows = fpl.comb_rows;
+    f.np = std::max(2, std::min(4, attn_pages_per_sub(fpl.chunk)));
+    f.items = d_items + fpl.item0;
+    f.heads = d_heads + fpl.head0;
+    constexpr int kMergeRows = 512 / (128 / 8 * 4);  // rows per merge slice (combine_slice<128, 4, 512>)
+    f.merge_spb = (fpl.comb_rows + kMergeRows - 1) / kMergeRows;
+    int n_single = 0;
+    for (int i = 0; i < fpl.n_items_real; ++i) n_single += fpl.items[i].nch == 1;
+    f.oin_target = (uint32_t)(n_single + fpl.n_heads_real * f.merge_spb);
+    f.qkv_group_target = (uint32_t)((G * dh + 2 * dh) / (16 * f.ns[FG_QKV]));
+    // phases of a layer
+    f.ph[FL_QKV] = 0;
+    f.ph[FL_ATTN] = f.n_cb[FG_QKV] * f.splits[FG_QKV];
+    f.ph[FL_MERGE] = f.ph[FL_ATTN] + fpl.n_items_real;
+    f.ph[FL_O] = f.ph[FL_MERGE] + fpl.n_heads_real * f.merge_spb;
+    f.ph[FL_GU] = f.ph[FL_O] + f.n_cb[FG_O] * f.splits[FG_O];
+    f.ph[FL_DOWN] = f.ph[FL_GU] + f.n_cb[FG_GU] * f.splits[FG_GU];
+    f.ph[FL_PHASES] = f.ph[FL_DOWN] + f.n_cb[FG_DOWN] * f.splits[FG_DOWN];
+    f.per_layer = f.ph[FL_PHASES];
+    f.n_lm = f.n_cb[FG_LM] * f.splits[FG_LM];
+    f.err = sx.flow_cnt;
+    if (k->flow_trace && (int64_t)4 * (c.n_layers * f.per_layer + f.n_lm) <= k->flow_trace_words)
+      f.trace = k->flow_trace;
+    f.cnt = sx.flow_cnt + 8;
+    f.cstride = flow_cstride;
+    f.c_unit = (c.n_kv_heads + 7) / 8 * 8;
+    f.c_oin = f.c_unit + (fpl.n_heads_real + 7) / 8 * 8;
+    f.c_o = f.c_oin + 8;
+    f.c_gu = f.c_o + 8;
+    f.c_down = f.c_gu + 8;
+    {
+      double bytes = 2.0 * ((double)c.n_layers * ((double)qd2 * D + (double)D * qd + 2.0 * F * D + (double)D * F) +
+                            (double)c.vocab * D);
+      for (int b = 0; b < B; ++b) bytes += (double)(seqs[b].ctx + seqs[b].k + 1) * kvd * 2 * 2 * c.n_layers;
+      ProfScope ps(k, PF_FLOW, bytes);
+      HIP_TRY(launch_flow(f, MT, s));
+    }
+    AcceptArgs ac{};
+    ac.part_val = sx.lm_val;
+    ac.part_idx = sx.lm_idx;
+    ac.n_part = f.n_cb[FG_LM];
+    ac.M = M;
+    ac.g = sx.g;
+    ac.seqs = d_seqs;
+    ac.rows = d_rows;
+    ac.B = B;
+    ac.out = sx.out;
+    ac.counter = sx.counter;
+    ac.path = sx.out + 2 * B;
+    ac.flow_err = sx.flow_cnt;
+    ProfScope ps(k, PF_OTHER, 0.0);
+    HIP_TRY(launch_accept(ac, s));
+    return HVD_OK;
+  };
+
   // ---------------------------------------------------------------- launches
   // Everything below only enqueues kernels whose arguments are fixed by
   // the GraphKey fields: captured once per shape into
@@ -931,18 +1223,15 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     e.pt = k->pt;
     e.pt_stride = k->pt_stride;
     e.V = c.vocab;
+    if (flow) {  // the one-launch step's error word and counters start at zero
+      e.zero = sx.flow_cnt;
+      e.n_zero = flow_words;
+    }
     ProfScope ps(k, PF_OTHER, 0.0);
     HIP_TRY(launch_embed(e, s));
   }
+  if (flow) return launch_flow_step();
 
-  // skinny GEMMs: row blocks of at most kGemmMaxMT tiles, balanced
-  const int mblocks = (MT + kGemmMaxMT - 1) / kGemmMaxMT;
-  const int mt_block = (MT + mblocks - 1) / mblocks;
-  // Workgroup shape per GEMM (measured on the 8B verify shapes): 4 strips
-  // per workgroup when that alone gives enough workgroups (8 for two row
-  // tiles, which halves the activation fragments per weight byte); for
-  // long-K GEMMs 4 strips plus a K split; otherwise 2 strips, or for one
-  // row tile 1 strip when that fills the GPU; K-split if still too few.
   int lm_parts = 0;
   auto gemm = [&](int epi, GemmArgs& a, int N, int K, int family) -> hvd_status {
     a.KT = K / 32;
@@ -986,38 +1275,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, sx.inv_rms, s));
       return HVD_OK;
     }
-    const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
     // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
     const bool single = lm_head && MT > 2 &&
                         ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
     int ns = 4, splits = 1;
-    // 8 strips per workgroup halve the activation fragments per weight byte:
-    // two row tiles, or three and four on the single-pass activation
-    if ((mt_block == 2 || (mt_block >= 3 && single && k->ns8_mt3)) && N % 128 == 0 && nb8 >= want) {
-      ns = 8;
-    } else if (nb4 >= want) {
-      ns = 4;
-    } else if (a.KT >= kGemmLongK) {
-      ns = 4;
-      splits = std::max(1, std::min((kGemmSplitTarget + nb4 - 1) / nb4, a.KT / 64));
-    } else if (nb2 >= want) {
-      ns = 2;
-    } else if (mt_block == 1 && epi != EPI_SILU && nb2 * 2 >= want) {
-      ns = 1;  // one strip per workgroup beats a K split plus its finish pass
-    } else {
-      ns = 2;
-      splits = std::max(1, std::min((kGemmSplitTarget + nb2 - 1) / nb2, a.KT / 64));
-    }
-    if (family <= PF_LM && k->gemm_force[family][0]) {
-      const int fns = k->gemm_force[family][0];
-      const bool ok = a.NT % fns == 0 && !(fns == 1 && epi == EPI_SILU) && !(fns == 8 && (mt_block > 2 || N % 128));
-      if (ok) {
-        ns = fns;
-        splits = std::min(k->gemm_force[family][1], a.KT);
-      }
-    }
-    while (splits > 1 && (size_t)(N / 16) * 16 * splits * mt_block * 16 * mblocks * 4 > sx.gemm_part_bytes) --splits;
-    if (splits > 1 && (size_t)(a.NT / ns) * mblocks > (size_t)kGemmCounters) splits = 1;
+    skinny_shape(epi, N, K, family, single, ns, splits);
     if (epi == EPI_LM) {
       lm_parts = a.NT / ns;
       a.n_part = lm_parts;
@@ -1248,10 +1510,12 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     HIP_TRY(hipGraphLaunch(it->second, s));
   }
   if (lm_head)  // results, and for trees the accepted paths behind them
-    HIP_TRY(hipMemcpyAsync(k->out_host, sx.out, (tree ? 2 + kMaxTreeNodes : 2) * (size_t)B * 4,
+    HIP_TRY(hipMemcpyAsync(k->out_host, sx.out, ((tree ? 2 + kMaxTreeNodes : 2) * (size_t)B + (flow ? 1 : 0)) * 4,
                            hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (k->prof) prof_collect(k);
+  if (flow && k->out_host[2 * B] != 0)
+    return set_err(HVD_ERR_DEVICE, "one-launch verify step: a dependency wait gave up (results invalid)");
   return HVD_OK;
 }
 
@@ -1296,6 +1560,7 @@ hvd_status carve_static(hvd_kv_s* k, int M, int B, StepScratch& sx) {
   Carver cv(k->static_base);
   sx.counter = cv.take<uint32_t>(64);
   sx.gemm_cnt = cv.take<uint32_t>(kGemmCounters);
+  sx.flow_cnt = cv.take<uint32_t>(kFlowCounterWords);
   sx.out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)B);
   sx.g = cv.take<int32_t>(Mp);
   sx.inv_rms = cv.take<float>(Mp);
@@ -1641,6 +1906,17 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
         k->graphs.clear();
       }
       return HVD_OK;
+    case HVD_OPT_FLOW:
+      k->use_flow = value != 0;
+      for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+      k->graphs.clear();
+      return HVD_OK;
+    case HVD_OPT_FLOW_ITEMS:
+      if (value < 1) return set_err(HVD_ERR_ARG, "HVD_OPT_FLOW_ITEMS must be >= 1");
+      k->flow_min_items = value;
+      for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+      k->graphs.clear();
+      return HVD_OK;
     case HVD_OPT_MLP_SINGLE:
     case HVD_OPT_LM_SINGLE:
       (option == HVD_OPT_MLP_SINGLE ? k->mlp_single : k->lm_single) = value != 0;
@@ -1649,6 +1925,14 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
       return HVD_OK;
   }
   return set_err(HVD_ERR_ARG, "unknown option");
+}
+
+extern "C" hvd_status hvd_flow_trace(hvd_kv k, uint64_t* dev_buf, int64_t n_words) {
+  if (!k) return set_err(HVD_ERR_ARG, "null handle");
+  if (dev_buf && n_words < 4) return set_err(HVD_ERR_ARG, "trace buffer too small");
+  k->flow_trace = dev_buf;
+  k->flow_trace_words = dev_buf ? n_words : 0;
+  return HVD_OK;
 }
 
 extern "C" const char* hvd_last_error(void) { return g_err.c_str(); }

@@ -28,420 +28,24 @@
 // A single-chunk item writes the normalized output straight into the O GEMM's
 // hi/lo operand; multi-chunk items write (m, l, unnormalized O) partials that
 // attn_combine merges.
-#include "common.h"
-#include "kernels.h"
+#include "attn.h"
 
 namespace hvd {
 
-// Item reads go through the constant address space: items are read-only
-// while attention runs, and uniform addresses there become scalar loads
-// whose results (the first sub-chunk's page ids included) sit in SGPRs.
-typedef const __attribute__((address_space(4))) AttnItem ConstItem;
-
-// NP = pages staged per sub-chunk (the launch picks it from the chunk
-// length), so short decode chunks issue only the loads they need.  NW waves
-// hold TPW row tiles each: an item covers up to 16*NW*TPW query rows (64 for
-// short drafts, up to 256 so one item covers all rows of a long draft and
-// its keys are read once).
-// Workgroups per CU the register budget is sized for: two 4-wave
-// workgroups share a CU while their staged sub-chunks fit LDS together.
-constexpr int attn_occupancy(int DH, int NP, int NW) { return NW == 4 && NP * kPage * DH <= 64 * 128 ? 2 : 1; }
-
 template <int DH, int NP, int NW, int TPW>
 __global__ __launch_bounds__(64 * NW, attn_occupancy(DH, NP, NW)) void verify_attn(AttnArgs a) {
-  constexpr int NT = 64 * NW;           // threads
-  constexpr int RPI = 16 * NW * TPW;    // query rows per item
-  constexpr int CH = NP * kPage;        // positions per sub-chunk
-  constexpr int KSEG = DH / 8;          // 16-byte segments per K row
-  constexpr int VU = CH / 4;            // 8-byte units per V row in LDS
-  constexpr int VM = VU < 16 ? VU : 16; // V swizzle span (units)
-  constexpr int LPP = 4 * DH / NT;      // 16-byte loads per thread per page (K and V: 4*DH units)
-  static_assert(NP >= 2 && NP <= kItemPages && (NP & (NP - 1)) == 0, "pages per sub-chunk");
-  static_assert(LPP >= 1 && LPP * NT == 4 * DH, "page units per thread");
-  // Sub-chunks of up to 4 pages are double-buffered in LDS: a sub-chunk is
-  // staged into the buffer its predecessor's predecessor used, which every
-  // wave has finished reading once it passed the previous staging barrier,
-  // so one barrier per sub-chunk suffices.
-  constexpr bool DB = NP <= 4;
-  constexpr int BUF_BYTES = CH * DH * 2 * 2;       // K and V of one sub-chunk
   extern __shared__ __align__(16) unsigned char smem[];
-  _Float16* sK = (_Float16*)smem;                  // [CH][DH], segment-swizzled
-  _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], 8-byte-unit-swizzled
-
-  ConstItem* ip = (ConstItem*)a.items + blockIdx.x;
-  const int kdr = ip->k;
-  if (kdr < 0) return;  // grid padding
-  const int slot = ip->slot, ctx = ip->ctx, cu = ip->cu, g = ip->g;
-  const int nch = ip->nch, rg = ip->rg, part = ip->part;
-  const bool tree = ip->tree != 0;  // token tree: rows see the context and their own path
-  const int p_begin = ip->p_begin, p_end = ip->p_end;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int G = a.group;
-  const int R = (kdr + 1) * G;
-  const int lg = lane >> 4;
-  const size_t vhalf = (size_t)a.Hkv * kPage * DH;
-  const _Float16* kvg = a.kv + (size_t)g * kPage * DH;  // this kv head's K block in a page
-
-  // per-wave state of its (up to) TPW 16-row tiles, kept across sub-chunks
-  int tile_row[TPW];
-  bool tile_on[TPW];
-  f16x8 qf[TPW][DH / 32];
-  float m[TPW], lsum[TPW];
-  f32x4 o[TPW][DH / 16];
-#pragma unroll
-  for (int q = 0; q < TPW; ++q) {
-    m[q] = -INFINITY;
-    lsum[q] = 0.f;
-    const int row_base = rg * RPI + (wave + NW * q) * 16;
-    tile_on[q] = row_base < R;
-    tile_row[q] = row_base + (lane & 15);
-#pragma unroll
-    for (int d = 0; d < DH / 16; ++d) o[q][d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  // ---- K/V loads of one sub-chunk, all in flight at once (page-major: per
-  // page, units [0, 2DH) are K rows, [2DH, 4DH) V rows of the head).  Pages
-  // past the sub-chunk's end repeat its first page (in-bounds, cached; their
-  // V is zeroed when staged).  The next sub-chunk's loads are issued before
-  // the current one is computed, so its latency hides behind the MFMAs.
-  // tree rows: ancestor sets (rows past R take the last row's)
-  uint64_t anc[TPW];
-#pragma unroll
-  for (int q = 0; q < TPW; ++q) {
-    const int r = tile_row[q];
-    anc[q] = tree ? a.tree_mask[cu + (r < R ? r / G : kdr)] : 0;
-  }
-  // query fragments (rows past R read a valid row; their results are dropped)
-#pragma unroll
-  for (int q = 0; q < TPW; ++q) {
-    const int r = tile_row[q];
-    const int i = r < R ? r / G : kdr;
-    const int h = g * G + (r < R ? r % G : 0);
-#pragma unroll
-    for (int kd = 0; kd < DH / 32; ++kd)
-      qf[q][kd] = *(const f16x8*)(a.Q + ((size_t)(cu + i) * a.Hq + h) * DH + kd * 32 + lg * 8);
-  }
-  u32x4 buf[NP][LPP];
-  auto issue = [&](const int (&pgid)[NP]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-      for (int j = 0; j < LPP; ++j) {
-        const int u = j * NT + tid;
-        const size_t off = u < 2 * DH ? (size_t)u * 8 : vhalf + (size_t)(u - 2 * DH) * 8;
-        buf[p][j] = *(const u32x4*)(kvg + (size_t)pgid[p] * a.page_stride + off);
-      }
-  };
-  {
-    int pgid[NP];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) pgid[p] = ip->pages[p];
-    issue(pgid);
-  }
-  // pool pages of the next sub-chunk to issue, one per lane (lane p < NP:
-  // page p; past the sub-chunk's end, its first page), loaded a sub-chunk
-  // ahead so issuing never waits on a page-table read
-  auto next_pages = [&](int nsub) __attribute__((always_inline)) {
-    const int np_sub = (min(CH, p_end - nsub) + kPage - 1) / kPage;
-    return a.pt[(size_t)slot * a.pt_stride + (nsub >> 4) + (lane < np_sub ? lane : 0)];
-  };
-  int pg_next = p_begin + CH < p_end ? next_pages(p_begin + CH) : 0;
-  // Wait here for everything issued so far (the first sub-chunk is staged
-  // right after anyway): the waitcnt pass then knows the query fragments are
-  // in, and places no wait for them inside the loop, where it would also
-  // wait for the next sub-chunk's loads.
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-
-  int nbuf = 0;
-  for (int sub = p_begin; sub < p_end; sub += CH) {
-    const int n_pos = min(CH, p_end - sub);
-    if constexpr (DB) {
-      sK = (_Float16*)(smem + nbuf * BUF_BYTES);
-      sV = (_Float16*)(smem + nbuf * BUF_BYTES + CH * DH * 2);
-      nbuf ^= 1;
-    } else {
-      if (sub != p_begin) __syncthreads();  // previous sub-chunk fully consumed
-    }
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-      for (int j = 0; j < LPP; ++j) {
-        const int u = j * NT + tid;
-        u32x4 x = buf[p][j];
-        if (u < 2 * DH) {
-          const int t = u / KSEG, sgm = u % KSEG;
-          const int pos = p * kPage + t;
-          *(u32x4*)(sK + pos * DH + ((sgm ^ (pos & 15)) & (KSEG - 1)) * 8) = x;
-        } else {
-          const int v = u - 2 * DH;
-          const int d = v >> 1, hh = v & 1;
-          // 8 positions pp .. pp+7 of row d; positions past the end are
-          // zeroed (their probabilities are 0, and stale values must not
-          // turn that into NaN)
-          const int pp = p * kPage + hh * 8;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t keep = (pp + 2 * e + 1 < n_pos) ? 0xffffffffu : (pp + 2 * e < n_pos ? 0xffffu : 0u);
-            x[e] &= keep;
-          }
-          const int u0 = pp >> 2;  // 8-byte units (4 positions)
-          uint2* row = (uint2*)(sV + (size_t)d * CH);
-          row[(u0 & ~(VM - 1)) | ((u0 & (VM - 1)) ^ (d & (VM - 1)))] = uint2{x[0], x[1]};
-          row[((u0 + 1) & ~(VM - 1)) | (((u0 + 1) & (VM - 1)) ^ (d & (VM - 1)))] = uint2{x[2], x[3]};
-        }
-      }
-    __syncthreads();
-    if (sub + CH < p_end) {
-      int pgid[NP];
-#pragma unroll
-      for (int p = 0; p < NP; ++p) pgid[p] = __builtin_amdgcn_readlane(pg_next, p);
-      issue(pgid);
-      if (sub + 2 * CH < p_end) pg_next = next_pages(sub + 2 * CH);
-    }
-
-    // The wave's row tiles over the sub-chunk in groups of SG 16-position
-    // blocks: all scores S^T = K Q^T of a group first (independent
-    // accumulator chains; each K fragment read from LDS once and used by
-    // every tile of the wave), one online-softmax update per tile, then
-    // O^T += V^T P^T over the group's block pairs (each V fragment read once
-    // for all tiles).  Every position is computed; those past the end are
-    // masked, so no load is conditional.  Tile 0 is live whenever any is.
-    constexpr int NB = CH / 16;                      // 16-position blocks
-    constexpr int SG = NB < 4 / TPW ? NB : 4 / TPW;  // blocks per score group (register budget)
-    if (tile_on[0]) {
-      int lim[TPW];  // last visible position of each tile's rows, sub-chunk-relative
-#pragma unroll
-      for (int q = 0; q < TPW; ++q) {
-        const int r = tile_row[q];
-        lim[q] = ctx + (r < R ? r / G : kdr) - sub;
-      }
-      // smallest of them over the wave (its first row: rows ascend)
-      const int lim_min = tree ? ctx - 1 - sub : ctx + (rg * RPI + wave * 16) / G - sub;
-#pragma unroll 1
-      for (int g0 = 0; g0 < NB; g0 += SG) {  // not unrolled: keeps each group's LDS reads in its group
-        f32x4 sc[TPW][SG];
-#pragma unroll
-        for (int kd = 0; kd < DH / 32; ++kd) {
-          const int sg = kd * 4 + lg;
-          f16x8 kf[SG];
-#pragma unroll
-          for (int b = 0; b < SG; ++b) {
-            const int p = (g0 + b) * 16 + (lane & 15);
-            kf[b] = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
-          }
-#pragma unroll
-          for (int q = 0; q < TPW; ++q)
-            if (q == 0 || tile_on[q]) {
-#pragma unroll
-              for (int b = 0; b < SG; ++b)
-                sc[q][b] = mfma_f16(kf[b], qf[q][kd], kd ? sc[q][b] : f32x4{0.f, 0.f, 0.f, 0.f});
-            }
-        }
-        f16x8 pf[TPW][SG / 2 > 0 ? SG / 2 : 1];
-        // whole group visible to every row of the wave (wave-uniform): no mask
-        const bool full = (g0 + SG) * 16 <= min(lim_min + 1, n_pos);
-#pragma unroll
-        for (int q = 0; q < TPW; ++q) {
-          if (q > 0 && !tile_on[q]) continue;
-          // running max m in log2 units; scores scaled inside the exp2's fma
-          float bm = -INFINITY;
-          if (full) {
-#pragma unroll
-            for (int b = 0; b < SG; ++b)
-#pragma unroll
-              for (int j = 0; j < 4; ++j) bm = fmaxf(bm, sc[q][b][j]);
-          } else {
-#pragma unroll
-            for (int b = 0; b < SG; ++b)
-#pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const int pa = (g0 + b) * 16 + lg * 4 + j;
-                bool vis = pa <= lim[q];
-                if (tree) {  // the context, then the row's ancestors (bit j = position ctx + j)
-                  const int rel = pa + sub - ctx;
-                  vis = rel < 0 || ((anc[q] >> (rel & 63)) & 1);
-                }
-                sc[q][b][j] = (vis && pa < n_pos) ? sc[q][b][j] : -INFINITY;
-                bm = fmaxf(bm, sc[q][b][j]);
-              }
-          }
-          bm = fmaxf(bm, __shfl_xor(bm, 16));
-          bm = fmaxf(bm, __shfl_xor(bm, 32));
-          const float mn = fmaxf(m[q], bm * a.scale_log2);
-          const float ms = mn == -INFINITY ? 0.f : mn;  // nothing visible yet: every weight is 0
-          const float alpha = __builtin_amdgcn_exp2f(m[q] - ms);
-          float ps = 0.f;
-#pragma unroll
-          for (int b = 0; b < SG; ++b)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              sc[q][b][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][b][j], a.scale_log2, -ms));
-              ps += sc[q][b][j];
-            }
-          lsum[q] = lsum[q] * alpha + ps;
-          m[q] = mn;
-          if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {  // the max moved for some row
-#pragma unroll
-            for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
-          }
-          // B operand of block pair c: positions 32c' + {4lg..4lg+3} and
-          // 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
-#pragma unroll
-          for (int c = 0; c < SG / 2; ++c)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              pf[q][c][j] = (_Float16)sc[q][2 * c][j];
-              pf[q][c][4 + j] = (_Float16)sc[q][2 * c + 1][j];
-            }
-        }
-#pragma unroll
-        for (int c = 0; c < SG / 2; ++c) {
-          const int ua = 4 * g0 + 8 * c + lg, ub = ua + 4;
-          uint2 va[DH / 16], vb[DH / 16];
-#pragma unroll
-          for (int dt = 0; dt < DH / 16; ++dt) {
-            const int d = dt * 16 + (lane & 15);
-            const uint2* row = (const uint2*)(sV + (size_t)d * CH);
-            va[dt] = row[(ua & ~(VM - 1)) | ((ua & (VM - 1)) ^ (d & (VM - 1)))];
-            vb[dt] = row[(ub & ~(VM - 1)) | ((ub & (VM - 1)) ^ (d & (VM - 1)))];
-          }
-#pragma unroll
-          for (int q = 0; q < TPW; ++q)
-            if (q == 0 || tile_on[q]) {
-#pragma unroll
-              for (int dt = 0; dt < DH / 16; ++dt) {
-                const u32x4 vv = {va[dt].x, va[dt].y, vb[dt].x, vb[dt].y};
-                o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf[q][c], o[q][dt]);
-              }
-            }
-        }
-      }
-    }
-  }
-
-#pragma unroll
-  for (int q = 0; q < TPW; ++q) {
-    if (!tile_on[q]) continue;
-    float l = lsum[q];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int r = tile_row[q];
-    const bool rvalid = r < R;
-    if (nch == 1) {
-      if (rvalid) {
-        const int i = r / G, h = g * G + r % G;
-        const float inv = l > 0.f ? 1.f / l : 0.f;
-        const int row = cu + i;
-#pragma unroll
-        for (int dt = 0; dt < DH / 16; ++dt) {
-          const int col = h * DH + dt * 16 + lg * 4;
-          uint16_t hi[4], lo[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) split_f16(o[q][dt][j] * inv, hi[j], lo[j]);
-          const size_t off = afrag_off(row, col, a.MTtot);
-          *(uint2*)(a.Ohi + off) = uint2{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16)};
-          *(uint2*)(a.Olo + off) = uint2{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16)};
-        }
-      }
-    } else {
-      const int lr = (wave + NW * q) * 16 + (lane & 15);
-      const size_t ps = (size_t)part * RPI + lr;
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt)
-        *(float4*)(a.part_o + ps * DH + dt * 16 + lg * 4) =
-            float4{o[q][dt][0], o[q][dt][1], o[q][dt][2], o[q][dt][3]};
-      if (lg == 0) *(float2*)(a.part_ml + ps * 2) = float2{m[q], l};
-    }
-  }
+  NoHooks hk;
+  attn_item<DH, NP, NW, TPW, false>(a, (ConstItem*)a.items + blockIdx.x, smem, hk);
 }
 
-// Merge the chunk partials of one (sequence, kv head, row group):
-// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c.  The merge is
-// latency-bound, so QS lanes share one (row, 8 dims): lane q takes chunks
-// q, q + QS, ... as a running (M, L, acc) merge over batches whose loads are
-// all issued before any is used, and the QS lanes then merge by shuffles.
-// One block per (head entry, slice of RPB rows); a.max_rows bounds the
-// slices per entry.  QS is 8 for short drafts (few rows to spread over) and
-// smaller when an entry has more rows, so blocks past a short entry's rows
-// stay few.
 template <int DH, int QS>
 __global__ __launch_bounds__(256) void attn_combine(CombineArgs a) {
-  constexpr int OCT = DH / 8;            // 8-dim octets per row
-  constexpr int RPB = 256 / (OCT * QS);  // rows per block
-  constexpr int NB = 8;                  // chunks per lane per batch
+  constexpr int RPB = 256 / (DH / 8 * QS);
   const int spb = (a.max_rows + RPB - 1) / RPB;
   const AttnItem hd = a.heads[blockIdx.x / spb];
   if (hd.k < 0) return;  // grid padding
-  const int slice = blockIdx.x % spb;
-  const int G = a.group;
-  const int R = (hd.k + 1) * G;
-  const int t = threadIdx.x;
-  const int qq = t % QS, o8 = (t / QS % OCT) * 8;
-  const int lr = slice * RPB + t / (QS * OCT);
-  const int r = hd.rg * a.rpi + lr;
-  if (lr >= a.rpi || r >= R) return;  // the QS lanes of a row leave together
-  const float* ml = a.part_ml + ((size_t)hd.part * a.rpi + lr) * 2;
-  const float* po = a.part_o + ((size_t)hd.part * a.rpi + lr) * DH + o8;
-  const size_t cstride_ml = (size_t)a.rpi * 2, cstride_o = (size_t)a.rpi * DH;
-  float M = -INFINITY, L = 0.f;
-  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int c0 = qq; c0 < hd.nch; c0 += QS * NB) {
-    float2 mlc[NB];
-    float4 x0[NB], x1[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int c = c0 + j * QS;
-      mlc[j] = float2{-INFINITY, 0.f};
-      x0[j] = x1[j] = float4{0.f, 0.f, 0.f, 0.f};
-      if (c < hd.nch) {
-        mlc[j] = *(const float2*)(ml + c * cstride_ml);
-        x0[j] = *(const float4*)(po + c * cstride_o);
-        x1[j] = *(const float4*)(po + c * cstride_o + 4);
-      }
-    }
-    float Mn = M;
-#pragma unroll
-    for (int j = 0; j < NB; ++j) Mn = fmaxf(Mn, mlc[j].x);
-    const float sc = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
-    L *= sc;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] *= sc;
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const float w = (mlc[j].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mlc[j].x - Mn);
-      L += w * mlc[j].y;
-      acc[0] += w * x0[j].x; acc[1] += w * x0[j].y; acc[2] += w * x0[j].z; acc[3] += w * x0[j].w;
-      acc[4] += w * x1[j].x; acc[5] += w * x1[j].y; acc[6] += w * x1[j].z; acc[7] += w * x1[j].w;
-    }
-    M = Mn;
-  }
-  // merge the QS lanes of this (row, octet)
-  float Mx = M;
-#pragma unroll
-  for (int o = 1; o < QS; o *= 2) Mx = fmaxf(Mx, __shfl_xor(Mx, o));
-  const float sc = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mx);
-  L *= sc;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] *= sc;
-#pragma unroll
-  for (int o = 1; o < QS; o *= 2) {
-    L += __shfl_xor(L, o);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o);
-  }
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  const int i = r / G, h = hd.g * G + r % G;
-  uint16_t hi[8], lo[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) split_f16(acc[j] * inv, hi[j], lo[j]);
-  const size_t off = afrag_off(hd.cu + i, h * DH + o8, a.MTtot);
-  if (qq == 0 || QS == 1)
-    *(uint4*)(a.Ohi + off) = uint4{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16),
-                                   hi[4] | ((uint32_t)hi[5] << 16), hi[6] | ((uint32_t)hi[7] << 16)};
-  if (qq == 1 || QS == 1)
-    *(uint4*)(a.Olo + off) = uint4{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16),
-                                   lo[4] | ((uint32_t)lo[5] << 16), lo[6] | ((uint32_t)lo[7] << 16)};
+  combine_slice<DH, QS, 256, false>(a, hd, blockIdx.x % spb);
 }
 
 int attn_pages_per_sub(int chunk) {

@@ -68,6 +68,60 @@ __device__ __forceinline__ float load_dev(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+__device__ __forceinline__ void st_u32_dev(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u16_dev(uint16_t* p, uint16_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u64_dev(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_u32_dev(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_u64_dev(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// 16-byte device-scope loads and stores: raw buffer accesses with the sc1
+// cache policy over a buffer that starts at `base` (wave-uniform) and is
+// addressed by a byte offset below 2^31.
+constexpr int kCachePolicySc1 = 16;
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, kBufferWord3);
+}
+__device__ __forceinline__ u32x4 ld_16_dev(const void* base, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(buf_rsrc(base), byte_off, 0, kCachePolicySc1);
+}
+__device__ __forceinline__ float4 ld_f4_dev(const void* base, uint32_t byte_off) {
+  const u32x4 v = ld_16_dev(base, byte_off);
+  return float4{__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w)};
+}
+__device__ __forceinline__ void st_16_dev(void* base, uint32_t byte_off, uint4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, buf_rsrc(base), byte_off, 0, kCachePolicySc1);
+}
+__device__ __forceinline__ void st_f4_dev(void* base, uint32_t byte_off, float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                                               __float_as_uint(v.w)},
+                                         buf_rsrc(base), byte_off, 0, kCachePolicySc1);
+}
+// fp16 bits of (lo, hi) packed into one 32-bit word (lo in the low half)
+__device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+}
+
+// Synchronisation points of work done inside a larger kernel (the one-launch
+// verify step): wait() runs once the work's first constant inputs (weights,
+// cached K/V) are requested and before any input another workgroup of the
+// same kernel produces is read; done() runs after the work's outputs are
+// written.  Stand-alone kernels use these no-ops.
+struct NoHooks {
+  __device__ __forceinline__ void wait() {}
+  __device__ __forceinline__ void done() {}
+};
+
 __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   return v;

@@ -86,6 +86,7 @@ struct GemmArgs {
   const float2* rope;  // [max_pos][dh/2] (cos, sin)
   // EPI_RESID
   float* X;            // residual stream [MTtot*16][D] fp32
+  float* X_out;        // nullable: the updated stream goes here instead of X
   int D;
   const float* gain_next;  // gain of the norm that consumes X next
   uint16_t* Nhi;       // next GEMM's A operand (hi), K = D
@@ -151,6 +152,8 @@ struct EmbedArgs {
   int32_t* pt;
   int pt_stride;
   int V;  // token ids outside [0, V) gather row 0 (they can never be accepted)
+  uint32_t* zero;  // nullable: n_zero words cleared before the step (one-launch step counters)
+  int n_zero;
 };
 
 struct AcceptArgs {
@@ -172,6 +175,7 @@ struct AcceptArgs {
   int32_t* astate;
   int32_t* hist;
   int hist_cap;
+  const uint32_t* flow_err;  // nullable: the one-launch step's error word, copied to out[2B]
 };
 // Moves the K/V of each tree sequence's accepted path from the nodes'
 // positions (ctx + 1 + node) to the chain positions ctx + 1 .. ctx + a.
@@ -214,6 +218,69 @@ struct AsyncPlanArgs {
   int M, B;
 };
 
+// One-launch verify step (flow.hip): every layer's QKV GEMM, attention,
+// split-KV merge, O, gate/up and down GEMMs, then the LM head, as one grid.
+// Workgroup w takes the role its index gives (layer, phase, unit); roles of
+// later phases have larger indices, so a workgroup only ever waits for work
+// of smaller indices, which the in-order dispatch has already started.
+// Finished output blocks are counted per layer and phase; a consumer
+// requests its weights (and cached K/V) first, waits (bounded, see err)
+// until its inputs are complete, then reads them with device-scope loads.
+// One layer's weights, KV pool and activation buffers.  In the one-launch
+// step every activation buffer is written once per launch and read only
+// after its producers are complete, so readers use ordinary (L2-cached)
+// loads: no buffer is shared by two layers.
+struct FlowLayer {
+  const uint4 *qkv, *o, *gu, *down;  // packed weights
+  const float *g_attn, *g_mlp;        // norm gains
+  _Float16* kv;                        // this layer's KV pool
+  // input: residual stream, next norm's operand (hi, lo), sums of squares
+  // (the previous layer's output; the embedding's for layer 0)
+  const float* x_in;
+  const uint16_t *n_in_hi, *n_in_lo;
+  const float* ss_in;
+  float* x_mid;  // after attention + O
+  uint16_t *n_mid_hi, *n_mid_lo;
+  float* ss_mid;
+  float* x_out;  // after the MLP
+  uint16_t *n_out_hi, *n_out_lo;
+  float* ss_out;
+  _Float16* q;                   // rotated queries
+  uint16_t *o_hi, *o_lo;         // attention output (O GEMM operand)
+  uint16_t *a_hi, *a_lo;         // SiLU(gate) * up (down GEMM operand)
+};
+enum { FL_QKV = 0, FL_ATTN = 1, FL_MERGE = 2, FL_O = 3, FL_GU = 4, FL_DOWN = 5, FL_PHASES = 6 };
+enum { FG_QKV = 0, FG_O = 1, FG_GU = 2, FG_DOWN = 3, FG_LM = 4, FG_N = 5 };
+struct FlowArgs {
+  const FlowLayer* layers;  // [L] (device)
+  int L;
+  GemmArgs g[FG_N];         // per GEMM role; W / kv / gains / counters set per layer in the kernel
+  int ns[FG_N], splits[FG_N], n_cb[FG_N];
+  const float* g_final;     // gain of the final norm (read by the last down GEMM's epilogue)
+  AttnArgs attn;            // kv set per layer
+  CombineArgs comb;
+  int np;                   // attention pages per sub-chunk
+  int per_layer;            // workgroups of one layer
+  int ph[FL_PHASES + 1];    // first workgroup of each phase within a layer (ph[FL_PHASES] = per_layer)
+  int n_lm;                 // LM-head workgroups after the layers
+  const AttnItem* items;    // attention items of one layer (pad4: merge unit of a multi-chunk item)
+  const AttnItem* heads;    // merge entries (pad4: merge unit)
+  int merge_spb;            // row slices per merge entry
+  // counters, `cstride` per layer: [0, Hkv) finished QKV blocks per kv-head
+  // group; [c_unit, +units) finished chunks per merge unit; then 8-way split
+  // counters (indexed by block & 7) of O inputs (single-chunk items and merge
+  // slices), O, gate/up and down output blocks
+  uint32_t* cnt;
+  int cstride, c_unit, c_oin, c_o, c_gu, c_down;
+  uint32_t qkv_group_target;  // QKV output blocks per kv-head group
+  uint32_t oin_target;        // single-chunk items + merge slices per layer
+  uint32_t* err;              // set (bit 0) if a wait gave up: results are then invalid
+  int G, dh;
+  // nullable diagnostics: per workgroup {start, inputs ready, end} in the
+  // 100 MHz constant clock and the hardware id (XCD, CU) it ran on
+  uint64_t* trace;
+};
+
 // Launchers: all enqueue on `s` and return the launch status.
 hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst, int N, int K,
                        hipStream_t s);
@@ -236,11 +303,18 @@ hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, i
 // max_np caps the pages staged per sub-chunk (longer chunks loop over sub-chunks)
 hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_item, int max_np, hipStream_t s);
 hipError_t attn_set_lds_limit();  // once per process, before the first launch
+int attn_pages_per_sub(int chunk);        // pages one sub-chunk stages for a chunk length
+size_t attn_lds_bytes(int dh, int np);    // LDS of a workgroup staging np-page sub-chunks
 hipError_t launch_combine(const CombineArgs& a, int n_heads, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int B, hipStream_t s);
 hipError_t launch_async_plan(const AsyncPlanArgs& a, hipStream_t s);
 hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* pt, int pt_stride, hipStream_t s);
+// One-launch verify step over MT (1 or 2) row tiles; false if this shape has
+// no compiled variant (head dim, strips per workgroup, pages per sub-chunk).
+bool flow_supported(int MT, int dh, int np, const int* ns);
+hipError_t launch_flow(const FlowArgs& f, int MT, hipStream_t s);
+hipError_t flow_set_lds_limit();  // once per process, before the first launch
 
 constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
 

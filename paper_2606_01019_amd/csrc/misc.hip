@@ -51,6 +51,7 @@ __global__ __launch_bounds__(256) void embed_rows(EmbedArgs a) {
   if (blockIdx.x == 0)
     for (int u = threadIdx.x, n = *a.n_upd; u < n; u += blockDim.x)
       a.pt[(size_t)a.upd[u * 3] * a.pt_stride + a.upd[u * 3 + 1]] = a.upd[u * 3 + 2];
+  for (int u = blockIdx.x * 256 + threadIdx.x; u < a.n_zero; u += gridDim.x * 256) a.zero[u] = 0u;
   const int R = blockIdx.x;
   const bool valid = R < a.M;
   int tok = valid ? a.rows[R].tok : 0;
@@ -182,6 +183,7 @@ __global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
   }
   __syncthreads();  // every thread has read the step count
   if (threadIdx.x == 0) {
+    if (a.flow_err) a.out[2 * a.B] = (int32_t)*a.flow_err;
     *a.counter = 0u;
     if (a.astate) a.astate[2 * a.B] = step + 1;
   }

@@ -20,10 +20,12 @@ _STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM
 EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
            "hvd_prefill", "hvd_verify", "hvd_verify_tree", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
            "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error",
-           "hvd_async_begin", "hvd_async_step", "hvd_async_end", "hvd_verify_noalloc")
+           "hvd_async_begin", "hvd_async_step", "hvd_async_end", "hvd_verify_noalloc", "hvd_flow_trace")
 HVD_OPT_GRAPHS = 1
 HVD_OPT_MLP_SINGLE = 2
 HVD_OPT_LM_SINGLE = 3
+HVD_OPT_FLOW = 4
+HVD_OPT_FLOW_ITEMS = 5
 MAX_TREE_NODES = 63  # nodes per token tree (hvd_verify_tree)
 
 
@@ -91,6 +93,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hvd_async_begin": (I32, [P, P, I32, PI32, PI32, PI32, I32, P, P, P, P, I32, PI32, ctypes.POINTER(P)]),
         "hvd_async_step": (I32, [P, I32]),
         "hvd_async_end": (I32, [P, PI32]),
+        "hvd_flow_trace": (I32, [P, P, ctypes.c_int64]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -256,6 +259,24 @@ class KVCache:
         """Large-batch verify LM head on the fp16 activation alone (default)
         or on the fp16 hi + lo pair."""
         _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_LM_SINGLE, 1 if on else 0))
+
+    def set_flow(self, on: bool):
+        """One-launch verify step for batches of at most 32 rows, or one
+        kernel launch per GEMM / attention pass (the default)."""
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_FLOW, 1 if on else 0))
+
+    def set_flow_items(self, n: int):
+        """Attention work items the one-launch step aims for (tuning)."""
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_FLOW_ITEMS, int(n)))
+
+    def flow_trace(self, buf=None):
+        """Record a per-workgroup timeline of one-launch steps into buf (an
+        int64 CUDA tensor, 4 words per workgroup), or stop (None)."""
+        if buf is None:
+            _check(self.lib.hvd_flow_trace(self.handle, None, 0))
+        else:
+            assert buf.is_cuda and buf.element_size() == 8 and buf.is_contiguous()
+            _check(self.lib.hvd_flow_trace(self.handle, ctypes.c_void_p(buf.data_ptr()), buf.numel()))
 
     def set_graphs(self, on: bool):
         """Replay step kernels from cached HIP graphs, or launch eagerly (default)."""
