@@ -20,6 +20,11 @@
  * pairing, grouped-query attention, SwiGLU MLP, untied LM head), bf16 weights.
  * The KV cache holds fp16 (the paper's data type, App. A) in 16-token pages.
  *
+ * The paper defines only Verify and the commit of its block (Alg. 1).  The
+ * other calls -- model loading, KV cache creation, prefill, truncate,
+ * sequence free, the device-resident loop, options, profiling and
+ * diagnostics -- are this library's own plumbing around them.
+ *
  * Conventions for every call:
  *  - Host pointers (const T* / T*) are owned by the caller and read or written
  *    only during the call.  "device" pointers point to GPU memory.
@@ -274,8 +279,27 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   attention pass (measured faster at batch 1).  Results agree within
  *   rounding (the attention split may differ).
  * HVD_OPT_FLOW_ITEMS (default 128): attention work items the one-launch step
- *   aims for (longer KV chunks when fewer); a tuning knob. */
-enum { HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3, HVD_OPT_FLOW = 4, HVD_OPT_FLOW_ITEMS = 5 };
+ *   aims for (longer KV chunks when fewer); a tuning knob.
+ *
+ * Tuning overrides of the launch policy (for measurements and tests; results
+ * stay within the verify step's tolerance whatever they are set to):
+ * HVD_OPT_GEMM_MIN_BLOCKS (192): GEMM workgroups below which the skinny GEMM
+ *   changes shape.  HVD_OPT_ATTN_MIN_ITEMS (256): attention items a launch
+ *   aims for.  HVD_OPT_ATTN_MAX_NP (16): most KV pages one attention
+ *   sub-chunk stages (power of two, 2..16).  HVD_OPT_SKINNY_MAX_MT (8): row
+ *   tiles above which GEMMs take the MFMA-tiled kernel.  HVD_OPT_NS8_MT3 (1):
+ *   8-strip skinny blocks at three and four single-pass row tiles.
+ *   HVD_OPT_PREFILL_ROWS (0 = policy): prefill chunk rows, a multiple of 16.
+ * HVD_OPT_GEMM_SHAPE + f, f = 0 QKV, 1 O, 2 gate/up, 3 down, 4 LM head:
+ *   skinny GEMM shape of that GEMM, strips * 100 + K splits (0 = policy).
+ * HVD_OPT_TILED_SHAPE + f: tiled GEMM shape, (tile + 1) * 100 + K splits
+ *   (tile 0 = 128x128, 1 = 128x256, 2 = 256x256 / 8 waves, 3 = 256x256 / 4
+ *   waves; 0 = policy). */
+enum {
+  HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3, HVD_OPT_FLOW = 4, HVD_OPT_FLOW_ITEMS = 5,
+  HVD_OPT_GEMM_MIN_BLOCKS = 10, HVD_OPT_ATTN_MIN_ITEMS = 11, HVD_OPT_ATTN_MAX_NP = 12, HVD_OPT_SKINNY_MAX_MT = 13,
+  HVD_OPT_NS8_MT3 = 14, HVD_OPT_PREFILL_ROWS = 15, HVD_OPT_GEMM_SHAPE = 16, HVD_OPT_TILED_SHAPE = 24
+};
 hvd_status hvd_kv_set_option(hvd_kv kv, int32_t option, int32_t value);
 
 /* Diagnostics of the one-launch step (HVD_OPT_FLOW): while dev_buf (DEVICE,
@@ -285,6 +309,14 @@ hvd_status hvd_kv_set_option(hvd_kv kv, int32_t option, int32_t value);
  * constant-rate device clock) and the hardware id it ran on (XCD << 32 |
  * HW_ID).  dev_buf NULL stops tracing.  Not needed for results. */
 hvd_status hvd_flow_trace(hvd_kv kv, uint64_t* dev_buf, int64_t n_words);
+
+/* Measure the dense fp16 MFMA rate of the current GPU (not a step of the
+ * verify path; a reference for the MFMA fractions the benchmark quotes):
+ * every SIMD runs waves of register-only MFMA 32x32x16 f16 chains on
+ * stream (hipStream_t, NULL = default) for a few milliseconds; *tflops
+ * receives the best of three timed launches.  Returns 0, or a negative
+ * hvd_status. */
+int hvd_measure_mfma_peak(void* stream, double* tflops);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* hvd_last_error(void);

@@ -38,10 +38,8 @@ constexpr size_t kAlign = 256;
 // Prefill chunk: rows whose query rows per kv head (rows x group) come to
 // 2048, between 128 and 512 rows (measured: 512 rows for the 8B shape,
 // group 4, above 256 and 1024; 256 for the 32B shape, group 8, above 512).
-// HVD_PREFILL_ROWS overrides it for sweeps.
+// HVD_OPT_PREFILL_ROWS overrides it per handle (up to this size).
 int prefill_rows(const hvd_config& c) {
-  static const int forced = getenv("HVD_PREFILL_ROWS") ? atoi(getenv("HVD_PREFILL_ROWS")) : 0;
-  if (forced >= 16) return forced / 16 * 16;
   const int G = c.n_q_heads / c.n_kv_heads;
   return std::max(128, std::min(512, 2048 / G));
 }
@@ -359,6 +357,7 @@ struct hvd_kv_s {
   int32_t* lm_idx = nullptr;
   int n_part_lm = 0;
   int gemm_min_blocks = kGemmMinBlocks;
+  int prefill_rows = 0;  // prefill chunk rows (0: the policy of prefill_rows())
   bool use_graphs = false;
   std::map<GraphKey, hipGraphExec_t> graphs;
   int attn_min_items = kAttnMinItems;
@@ -569,52 +568,6 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
     }
   }
   k->hs = new HostState(max_seqs, n_pages, kPage, c.max_pos, c.max_draft, c.vocab);
-  if (const char* e = getenv("HVD_GEMM_MIN_BLOCKS")) k->gemm_min_blocks = std::max(1, atoi(e));
-  if (const char* e = getenv("HVD_ATTN_MIN_ITEMS")) k->attn_min_items = std::max(1, atoi(e));
-  if (const char* e = getenv("HVD_ATTN_MAX_NP")) k->attn_max_np = std::max(2, std::min(kItemPages, atoi(e)));
-  if (const char* e = getenv("HVD_GRAPHS")) k->use_graphs = atoi(e) != 0;
-  if (const char* e = getenv("HVD_SKINNY_MAX_MT")) k->skinny_max_mt = std::max(1, std::min(64, atoi(e)));
-  if (const char* e = getenv("HVD_NS8_MT3")) k->ns8_mt3 = atoi(e) != 0;
-  // tuning override of the skinny GEMM shape: "qkv=2:1,o=1:1" (family=strips:splits)
-  if (const char* e = getenv("HVD_GEMM_SHAPE")) {
-    static const char* names[PF_LM + 1] = {"qkv", "o", "gateup", "down", "lm"};
-    std::string spec(e);
-    size_t at = 0;
-    while (at < spec.size()) {
-      size_t end = spec.find(',', at);
-      if (end == std::string::npos) end = spec.size();
-      const std::string item = spec.substr(at, end - at);
-      int ns = 0, sp = 0;
-      const size_t eq = item.find('=');
-      if (eq != std::string::npos && sscanf(item.c_str() + eq + 1, "%d:%d", &ns, &sp) == 2)
-        for (int f = 0; f <= PF_LM; ++f)
-          if (item.compare(0, eq, names[f]) == 0 && (ns == 1 || ns == 2 || ns == 4 || ns == 8) && sp >= 1 && sp <= 16) {
-            k->gemm_force[f][0] = ns;
-            k->gemm_force[f][1] = sp;
-          }
-      at = end + 1;
-    }
-  }
-  // tuning override of the tiled GEMM: "down=2:4" (family=tile:splits, tile 0..3)
-  if (const char* e = getenv("HVD_TILED_SHAPE")) {
-    static const char* names[PF_LM + 1] = {"qkv", "o", "gateup", "down", "lm"};
-    std::string spec(e);
-    size_t at = 0;
-    while (at < spec.size()) {
-      size_t end = spec.find(',', at);
-      if (end == std::string::npos) end = spec.size();
-      const std::string item = spec.substr(at, end - at);
-      int t = -1, sp = 0;
-      const size_t eq = item.find('=');
-      if (eq != std::string::npos && sscanf(item.c_str() + eq + 1, "%d:%d", &t, &sp) == 2)
-        for (int f = 0; f <= PF_LM; ++f)
-          if (item.compare(0, eq, names[f]) == 0 && t >= 0 && t <= 3 && sp >= 1 && sp <= 8) {
-            k->tiled_force[f][0] = t + 1;
-            k->tiled_force[f][1] = sp;
-          }
-      at = end + 1;
-    }
-  }
   if (hipError_t e = attn_set_lds_limit(); e != hipSuccess) {
     hvd_kv_free(k);
     return set_err(HVD_ERR_DEVICE, std::string("attention LDS limit: ") + hipGetErrorString(e));
@@ -1531,7 +1484,7 @@ extern "C" hvd_status hvd_prefill(hvd_model m, hvd_kv k, int32_t seq_id, const i
   if (k->m != m) return set_err(HVD_ERR_ARG, "kv handle belongs to another model");
   if (hvd_status st = from_host(k->hs->begin_prefill(seq_id, tokens, n), k); st != HVD_OK) return st;
   const int body = n - 1;
-  const int chunk_rows = prefill_rows(m->cfg);
+  const int chunk_rows = k->prefill_rows ? k->prefill_rows : prefill_rows(m->cfg);
   for (int s0 = 0; s0 < body; s0 += chunk_rows) {
     const int cnt = std::min(chunk_rows, body - s0);
     std::vector<SeqMeta> seqs{{seq_id, s0, cnt - 1, 0}};
@@ -1917,12 +1870,64 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
       for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
       k->graphs.clear();
       return HVD_OK;
+    case HVD_OPT_GEMM_MIN_BLOCKS:
+    case HVD_OPT_ATTN_MIN_ITEMS:
+    case HVD_OPT_ATTN_MAX_NP:
+    case HVD_OPT_SKINNY_MAX_MT:
+    case HVD_OPT_NS8_MT3:
+    case HVD_OPT_PREFILL_ROWS: {
+      const hvd_config& c = k->m->cfg;
+      if (option == HVD_OPT_GEMM_MIN_BLOCKS) {
+        if (value < 1) return set_err(HVD_ERR_ARG, "HVD_OPT_GEMM_MIN_BLOCKS must be >= 1");
+        k->gemm_min_blocks = value;
+      } else if (option == HVD_OPT_ATTN_MIN_ITEMS) {
+        if (value < 1) return set_err(HVD_ERR_ARG, "HVD_OPT_ATTN_MIN_ITEMS must be >= 1");
+        k->attn_min_items = value;
+      } else if (option == HVD_OPT_ATTN_MAX_NP) {
+        if (value < 2 || value > kItemPages || (value & (value - 1)))
+          return set_err(HVD_ERR_ARG, "HVD_OPT_ATTN_MAX_NP must be a power of two in [2, 16]");
+        k->attn_max_np = value;
+      } else if (option == HVD_OPT_SKINNY_MAX_MT) {
+        if (value < 1 || value > 64) return set_err(HVD_ERR_ARG, "HVD_OPT_SKINNY_MAX_MT must be in [1, 64]");
+        k->skinny_max_mt = value;
+      } else if (option == HVD_OPT_NS8_MT3) {
+        k->ns8_mt3 = value != 0;
+      } else {
+        if (value != 0 && (value < 16 || value % 16 || value > k->max_rows))
+          return set_err(HVD_ERR_ARG, "HVD_OPT_PREFILL_ROWS must be 0 or a multiple of 16 within the row workspace");
+        k->prefill_rows = value;
+      }
+      (void)c;
+      for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+      k->graphs.clear();
+      return HVD_OK;
+    }
     case HVD_OPT_MLP_SINGLE:
     case HVD_OPT_LM_SINGLE:
       (option == HVD_OPT_MLP_SINGLE ? k->mlp_single : k->lm_single) = value != 0;
       for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);  // captured with the old choice
       k->graphs.clear();
       return HVD_OK;
+  }
+  if (option >= HVD_OPT_GEMM_SHAPE && option <= HVD_OPT_GEMM_SHAPE + PF_LM) {
+    const int f = option - HVD_OPT_GEMM_SHAPE, ns = value / 100, sp = value % 100;
+    if (value != 0 && !((ns == 1 || ns == 2 || ns == 4 || ns == 8) && sp >= 1 && sp <= 16))
+      return set_err(HVD_ERR_ARG, "HVD_OPT_GEMM_SHAPE value: 0, or strips (1, 2, 4, 8) * 100 + K splits (1..16)");
+    k->gemm_force[f][0] = value ? ns : 0;
+    k->gemm_force[f][1] = value ? sp : 0;
+    for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+    k->graphs.clear();
+    return HVD_OK;
+  }
+  if (option >= HVD_OPT_TILED_SHAPE && option <= HVD_OPT_TILED_SHAPE + PF_LM) {
+    const int f = option - HVD_OPT_TILED_SHAPE, t = value / 100 - 1, sp = value % 100;
+    if (value != 0 && !(t >= 0 && t <= 3 && sp >= 1 && sp <= 8))
+      return set_err(HVD_ERR_ARG, "HVD_OPT_TILED_SHAPE value: 0, or (tile + 1) * 100 + K splits (1..8)");
+    k->tiled_force[f][0] = value ? t + 1 : 0;
+    k->tiled_force[f][1] = value ? sp : 0;
+    for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+    k->graphs.clear();
+    return HVD_OK;
   }
   return set_err(HVD_ERR_ARG, "unknown option");
 }

@@ -20,12 +20,22 @@ _STATUS = {0: "HVD_OK", -1: "HVD_ERR_ARG", -2: "HVD_ERR_STATE", -3: "HVD_ERR_OOM
 EXPORTS = ("hvd_model_bytes", "hvd_model_load", "hvd_model_free", "hvd_kv_bytes", "hvd_kv_alloc", "hvd_kv_free",
            "hvd_prefill", "hvd_verify", "hvd_verify_tree", "hvd_commit", "hvd_truncate", "hvd_seq_free", "hvd_seq_info",
            "hvd_kv_free_pages", "hvd_profile_enable", "hvd_profile_read", "hvd_kv_set_option", "hvd_last_error",
-           "hvd_async_begin", "hvd_async_step", "hvd_async_end", "hvd_verify_noalloc", "hvd_flow_trace")
+           "hvd_async_begin", "hvd_async_step", "hvd_async_end", "hvd_verify_noalloc", "hvd_flow_trace",
+           "hvd_measure_mfma_peak")
 HVD_OPT_GRAPHS = 1
 HVD_OPT_MLP_SINGLE = 2
 HVD_OPT_LM_SINGLE = 3
 HVD_OPT_FLOW = 4
 HVD_OPT_FLOW_ITEMS = 5
+HVD_OPT_GEMM_MIN_BLOCKS = 10
+HVD_OPT_ATTN_MIN_ITEMS = 11
+HVD_OPT_ATTN_MAX_NP = 12
+HVD_OPT_SKINNY_MAX_MT = 13
+HVD_OPT_NS8_MT3 = 14
+HVD_OPT_PREFILL_ROWS = 15
+HVD_OPT_GEMM_SHAPE = 16  # + GEMM family
+HVD_OPT_TILED_SHAPE = 24  # + GEMM family
+GEMM_FAMILIES = ("qkv", "o", "gateup", "down", "lm")
 MAX_TREE_NODES = 63  # nodes per token tree (hvd_verify_tree)
 
 
@@ -94,6 +104,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hvd_async_step": (I32, [P, I32]),
         "hvd_async_end": (I32, [P, PI32]),
         "hvd_flow_trace": (I32, [P, P, ctypes.c_int64]),
+        "hvd_measure_mfma_peak": (I32, [P, ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -101,6 +112,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         f.argtypes = args
     _lib = L
     return L
+
+
+def measure_mfma_peak(stream=None) -> float:
+    """Dense fp16 MFMA TFLOP/s measured on the current GPU (hvd_measure_mfma_peak)."""
+    t = ctypes.c_double()
+    _check(load_library().hvd_measure_mfma_peak(_stream(stream), ctypes.byref(t)))
+    return t.value
 
 
 def _check(status):
@@ -277,6 +295,22 @@ class KVCache:
         else:
             assert buf.is_cuda and buf.element_size() == 8 and buf.is_contiguous()
             _check(self.lib.hvd_flow_trace(self.handle, ctypes.c_void_p(buf.data_ptr()), buf.numel()))
+
+    def set_option(self, option: int, value: int):
+        """Set one of the handle's launch options (HVD_OPT_*)."""
+        _check(self.lib.hvd_kv_set_option(self.handle, int(option), int(value)))
+
+    def set_gemm_shape(self, family: str, strips: int = 0, splits: int = 0):
+        """Force the weight-streaming GEMM shape of one GEMM family (strips
+        per workgroup, K splits); strips 0 returns it to the policy."""
+        value = strips * 100 + splits if strips else 0
+        self.set_option(HVD_OPT_GEMM_SHAPE + GEMM_FAMILIES.index(family), value)
+
+    def set_tiled_shape(self, family: str, tile: int = -1, splits: int = 0):
+        """Force the tiled GEMM shape of one GEMM family (tile 0..3, K
+        splits); tile -1 returns it to the policy."""
+        value = (tile + 1) * 100 + splits if tile >= 0 else 0
+        self.set_option(HVD_OPT_TILED_SHAPE + GEMM_FAMILIES.index(family), value)
 
     def set_graphs(self, on: bool):
         """Replay step kernels from cached HIP graphs, or launch eagerly (default)."""

@@ -13,7 +13,6 @@ whose decisions include an oracle near tie (top-2 margin below 2e-2) end
 the comparison, as in the other parity tests.  After the loop, a
 synchronous verify on the loop's KV cache is checked against the oracle."""
 
-import os
 
 import numpy as np
 import pytest
@@ -111,10 +110,12 @@ def check_after_loop(torch, om, kv, sid, st, rep, k=8):
     kv.commit([sid])
 
 
-def run_copy_loop(torch, om, gm, seqs, steps, n_pages=512, seed=0):
+def run_copy_loop(torch, om, gm, seqs, steps, n_pages=512, seed=0, attn_min_items=None):
     """seqs: list of (context length, k).  Returns the mean accepted length per sequence."""
     import paper_2606_01019_amd as hvd
     kv = hvd.KVCache(gm, max_seqs=len(seqs), n_pages=n_pages)
+    if attn_min_items:
+        kv.set_option(hvd.hvd.HVD_OPT_ATTN_MIN_ITEMS, attn_min_items)
     V = om.cfg.vocab
     sts, refs = [], []
     for b, (L, k) in enumerate(seqs):
@@ -159,16 +160,7 @@ def test_async_copy_drafter_tiny(torch_cuda, tiny, min_items):
     (several sub-chunks per item, chunk ends moving inside them); the
     default plans 32-position chunks whose count grows during the loop."""
     om, gm = tiny
-    old = os.environ.get("HVD_ATTN_MIN_ITEMS")
-    if min_items:
-        os.environ["HVD_ATTN_MIN_ITEMS"] = str(min_items)
-    try:
-        m = run_copy_loop(torch_cuda, om, gm, [(512, 8)], 12, seed=1 if min_items else 0)
-    finally:
-        if old is None:
-            os.environ.pop("HVD_ATTN_MIN_ITEMS", None)
-        else:
-            os.environ["HVD_ATTN_MIN_ITEMS"] = old
+    m = run_copy_loop(torch_cuda, om, gm, [(512, 8)], 12, seed=1 if min_items else 0, attn_min_items=min_items)
     assert m[0] > 0.5  # drafts were accepted: the loop followed the stream
 
 

@@ -46,14 +46,15 @@ def mid_cases():
 
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("strips", [1, 2, 4, 8])
-def test_forced_strip_count_matches_oracle(mid_cases, monkeypatch, strips, splits):
+def test_forced_strip_count_matches_oracle(mid_cases, strips, splits):
     import paper_2606_01019_amd as hvd
     torch, w, cases = mid_cases
-    monkeypatch.setenv("HVD_GEMM_SHAPE", ",".join(f"{f}={strips}:{splits}" for f in FAMILIES))
     gm = hvd.Model(MID, w)
     kv = None
     try:
         kv = hvd.KVCache(gm, max_seqs=1, n_pages=128)
+        for f in FAMILIES:
+            kv.set_gemm_shape(f, strips, splits)
         rep = Report()
         for ctx, st, d, res in cases:
             print(f"{strips} strips, {splits} split(s), k = {len(d)}", flush=True)

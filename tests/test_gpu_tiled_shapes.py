@@ -53,15 +53,16 @@ def wide_case():
 
 @pytest.mark.parametrize("splits", [1, 2])
 @pytest.mark.parametrize("tile", [0, 1, 2, 3])
-def test_forced_tile_shape_matches_oracle(wide_case, monkeypatch, tile, splits):
+def test_forced_tile_shape_matches_oracle(wide_case, tile, splits):
     import paper_2606_01019_amd as hvd
     torch, w, ctxs, states, drafts, results = wide_case
-    monkeypatch.setenv("HVD_TILED_SHAPE", ",".join(f"{f}={tile}:{splits}" for f in FAMILIES))
     gm = hvd.Model(WIDE, w)
     kv = None
     try:
         B, k = len(ctxs), WIDE.max_draft
         kv = hvd.KVCache(gm, max_seqs=B, n_pages=sum((len(c) + k + 16) // 16 + 1 for c in ctxs) + 8)
+        for f in FAMILIES:
+            kv.set_tiled_shape(f, tile, splits)
         for s, c in enumerate(ctxs):
             kv.prefill(s, c)
         rows = B * (k + 1)
