@@ -218,31 +218,63 @@ class PayoffMLP:
         return losses
 
 
+class StepHistory:
+    """The App. B recent-history features over the last HISTORY decoding
+    steps: the share of steps that verified the cache draft, and the mean
+    accepted length of the cache drafts among them.  The decoding loop and
+    the training replay both keep one, so training and inference see the
+    same quantity."""
+
+    def __init__(self):
+        self.sel: List[float] = []
+        self.acc: List[int] = []
+
+    def recent(self):
+        s, a = self.sel[-HISTORY:], self.acc[-HISTORY:]
+        return (float(np.mean(s)) if s else 0.0, float(np.mean(a)) if a else 0.0)
+
+    def record(self, cache_selected: bool, accepted: int = 0):
+        self.sel.append(1.0 if cache_selected else 0.0)
+        if cache_selected:
+            self.acc.append(int(accepted))
+
+
 def replay_labels(trace: Sequence[int], prompt_len: int, cache_streams: Sequence[Sequence[int]] = (),
-                  max_new: Optional[int] = None):
-    """Training pairs from a recorded generation (App. B): each position t
-    of the generated part is a decoding state; the cache built from the
-    warmup streams and x[:t] proposes d_t, and the label is the longest
-    prefix of d_t equal to the trace's next tokens.  Recent-history features
-    follow a replay that selects every cache draft."""
+                  max_new: Optional[int] = None, policy: Optional[Callable] = None):
+    """Training pairs from a recorded generation (App. B).  The replay walks
+    the trace the way the decoding loop would with a verifier that commits
+    the trace (the greedy stream) and no model drafter: at each decoding
+    state the cache built from the warmup streams and the committed prefix
+    proposes d_t, the label is the longest prefix of d_t equal to the
+    trace's next tokens, and ``policy(phi) -> bool`` (default: always)
+    decides whether the step verifies d_t (committing label + 1 tokens) or
+    takes one greedy step.  Features, including the recent-history ones,
+    come from the same helpers as in ``HybridVerifiedDecoder.generate``."""
     cache = SuffixCache()
     for s in cache_streams:
         cache.new_stream(s)
     sid = cache.new_stream(trace[:prompt_len])
     max_new = max_new or (len(trace) - prompt_len)
-    X, y, hist = [], [], []
-    for t in range(prompt_len, len(trace)):
+    hist = StepHistory()
+    X, y = [], []
+    t = prompt_len
+    while t < len(trace) and t - prompt_len < max_new:
+        generated = t - prompt_len
+        room = max_new - generated - 1
         d, L, score = cache.draft(sid)
+        d = d[:max(0, min(room, MAX_DRAFT))]
+        selected, lab = False, 0
         if d:
-            lab = 0
             while lab < len(d) and t + lab < len(trace) and d[lab] == trace[t + lab]:
                 lab += 1
-            recent = hist[-HISTORY:]
-            X.append(features(score, L, d, prompt_len, t - prompt_len, max_new,
-                              1.0 if recent else 0.0, float(np.mean(recent)) if recent else 0.0))
+            phi = features(score, L, d, prompt_len, generated, max_new, *hist.recent())
+            X.append(phi)
             y.append(lab)
-            hist.append(lab)
-        cache.extend(sid, [trace[t]])
+            selected = True if policy is None else bool(policy(phi))
+        z = list(trace[t:t + (lab if selected else 0) + 1])
+        hist.record(selected, lab)
+        cache.extend(sid, z)
+        t += len(z)
     return np.asarray(X, np.float32).reshape(-1, N_FEATURES), np.asarray(y, np.float32)
 
 
@@ -277,6 +309,7 @@ class HybridVerifiedDecoder:
         self.cache = SuffixCache()
         for s in warmup_streams:
             self.cache.new_stream(s)
+        self.on_features: Optional[Callable] = None  # observer of each phi_t (tests)
 
     def generate(self, prompt: Sequence[int], max_new: int, eos: Optional[int] = None):
         prompt = [int(t) for t in prompt]
@@ -285,7 +318,7 @@ class HybridVerifiedDecoder:
         x = list(prompt)
         st = LoopStats()
         t0 = time.perf_counter()
-        hist_sel, hist_acc = [], []
+        hist = StepHistory()
         max_draft = MAX_DRAFT
         while st.generated < max_new:
             room = max_new - st.generated - 1  # tokens the step may add beyond the next one
@@ -293,10 +326,9 @@ class HybridVerifiedDecoder:
             d_c = d_c[:max(0, min(room, max_draft))]
             use_cache = False
             if d_c:
-                recent = hist_acc[-HISTORY:]
-                phi = features(score, L, d_c, len(prompt), st.generated, max_new,
-                               float(np.mean(hist_sel[-HISTORY:])) if hist_sel else 0.0,
-                               float(np.mean(recent)) if recent else 0.0)
+                phi = features(score, L, d_c, len(prompt), st.generated, max_new, *hist.recent())
+                if self.on_features is not None:
+                    self.on_features(phi)
                 use_cache = float(self.g(phi[None, :])[0]) >= self.tau
             if use_cache:
                 d = d_c
@@ -311,11 +343,10 @@ class HybridVerifiedDecoder:
             self.cache.extend(sid, z)
             st.cycles += 1
             st.generated += len(z)
-            hist_sel.append(1.0 if use_cache else 0.0)
+            hist.record(use_cache, a)
             if use_cache:
                 st.cache_steps += 1
                 st.cache_accepted.append(a)
-                hist_acc.append(a)
             elif d:
                 st.model_accepted.append(a)
             if eos is not None and eos in z:

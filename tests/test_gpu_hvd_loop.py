@@ -1,8 +1,9 @@
 """The Hybrid Verified Decoding loop (Alg. 1) driving the GPU verify step on
 the tiny decoder: whatever the draft selection, the committed stream is the
-target's greedy stream (compared with the GPU's own one-token greedy steps;
-a difference is allowed only at a near tie of the oracle's logits, where a
-k-row verify may round the other way)."""
+target's greedy stream as the oracle computes it (float64, no cache
+reuse across drafts).  The streams may part only at a position where the
+oracle's top-2 logit margin is below the near-tie margin (there either token
+is correct); the test reports where, and compares nothing after it."""
 
 import numpy as np
 import pytest
@@ -25,31 +26,24 @@ def tiny():
     return oracle.OracleModel(TINY, w), hvd.Model(TINY, w)
 
 
-def _greedy(kv, sid, prompt, n):
-    kv.prefill(sid, prompt)
-    out = []
-    for _ in range(n):
-        c, _, _ = kv.seq_info(sid)
-        _, nx = kv.verify([sid], [c], [np.zeros(0, np.int32)])
-        kv.commit([sid])
-        out.append(int(nx[0]))
-    kv.seq_free(sid)
-    return out
+def _oracle_greedy(om, prompt, n):
+    out, _ = oracle.greedy_decode(om, oracle.prefill(om, list(prompt)), n)
+    return [int(t) for t in out]
 
 
 @pytest.mark.parametrize("policy", ["always", "mlp"])
-def test_loop_on_gpu_commits_the_greedy_stream(tiny, policy):
+def test_loop_on_gpu_commits_the_oracles_greedy_stream(tiny, policy):
     import paper_2606_01019_amd as hvd
     om, gm = tiny
-    kv = hvd.KVCache(gm, max_seqs=2, n_pages=256)
+    kv = hvd.KVCache(gm, max_seqs=1, n_pages=256)
     prompt = wt.segment_context(wt.rng_for("context", 91), 600, TINY.vocab, seg=32, n_base=4)
     n_new = 96
-    ref = _greedy(kv, 1, prompt, n_new)
+    ref = _oracle_greedy(om, prompt, n_new)
     if policy == "always":
         pred = lambda phi: np.full(len(phi), np.inf)
     else:  # trained on the replay of another prompt's greedy trace (App. B)
         other = wt.segment_context(wt.rng_for("context", 92), 600, TINY.vocab, seg=32, n_base=4)
-        trace = list(other) + _greedy(kv, 1, other, 160)
+        trace = list(other) + _oracle_greedy(om, other, 160)
         X, y = hl.replay_labels(trace, len(other))
         pred = hl.PayoffMLP()
         pred.fit(X, y, batch=4096, epochs=20)
@@ -57,9 +51,12 @@ def test_loop_on_gpu_commits_the_greedy_stream(tiny, policy):
     out, st = dec.generate(prompt, n_new)
     print(f"{policy}: {st.cycles} cycles for {st.generated} tokens ({st.cycles_per_1k:.0f} per 1K), "
           f"{st.cache_steps} cache verifies, accepted {st.cache_accepted}")
+    if policy == "always":
+        assert st.cache_steps > 0
     if out != ref:
         p = next(i for i, (a, b) in enumerate(zip(out, ref)) if a != b)
-        st0 = oracle.prefill(om, list(prompt) + ref[:p])
-        r = oracle.verify(om, st0, [])
-        assert top2_margin(r.logits)[0] < TIE_MARGIN, f"streams differ at {p} without a near tie"
-        print(f"streams part at token {p} (near tie)")
+        r = oracle.verify(om, oracle.prefill(om, list(prompt) + ref[:p]), [])
+        assert top2_margin(r.logits)[0] < TIE_MARGIN, f"streams differ at token {p} without a near tie"
+        print(f"streams part at token {p} (oracle top-2 margin {top2_margin(r.logits)[0]:.2e})")
+    else:
+        print(f"all {n_new} tokens equal the oracle's greedy stream")

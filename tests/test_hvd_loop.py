@@ -93,18 +93,23 @@ def test_replay_labels_are_longest_agreeing_prefixes():
     trace = _repetitive(rng, 300, 12)
     X, y = hl.replay_labels(trace, prompt_len=60)
     assert X.shape[1] == hl.N_FEATURES and len(y) == len(X) > 0
-    # recompute the labels by brute force
+    # recompute the labels by brute force along the decoder's walk (every
+    # cache draft verified: label + 1 tokens committed, else one token)
     cache = hl.SuffixCache()
     sid = cache.new_stream(trace[:60])
     labels = []
-    for t in range(60, len(trace)):
+    t, max_new = 60, len(trace) - 60
+    while t < len(trace):
         d, _, _ = _brute_draft(cache.streams, sid)
+        d = d[:max(0, min(max_new - (t - 60) - 1, hl.MAX_DRAFT))]
+        lab = 0
         if d:
-            lab = 0
             while lab < len(d) and t + lab < len(trace) and d[lab] == trace[t + lab]:
                 lab += 1
             labels.append(lab)
-        cache.extend(sid, [trace[t]])
+        z = trace[t:t + lab + 1]
+        cache.extend(sid, z)
+        t += len(z)
     assert y.tolist() == labels
 
 
@@ -208,3 +213,27 @@ def test_loop_commits_exactly_the_greedy_stream(micro, policy):
     assert st.generated >= n_new and st.cycles <= n_new
     if policy == "always":
         assert st.cache_steps > 0
+
+
+def test_replay_features_equal_the_loops_features(micro):
+    """Training features come from the same helpers as inference: replaying
+    the loop's own greedy output under the loop's own selection policy
+    reproduces every feature vector the loop computed, recent-history
+    features included (App. B)."""
+    rng = wt.rng_for("misc", 86)
+    prompt = _repetitive(rng, 90, MICRO.vocab)
+    n_new = 48
+    g = hl.PayoffMLP(seed=5)
+    X0, y0 = hl.replay_labels(prompt + _repetitive(rng, 60, MICRO.vocab), len(prompt))
+    g.fit(X0, y0, batch=64, epochs=3)
+    tau = float(np.median(g(X0)))  # a threshold that selects some drafts and rejects others
+    seen = []
+    dec = hl.HybridVerifiedDecoder(OracleVerifier(micro), 0, g, tau=tau)
+    dec.on_features = lambda phi: seen.append(np.array(phi))
+    out, st = dec.generate(prompt, n_new)
+    assert 0 < st.cache_steps < len(seen)  # both choices occur
+    X, y = hl.replay_labels(prompt + out, len(prompt), max_new=n_new,
+                            policy=lambda phi: float(g(phi[None, :])[0]) >= tau)
+    assert X.shape[0] == len(seen)
+    np.testing.assert_array_equal(X, np.stack(seen))
+    assert np.any((X[:, 6] > 0) & (X[:, 6] < 1))  # the selection rate varies
