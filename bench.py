@@ -341,12 +341,31 @@ def leg_hvd_loop(model, reps):
         if warm:
             res[name]["tokens_equal_to_earlier_response"] = same(out, earlier)
     res["earlier_response"] = {"reruns": rounds, "tokens_equal_to_greedy": same(earlier, ref)}
+    # the same requests on the library's default numerics (MLP and LM head of
+    # verifies over 32 rows on the single fp16 activation)
+    kv.set_mlp_single(True)
+    kv.set_lm_single(True)
+    res["default_numerics"] = {}
+    for name, pred, warm in (("fresh_hvd", g, []), ("retry_hvd", g, [list(prompt) + earlier])):
+        dec = hl.HybridVerifiedDecoder(kv, 0, pred, warmup_streams=warm)
+        out, st = dec.generate(prompt, n_new)
+        kv.seq_free(0)
+        res["default_numerics"][name] = {
+            "cycles_per_1k": st.cycles_per_1k, "tokens_per_s": st.generated / st.decode_s,
+            "cache_verifies": st.cache_steps,
+            "mean_cache_accepted": float(np.mean(st.cache_accepted)) if st.cache_accepted else 0.0,
+            "tokens_equal_to_greedy": same(out, ref)}
+        if warm:
+            res["default_numerics"][name]["tokens_equal_to_earlier_response"] = same(out, earlier)
     kv.close()
     res["workload"] = (f"8B shape, batch 1, agentic-style prompt of {n} tokens, {n_new} new tokens, verifies with "
-                       f"fp16 hi+lo activations at every row count; fresh: empty "
+                       f"fp16 hi+lo activations at every row count (default_numerics: the library's defaults); "
+                       f"fresh: empty "
                        f"cache warmup; retry: the cache holds the decoder's own response to the same request from an "
                        f"earlier run; payoff MLP trained on "
                        f"{len(y)} replayed cache drafts of another request")
+    # a constructed best case (the cache holds the decoder's own earlier
+    # response): context for the loop, not evidence of the paper's speedups
     res["retry_speedup_vs_greedy"] = res["retry_hvd"]["tokens_per_s"] / res["greedy"]["tokens_per_s"]
     return res
 
@@ -553,34 +572,49 @@ def plan_drafts(kv, ks, planned, vocab, seq=0):
 
 
 def cpu_baseline(cfg, ctx_len, committed_per_step, w):
-    """Time the CPU oracle on a bounded sample of the same step: one verify of
-    k = 8 through the full model (all layers, full width, the same weights)
-    over a ctx_len-token cache, after one untimed call."""
+    """Time the CPU oracle (float32, the precision of the full-size parity
+    references) on a bounded sample of the same step: one verify of k = 8
+    through the full model (all layers, full width, the same weights) over a
+    ctx_len-token cache of random K/V (timing only: the values do not change
+    the work), median of three timed calls after one untimed call."""
     import oracle
     from oracle.model import SeqState
     from workloads import tokens as wt
     threads = len(os.sched_getaffinity(0))
+    blas = "unknown"
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')} ({info[0].get('num_threads')} threads)"
+    except Exception:  # pragma: no cover
+        pass
     rng = np.random.default_rng(0)
-    om = oracle.OracleModel(cfg, w, cache=False)
+    om = oracle.OracleModel(cfg, w, dtype=np.float32, cache=False)
     toks = list(wt.zipf_context(wt.rng_for("context", 2), ctx_len + 1, cfg.vocab))
-    K = [rng.standard_normal((ctx_len, cfg.n_kv_heads, cfg.head_dim)) for _ in range(cfg.n_layers)]
-    V = [rng.standard_normal((ctx_len, cfg.n_kv_heads, cfg.head_dim)) for _ in range(cfg.n_layers)]
+    K = [rng.standard_normal((ctx_len, cfg.n_kv_heads, cfg.head_dim)).astype(np.float32) for _ in range(cfg.n_layers)]
+    V = [rng.standard_normal((ctx_len, cfg.n_kv_heads, cfg.head_dim)).astype(np.float32) for _ in range(cfg.n_layers)]
     st = SeqState(tokens=toks, K=K, V=V)
     d = wt.random_chain(rng, 8, cfg.vocab)
     t0 = time.perf_counter()
     oracle.verify(om, st, d)
     t_first = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.verify(om, st, d)
-    step_s = time.perf_counter() - t0
+    times = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.verify(om, st, d)
+        times.append(time.perf_counter() - t0)
+    step_s = float(np.median(times))
     return {
         "value": committed_per_step / step_s,
         "unit": "committed tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"float64 numpy oracle, one k=8 verify through all {cfg.n_layers} layers at full width over a "
-                   f"{ctx_len}-token cache: {step_s:.2f}s (first call {t_first:.2f}s, untimed); committed tokens "
-                   f"per step taken from the GPU run ({committed_per_step:.2f})"),
+        "blas": blas,
+        "sample": (f"float32 numpy oracle, one k=8 verify through all {cfg.n_layers} layers at full width over a "
+                   f"{ctx_len}-token cache (random K/V), median of 3 timed calls {step_s:.2f}s (runs "
+                   f"{', '.join(f'{t:.2f}' for t in times)}s; first call {t_first:.2f}s, untimed); committed "
+                   f"tokens per step taken from the GPU run ({committed_per_step:.2f}); BLAS {blas}"),
     }
 
 
@@ -696,7 +730,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "fp16",
+        "dtype_note": ("fp16 MFMA with fp32 accumulation on bf16-valued weights (stored as fp16, exact), fp16 "
+                       "hi+lo activation pairs, fp16 KV cache, fp32 residual stream and logits"),
         "data": "synthetic",
         "config": {"workload": (f"8B-shaped random-init decoder ({cfg.n_layers} layers), batch 1, context "
                                 f"{args.ctx} Zipf(1.1) tokens, chain drafts k in {list(K_CYCLE)} planted "
@@ -709,14 +745,21 @@ def main():
         "step_roofline": {"bound": "hbm", "algorithmic_bytes_per_step": step_bytes,
                           "achieved_GBs": step_bytes / (ms_step * 1e-3) / 1e9,
                           "frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        "roofline": {"bound": "hbm", "kernel": f"gemm_skinny {dom} GEMM (incl. its split-K finish pass, if any)",
+        "roofline": {"bound": "hbm", "kernel": f"gemm_skinny {dom} GEMM (the dominant kernel)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "step_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "note": ("frac is the dominant kernel's; step_frac is the whole step's fraction of the HBM "
+                              "roofline (the target quantity for k <= 16)"),
                      "traffic": counter_traffic() if dom == "gateup" else None,
                      "avg_launch_us": d_ms * 1e3 / max(d_n, 1), "launches": d_n,
                      "bytes_per_launch": d_b / max(d_n, 1)},
         "kernel_families": fam,
     }
     kv.close()
+    peak_meas = hvd.measure_mfma_peak()
+    out["mfma_peak"] = {"vendor_dense_fp16_TFLOPs": MFMA_PEAK_TFLOPS, "measured_fp16_TFLOPs": peak_meas,
+                        "how": "register-only MFMA 32x32x16 f16 chains on every SIMD (hvd_measure_mfma_peak)"}
+    log(f"measured MFMA peak {peak_meas:.0f} TFLOP/s")
     legs = [x for x in args.workloads.split(",") if x]
     # the 32B leg frees the 8B model: it runs last whatever the order given
     legs = [x for x in legs if x != "multistep_32b"] + [x for x in legs if x == "multistep_32b"]

@@ -11,5 +11,6 @@ from .hvd import (  # noqa: F401
     KVCache,
     Model,
     load_library,
+    measure_mfma_peak,
     tensor_names,
 )
