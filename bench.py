@@ -32,7 +32,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = 2500.0  # dense fp16/bf16
 K_CYCLE = (1, 2, 4, 8, 16)
 # profiling families of hvd_profile_read, in order
-FAMILIES = ("qkv", "o", "gateup", "down", "lm_head", "attention", "combine", "other")
+FAMILIES = ("qkv", "o", "gateup", "down", "lm_head", "attention", "combine", "other", "flow", "attn_o")
 GEMM_FAMILIES = ("qkv", "o", "gateup", "down", "lm_head")
 
 

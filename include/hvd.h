@@ -251,7 +251,8 @@ int32_t hvd_kv_free_pages(hvd_kv kv);
  * 1 = O GEMM, 2 = gate/up GEMM, 3 = down GEMM, 4 = LM-head GEMM, 5 = verify
  * attention, 6 = attention combine, 7 = everything else, 8 = the one-launch
  * verify step (HVD_OPT_FLOW: the whole forward, its bytes the step's weights
- * and K/V).  hvd_profile_read returns the
+ * and K/V), 9 = the attention + O launch (HVD_OPT_ATTN_O: its bytes the K/V
+ * and the O weights).  hvd_profile_read returns the
  * summed event time (ms), launch count and algorithmic bytes since the last
  * enable.  The events add a little time to every bracketed launch. */
 hvd_status hvd_profile_enable(hvd_kv kv, int32_t enable);
@@ -280,6 +281,12 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   rounding (the attention split may differ).
  * HVD_OPT_FLOW_ITEMS (default 128): attention work items the one-launch step
  *   aims for (longer KV chunks when fewer); a tuning knob.
+ * HVD_OPT_ATTN_O (default 0): 1 runs each layer's attention, split-KV merge
+ *   and O projection of verify forwards of at most 32 rows as one launch
+ *   whose workgroups hold their O weight strip in registers while the
+ *   attention runs (head dim 128, K = 4096 and at most one 16-column strip
+ *   per compute unit); results agree with the separate launches within
+ *   rounding (the KV chunking may differ).
  *
  * Tuning overrides of the launch policy (for measurements and tests; results
  * stay within the verify step's tolerance whatever they are set to):
@@ -297,6 +304,7 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   waves; 0 = policy). */
 enum {
   HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3, HVD_OPT_FLOW = 4, HVD_OPT_FLOW_ITEMS = 5,
+  HVD_OPT_ATTN_O = 6,
   HVD_OPT_GEMM_MIN_BLOCKS = 10, HVD_OPT_ATTN_MIN_ITEMS = 11, HVD_OPT_ATTN_MAX_NP = 12, HVD_OPT_SKINNY_MAX_MT = 13,
   HVD_OPT_NS8_MT3 = 14, HVD_OPT_PREFILL_ROWS = 15, HVD_OPT_GEMM_SHAPE = 16, HVD_OPT_TILED_SHAPE = 24
 };
@@ -307,7 +315,11 @@ hvd_status hvd_kv_set_option(hvd_kv kv, int32_t option, int32_t value);
  * (4 words each) writes, for workgroup w in launch order, words 4w..4w+3:
  * its start, the time it found its inputs complete, its end (a 100 MHz
  * constant-rate device clock) and the hardware id it ran on (XCD << 32 |
- * HW_ID).  dev_buf NULL stops tracing.  Not needed for results. */
+ * HW_ID).  The attention + O launches (HVD_OPT_ATTN_O) of a step whose
+ * stamps fit write, for layer l and workgroup w, 8 words at
+ * 8 * (l * workgroups + w): the workgroup's start, its attention items done,
+ * counted, all items seen, its merges done, counted, all merges seen, and
+ * its end.  dev_buf NULL stops tracing.  Not needed for results. */
 hvd_status hvd_flow_trace(hvd_kv kv, uint64_t* dev_buf, int64_t n_words);
 
 /* Measure the dense fp16 MFMA rate of the current GPU (not a step of the

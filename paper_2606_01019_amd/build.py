@@ -22,7 +22,7 @@ ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", "-Wall", "-Wno-unused-function"]
 
-HIP_SOURCES = ["gemm.hip", "gemm_tiled.hip", "attn.hip", "misc.hip", "scratch.hip", "flow.hip", "peak.hip"]
+HIP_SOURCES = ["gemm.hip", "gemm_tiled.hip", "attn.hip", "attn_o.hip", "misc.hip", "scratch.hip", "flow.hip", "peak.hip"]
 HOST_SOURCES = ["api.cpp", "host_state.cpp"]
 
 

@@ -53,6 +53,7 @@ constexpr int kGemmLongK = 256;              // K steps above which a K split pa
 constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
 constexpr int kGemmCounters = 16384;          // split-K arrival counters (output blocks of one launch)
 constexpr int kFlowCounterWords = 1 << 17;    // one-launch step: error word and per-layer counters
+constexpr int kAoCounterBase = 64;             // attention + O launches: their counters after the error word
 constexpr int kFlowAttnItems = 128;           // attention items the one-launch step aims for
 constexpr int kFlowRows = 32;                 // rows of the one-launch step (two 16-row tiles)
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
@@ -62,7 +63,7 @@ constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items
 constexpr size_t kMaxGraphs = 64;  // cached step graphs per KV handle
 // profiling families: GEMM by role, attention, combine, everything else
 enum { PF_QKV = 0, PF_O = 1, PF_GATEUP = 2, PF_DOWN = 3, PF_LM = 4, PF_ATTN = 5, PF_COMBINE = 6, PF_OTHER = 7,
-       PF_FLOW = 8, kProfFamilies = 9 };
+       PF_FLOW = 8, PF_ATTN_O = 9, kProfFamilies = 10 };
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -382,6 +383,8 @@ struct hvd_kv_s {
   int32_t* out_host = nullptr;
   StepScratch sx;                 // the handle's own step scratch
   bool use_flow = false;          // one-launch step (flow.hip) where the shape allows it (HVD_OPT_FLOW)
+  bool use_attn_o = false;        // attention + merge + O GEMM as one launch (attn_o.hip; HVD_OPT_ATTN_O)
+  int n_cus = 0;                  // compute units of the device
   int flow_min_items = kFlowAttnItems;  // attention items the one-launch step aims for
   FlowLayer* flow_layers = nullptr;     // [n_layers] (device)
   std::vector<FlowLayer> flow_host;     // the same table on the host (filled by carve_kv)
@@ -576,6 +579,19 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
     hvd_kv_free(k);
     return set_err(HVD_ERR_DEVICE, std::string("one-launch step LDS limit: ") + hipGetErrorString(e));
   }
+  if (hipError_t e = attn_o_set_lds_limit(); e != hipSuccess) {
+    hvd_kv_free(k);
+    return set_err(HVD_ERR_DEVICE, std::string("attention + O launch LDS limit: ") + hipGetErrorString(e));
+  }
+  {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      hvd_kv_free(k);
+      return set_err(HVD_ERR_DEVICE, "device attribute query failed");
+    }
+    k->n_cus = cus;
+  }
 
   // this device's static scratch (hvd_verify_noalloc): its address is taken
   // here, once per device, with the device current
@@ -665,7 +681,8 @@ struct Plan {
 // KV chunks of `chunk` positions, chosen so the launch has enough workgroups
 // to fill the GPU; at most part_rows_free partial-buffer rows.
 bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<SeqMeta>& seqs,
-                    const std::vector<int>& members, int min_items, int rpi, size_t part_rows_free, Plan& p) {
+                    const std::vector<int>& members, int min_items, int rpi, size_t part_rows_free, Plan& p,
+                    int max_items = 0) {
   const int G = c.n_q_heads / c.n_kv_heads;
   struct Unit { int b, g, rg, keys; };
   auto item = [&](const Unit& u, int ci, int nch, int part, int chunk) {
@@ -715,6 +732,16 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   const int cap = rpi <= kAttnRows / 2 ? (1 << 20) : rpi <= kAttnRows ? 1024 : 512;
   int chunk = rpi <= kAttnRows / 2 ? 64 : 32;
   while (chunk < cap && 2 * chunk <= want) chunk *= 2;
+  if (max_items > 0) {
+    // the shortest power-of-two chunk that keeps the items within max_items
+    auto n_items_at = [&](int ch) {
+      int64_t n = 0;
+      for (const Unit& u : units) n += (u.keys + ch - 1) / ch;
+      return n;
+    };
+    chunk = 32;
+    while (chunk < (1 << 20) && n_items_at(chunk) > max_items) chunk *= 2;
+  }
   for (;;) {
     p.items.clear();
     p.heads.clear();
@@ -797,10 +824,19 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // attention item; chain drafts only, outside a device-resident loop.
   bool flow = k->use_flow && lm_head && !tree && !acap && MT * 16 <= kFlowRows && dh == 128;
   for (int b = 0; b < B && flow; ++b) flow = (seqs[b].k + 1) * G <= kAttnRows;
+  // Attention + merge + O GEMM as one launch (attn_o.hip): up to two row
+  // tiles, head dim 128, an O GEMM of K = 4096 with at most one strip per CU;
+  // every sequence's rows in 128-row items.
+  const bool attn_o = !flow && k->use_attn_o && !acap && (MT == 1 || MT == 2) &&
+                      attn_o_supported(dh, 2, MT, qd / 32, D / 16, k->n_cus);
+  // the attention workgroups of that launch: the CUs' second slots beside the O strips
+  const int ao_attn_wgs = attn_o ? std::min(2 * k->n_cus - D / 16, k->n_cus) : 0;
   std::vector<int> members[3];
+  int ao_rpi = kAttnRows / 2;  // attention + O launch: 64-row items unless a sequence has more rows
   for (int b = 0; b < B; ++b) {
     const int R = (seqs[b].k + 1) * G;
-    members[flow ? 1 : R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2].push_back(b);
+    if (R > kAttnRows / 2) ao_rpi = kAttnRows;
+    members[flow || attn_o ? 1 : R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2].push_back(b);
   }
   Plan plans[3];
   std::vector<AttnItem> items_all, heads_all;
@@ -809,8 +845,9 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   for (int cl = 0; cl < 3; ++cl) {
     if (members[cl].empty()) continue;
     Plan& pl = plans[cl];
-    if (!plan_attention(c, *k->hs, seqs, members[cl], flow ? k->flow_min_items : k->attn_min_items, kClassRows[cl],
-                        sx.part_rows - part_used, pl))
+    if (!plan_attention(c, *k->hs, seqs, members[cl], flow ? k->flow_min_items : k->attn_min_items,
+                        attn_o ? ao_rpi : kClassRows[cl], sx.part_rows - part_used, pl,
+                        attn_o ? ao_attn_wgs : 0))
       return set_err(HVD_ERR_OOM, "attention partial slots exhausted");
     pl.part_base = part_used;
     part_used += pl.part_rows;
@@ -1179,6 +1216,12 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     if (flow) {  // the one-launch step's error word and counters start at zero
       e.zero = sx.flow_cnt;
       e.n_zero = flow_words;
+    } else if (attn_o) {  // likewise the attention + O launches' counters
+      e.zero = sx.flow_cnt;
+      e.n_zero = kAoCounterBase + 2 * kAoSlots * kAoSlotWords;
+    } else {  // the error word alone
+      e.zero = sx.flow_cnt;
+      e.n_zero = 1;
     }
     ProfScope ps(k, PF_OTHER, 0.0);
     HIP_TRY(launch_embed(e, s));
@@ -1270,8 +1313,10 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.rope = m->rope;
       if (hvd_status st = gemm(EPI_QKV, a, qd + 2 * kvd, D, PF_QKV); st != HVD_OK) return st;
     }
-    {
-      AttnArgs a{};
+    if (attn_o) {
+      const Plan& pl = plans[1];
+      AttnOArgs ao{};
+      AttnArgs& a = ao.at;
       a.Q = k->Q;
       a.kv = kvl;
       a.page_stride = k->page_stride;
@@ -1281,54 +1326,118 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.group = G;
       a.pt = k->pt;
       a.pt_stride = k->pt_stride;
-      a.items = d_items;
+      a.items = d_items + pl.item0;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
       a.Ohi = k->Ohi;
       a.Olo = k->Olo;
       a.MTtot = MT;
       a.tree_mask = d_mask;
-      // one launch per row class, then the combine passes
-      for (int cl = 0; cl < 3; ++cl) {
-        const Plan& pl = plans[cl];
-        if (pl.items.empty()) continue;
-        a.items = d_items + pl.item0;
-        a.part_o = sx.part_o + pl.part_base * dh;
-        a.part_ml = sx.part_ml + pl.part_base * 2;
-        ProfScope ps(k, PF_ATTN, kv_bytes_cl[cl]);
-        HIP_TRY(launch_attn(a, (int)pl.items.size(), pl.chunk, pl.rpi, k->attn_max_np, s));
+      a.part_o = sx.part_o + pl.part_base * dh;
+      a.part_ml = sx.part_ml + pl.part_base * 2;
+      CombineArgs& cb = ao.cb;
+      cb.heads = d_heads + pl.head0;
+      cb.Hq = c.n_q_heads;
+      cb.Hkv = c.n_kv_heads;
+      cb.dh = dh;
+      cb.group = G;
+      cb.part_o = a.part_o;
+      cb.part_ml = a.part_ml;
+      cb.Ohi = k->Ohi;
+      cb.Olo = k->Olo;
+      cb.MTtot = MT;
+      cb.rpi = pl.rpi;
+      cb.max_rows = pl.comb_rows;
+      ao.n_attn = ao_attn_wgs;
+      ao.n_items = pl.n_items_real;
+      ao.n_heads = pl.n_heads_real;
+      ao.merge_spb = (pl.comb_rows + kAoMergeRows - 1) / kAoMergeRows;
+      GemmArgs& g = ao.go;
+      g.W = (const uint4*)L.o;
+      g.KT = qd / 32;
+      g.NT = D / 16;
+      g.wg = (size_t)g.KT * 256;
+      g.wk = 256;
+      g.Ahi = (const uint4*)k->Ohi;
+      g.Alo = (const uint4*)k->Olo;
+      g.MTtot = MT;
+      g.M = M;
+      g.X = k->X;
+      g.D = D;
+      g.gain_next = L.g_mlp;
+      g.Nhi = k->Nhi;
+      g.Nlo = k->Nlo;
+      g.ss_out = k->ss;
+      ao.cnt = sx.flow_cnt + kAoCounterBase;
+      ao.target = (uint32_t)(l + 1) * (uint32_t)ao_attn_wgs;
+      ao.err = sx.flow_cnt;
+      const size_t grid = (size_t)ao_attn_wgs + g.NT;
+      if (k->flow_trace && (size_t)c.n_layers * grid * kAoTraceWords <= (size_t)k->flow_trace_words)
+        ao.trace = k->flow_trace + (size_t)l * grid * kAoTraceWords;
+      // 2-page sub-chunks for 128-row items (4 would spill registers)
+      const int np = std::min(pl.rpi > kAttnRows / 2 ? 2 : 4, attn_pages_per_sub(pl.chunk));
+      ProfScope ps(k, PF_ATTN_O, kv_bytes_cl[1] + (double)qd * D * 2);
+      HIP_TRY(launch_attn_o(ao, np, pl.rpi, MT, s));
+    } else {
+      {
+        AttnArgs a{};
+        a.Q = k->Q;
+        a.kv = kvl;
+        a.page_stride = k->page_stride;
+        a.Hq = c.n_q_heads;
+        a.Hkv = c.n_kv_heads;
+        a.dh = dh;
+        a.group = G;
+        a.pt = k->pt;
+        a.pt_stride = k->pt_stride;
+        a.items = d_items;
+        a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)dh));
+        a.Ohi = k->Ohi;
+        a.Olo = k->Olo;
+        a.MTtot = MT;
+        a.tree_mask = d_mask;
+        // one launch per row class, then the combine passes
+        for (int cl = 0; cl < 3; ++cl) {
+          const Plan& pl = plans[cl];
+          if (pl.items.empty()) continue;
+          a.items = d_items + pl.item0;
+          a.part_o = sx.part_o + pl.part_base * dh;
+          a.part_ml = sx.part_ml + pl.part_base * 2;
+          ProfScope ps(k, PF_ATTN, kv_bytes_cl[cl]);
+          HIP_TRY(launch_attn(a, (int)pl.items.size(), pl.chunk, pl.rpi, k->attn_max_np, s));
+        }
+        for (int cl = 0; cl < 3; ++cl) {
+          const Plan& pl = plans[cl];
+          if (pl.heads.empty()) continue;
+          CombineArgs cb{};
+          cb.heads = d_heads + pl.head0;
+          cb.Hq = c.n_q_heads;
+          cb.Hkv = c.n_kv_heads;
+          cb.dh = dh;
+          cb.group = G;
+          cb.part_o = sx.part_o + pl.part_base * dh;
+          cb.part_ml = sx.part_ml + pl.part_base * 2;
+          cb.Ohi = k->Ohi;
+          cb.Olo = k->Olo;
+          cb.MTtot = MT;
+          cb.rpi = pl.rpi;
+          cb.max_rows = pl.comb_rows;
+          ProfScope ps(k, PF_COMBINE, 0.0);
+          HIP_TRY(launch_combine(cb, (int)pl.heads.size(), s));
+        }
       }
-      for (int cl = 0; cl < 3; ++cl) {
-        const Plan& pl = plans[cl];
-        if (pl.heads.empty()) continue;
-        CombineArgs cb{};
-        cb.heads = d_heads + pl.head0;
-        cb.Hq = c.n_q_heads;
-        cb.Hkv = c.n_kv_heads;
-        cb.dh = dh;
-        cb.group = G;
-        cb.part_o = sx.part_o + pl.part_base * dh;
-        cb.part_ml = sx.part_ml + pl.part_base * 2;
-        cb.Ohi = k->Ohi;
-        cb.Olo = k->Olo;
-        cb.MTtot = MT;
-        cb.rpi = pl.rpi;
-        cb.max_rows = pl.comb_rows;
-        ProfScope ps(k, PF_COMBINE, 0.0);
-        HIP_TRY(launch_combine(cb, (int)pl.heads.size(), s));
+      {
+        GemmArgs a{};
+        a.W = (const uint4*)L.o;
+        a.Ahi = (const uint4*)k->Ohi;
+        a.Alo = (const uint4*)k->Olo;
+        a.X = k->X;
+        a.D = D;
+        a.gain_next = L.g_mlp;
+        a.Nhi = k->Nhi;
+        a.Nlo = k->Nlo;
+        a.ss_out = k->ss;
+        if (hvd_status st = gemm(EPI_RESID, a, D, qd, PF_O); st != HVD_OK) return st;
       }
-    }
-    {
-      GemmArgs a{};
-      a.W = (const uint4*)L.o;
-      a.Ahi = (const uint4*)k->Ohi;
-      a.Alo = (const uint4*)k->Olo;
-      a.X = k->X;
-      a.D = D;
-      a.gain_next = L.g_mlp;
-      a.Nhi = k->Nhi;
-      a.Nlo = k->Nlo;
-      a.ss_out = k->ss;
-      if (hvd_status st = gemm(EPI_RESID, a, D, qd, PF_O); st != HVD_OK) return st;
     }
     {
       GemmArgs a{};
@@ -1861,6 +1970,11 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
       return HVD_OK;
     case HVD_OPT_FLOW:
       k->use_flow = value != 0;
+      for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
+      k->graphs.clear();
+      return HVD_OK;
+    case HVD_OPT_ATTN_O:
+      k->use_attn_o = value != 0;
       for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);
       k->graphs.clear();
       return HVD_OK;

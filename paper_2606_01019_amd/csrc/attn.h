@@ -29,6 +29,10 @@ constexpr int attn_occupancy(int DH, int NP, int NW) { return NW == 4 && NP * kP
 // outputs are written with device-scope stores, and the query rows (a
 // buffer written once per launch) with ordinary loads; hk.wait() runs once
 // the first sub-chunk's cached K/V is requested, hk.done() after the outputs.
+// Hooks::kDevOut alone asks for device-scope outputs (inputs from earlier
+// launches).  hk.after_issue() runs once the first sub-chunk's K/V and the
+// query rows are requested and may request Hooks::kPending more loads per
+// thread, which the item does not wait for.
 template <int DH, int NP, int NW, int TPW, bool COH, class Hooks>
 __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsigned char* smem, Hooks& hk) {
   constexpr int NT = 64 * NW;           // threads
@@ -45,6 +49,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
   // wave has finished reading once it passed the previous staging barrier,
   // so one barrier per sub-chunk suffices.
   constexpr bool DB = NP <= 4;
+  constexpr bool DEV_OUT = COH || Hooks::kDevOut;
+  static_assert(Hooks::kPending >= 0 && Hooks::kPending < 64, "loads left in flight");
   constexpr int BUF_BYTES = CH * DH * 2 * 2;       // K and V of one sub-chunk
   _Float16* sK = (_Float16*)smem;                  // [CH][DH], segment-swizzled
   _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], 8-byte-unit-swizzled
@@ -145,11 +151,12 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
     return a.pt[(size_t)slot * a.pt_stride + (nsub >> 4) + (lane < np_sub ? lane : 0)];
   };
   int pg_next = p_begin + CH < p_end ? next_pages(p_begin + CH) : 0;
+  hk.after_issue();
   // Wait here for everything issued so far (the first sub-chunk is staged
   // right after anyway): the waitcnt pass then knows the query fragments are
   // in, and places no wait for them inside the loop, where it would also
-  // wait for the next sub-chunk's loads.
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  // wait for the next sub-chunk's loads.  Loads the hook added stay in flight.
+  __builtin_amdgcn_s_waitcnt(vmcnt_enc(Hooks::kPending));
 
   int nbuf = 0;
   for (int sub = p_begin; sub < p_end; sub += CH) {
@@ -340,7 +347,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
           const size_t off = afrag_off(row, col, a.MTtot);
           const uint2 vh = uint2{hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16)};
           const uint2 vl = uint2{lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16)};
-          if constexpr (COH) {
+          if constexpr (DEV_OUT) {
             st_u64_dev((uint64_t*)(a.Ohi + off), (uint64_t)vh.x | ((uint64_t)vh.y << 32));
             st_u64_dev((uint64_t*)(a.Olo + off), (uint64_t)vl.x | ((uint64_t)vl.y << 32));
           } else {
@@ -355,11 +362,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
 #pragma unroll
       for (int dt = 0; dt < DH / 16; ++dt) {
         const float4 v = float4{o[q][dt][0], o[q][dt][1], o[q][dt][2], o[q][dt][3]};
-        if constexpr (COH) st_f4_dev(a.part_o, (uint32_t)((ps * DH + dt * 16 + lg * 4) * 4), v);
+        if constexpr (DEV_OUT) st_f4_dev(a.part_o, (uint32_t)((ps * DH + dt * 16 + lg * 4) * 4), v);
         else *(float4*)(a.part_o + ps * DH + dt * 16 + lg * 4) = v;
       }
       if (lg == 0) {
-        if constexpr (COH)
+        if constexpr (DEV_OUT)
           st_u64_dev((uint64_t*)(a.part_ml + ps * 2), (uint64_t)__float_as_uint(m[q]) |
                                                           ((uint64_t)__float_as_uint(l) << 32));
         else
@@ -382,8 +389,10 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
 // smaller when an entry has more rows, so blocks past a short entry's rows
 // stay few.
 // One (head entry, row slice) of the merge by a block of NT threads.  COH:
-// partials are read, and the output written, with device-scope accesses.
-template <int DH, int QS, int NT, bool COH>
+// partials are read, and the output written, with device-scope accesses
+// (COH_IN false: partials read with ordinary loads, for partial buffers no
+// reader touches before they are complete and whose lines have one writer).
+template <int DH, int QS, int NT, bool COH, bool COH_IN = COH>
 __device__ __forceinline__ void combine_slice(const CombineArgs& a, const AttnItem& hd, int slice) {
   constexpr int OCT = DH / 8;            // 8-dim octets per row
   constexpr int RPB = NT / (OCT * QS);   // rows per block
@@ -409,7 +418,7 @@ __device__ __forceinline__ void combine_slice(const CombineArgs& a, const AttnIt
       mlc[j] = float2{-INFINITY, 0.f};
       x0[j] = x1[j] = float4{0.f, 0.f, 0.f, 0.f};
       if (c < hd.nch) {
-        if constexpr (COH) {
+        if constexpr (COH_IN) {
           const uint64_t mv = ld_u64_dev((const uint64_t*)(ml + c * cstride_ml));
           mlc[j] = float2{__uint_as_float((uint32_t)mv), __uint_as_float((uint32_t)(mv >> 32))};
           x0[j] = ld_f4_dev(a.part_o, (uint32_t)((po - a.part_o + c * cstride_o) * 4));

@@ -118,9 +118,17 @@ __device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
 // same kernel produces is read; done() runs after the work's outputs are
 // written.  Stand-alone kernels use these no-ops.
 struct NoHooks {
+  static constexpr bool kDevOut = false;
+  static constexpr int kPending = 0;
   __device__ __forceinline__ void wait() {}
+  __device__ __forceinline__ void after_issue() {}
   __device__ __forceinline__ void done() {}
 };
+
+// s_waitcnt immediate that waits until at most n (< 64) vector memory
+// operations are outstanding (lgkmcnt and expcnt left alone): vmcnt is
+// split over bits 3:0 and 15:14.
+__host__ __device__ constexpr int vmcnt_enc(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
 
 __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);

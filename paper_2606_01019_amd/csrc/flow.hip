@@ -63,6 +63,8 @@ __device__ __forceinline__ void flow_signal(uint32_t* ctr) {
 }
 
 struct FlowHooks {
+  static constexpr bool kDevOut = true;
+  static constexpr int kPending = 0;
   const uint32_t* wctr;  // null: nothing to wait for
   int wn;
   uint32_t wtarget;
@@ -73,6 +75,7 @@ struct FlowHooks {
     if (wctr) flow_wait(wctr, wn, wtarget, err);
     if (trace && threadIdx.x == 0) trace[1] = __builtin_amdgcn_s_memrealtime();
   }
+  __device__ __forceinline__ void after_issue() {}
   __device__ __forceinline__ void done() {
     if (dctr) flow_signal(dctr);
   }

@@ -281,6 +281,29 @@ struct FlowArgs {
   uint64_t* trace;
 };
 
+// Attention, its split-KV merge and the O GEMM of one layer as one launch
+// of n_attn + go.NT co-resident 256-thread workgroups (attn_o.hip).
+struct AttnOArgs {
+  AttnArgs at;              // items: n_items (attention workgroup r takes items r, r + n_attn, ...)
+  CombineArgs cb;           // merge entries: n_heads, merge_spb row slices each
+  GemmArgs go;              // the O GEMM: one 16-column strip per O workgroup
+  int n_attn;               // attention workgroups (the first of the grid)
+  int n_items, n_heads, merge_spb;
+  // [2][kAoSlots] counters kAoSlotWords apart (items done, merges done),
+  // zeroed once per step; layer l waits for (l + 1) * n_attn arrivals
+  uint32_t* cnt;
+  uint32_t target;          // (layer + 1) * n_attn
+  uint32_t* err;            // bit 0 set if a wait gave up (results then invalid)
+  // nullable diagnostics: per workgroup kAoTraceWords constant-clock stamps
+  // (attention: start, items done, counted, all items seen, merges done,
+  // counted; O: start, strip requested, all merges seen, end at 0, 1, 6, 7)
+  uint64_t* trace;
+};
+constexpr int kAoTraceWords = 8;
+constexpr int kAoSlots = 32;
+constexpr int kAoSlotWords = 32;  // one 128-byte line per counter slot
+constexpr int kAoMergeRows = 2;   // rows per merge slice (256 threads, 8 lanes per (row, 8 dims))
+
 // Launchers: all enqueue on `s` and return the launch status.
 hipError_t launch_pack(const uint16_t* src, const int32_t* rowmap, uint16_t* dst, int N, int K,
                        hipStream_t s);
@@ -315,6 +338,12 @@ hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* p
 bool flow_supported(int MT, int dh, int np, const int* ns);
 hipError_t launch_flow(const FlowArgs& f, int MT, hipStream_t s);
 hipError_t flow_set_lds_limit();  // once per process, before the first launch
+// Whether the fused attention + O launch handles this shape (head dim, pages
+// per sub-chunk, row tiles, K steps and strips of the O GEMM) and fits
+// `n_cus` compute units.
+bool attn_o_supported(int dh, int np, int MT, int KT, int NT, int n_cus);
+hipError_t launch_attn_o(const AttnOArgs& a, int np, int rows_per_item, int MT, hipStream_t s);
+hipError_t attn_o_set_lds_limit();
 
 constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
 

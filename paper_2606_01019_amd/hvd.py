@@ -27,6 +27,7 @@ HVD_OPT_MLP_SINGLE = 2
 HVD_OPT_LM_SINGLE = 3
 HVD_OPT_FLOW = 4
 HVD_OPT_FLOW_ITEMS = 5
+HVD_OPT_ATTN_O = 6
 HVD_OPT_GEMM_MIN_BLOCKS = 10
 HVD_OPT_ATTN_MIN_ITEMS = 11
 HVD_OPT_ATTN_MAX_NP = 12
@@ -282,6 +283,11 @@ class KVCache:
         """One-launch verify step for batches of at most 32 rows, or one
         kernel launch per GEMM / attention pass (the default)."""
         _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_FLOW, 1 if on else 0))
+
+    def set_attn_o(self, on: bool):
+        """Attention, merge and O projection of small verify batches as one
+        launch per layer, or as separate launches (the default)."""
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_ATTN_O, 1 if on else 0))
 
     def set_flow_items(self, n: int):
         """Attention work items the one-launch step aims for (tuning)."""
