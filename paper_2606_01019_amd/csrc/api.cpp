@@ -764,6 +764,45 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
     // longer chunks: multiples of kAttnChunk above it (looped in LDS-sized pieces)
     chunk = chunk < kAttnChunk ? std::min(kAttnChunk, chunk * 2) : chunk * 2;
   }
+  // Several row groups of one (sequence, kv head) read the same K/V chunks.
+  // Their items go 8 grid positions apart, next to each other in dispatch
+  // order: the same XCD under round-robin dispatch, at nearly the same time,
+  // so the chunk comes from HBM once and from that XCD's L2 for the others.
+  // Keys (sequence, head, chunk) in plan order, eight per group; item (key
+  // j of the group, row group r) at group base + 8r + j.  A missing (key,
+  // row group) pair is a no-op item (k = -1).
+  bool multi_rg = false;
+  for (const AttnItem& it : p.items) multi_rg |= it.rg > 0;
+  if (multi_rg) {
+    std::vector<std::array<int, 3>> keys;  // (sequence, head, chunk) in first-seen order
+    std::map<std::array<int, 3>, std::vector<int>> by_key;  // -> item index per row group
+    for (size_t i = 0; i < p.items.size(); ++i) {
+      const AttnItem& it = p.items[i];
+      const std::array<int, 3> key{it.pad1, it.g, it.c};
+      auto& v = by_key[key];
+      if (v.empty()) keys.push_back(key);
+      if ((int)v.size() <= it.rg) v.resize(it.rg + 1, -1);
+      v[it.rg] = (int)i;
+    }
+    AttnItem none{};
+    none.k = -1;
+    std::vector<AttnItem> out;
+    for (size_t g0 = 0; g0 < keys.size(); g0 += 8) {
+      const size_t n = std::min<size_t>(8, keys.size() - g0);
+      size_t R = 0;
+      for (size_t j = 0; j < n; ++j) R = std::max(R, by_key[keys[g0 + j]].size());
+      for (size_t r = 0; r < R; ++r)
+        for (size_t j = 0; j < 8; ++j) {
+          if (j >= n) {
+            if (g0 + 8 < keys.size()) out.push_back(none);  // keep the next group 8-aligned
+            continue;
+          }
+          const auto& v = by_key[keys[g0 + j]];
+          out.push_back(r < v.size() && v[r] >= 0 ? p.items[(size_t)v[r]] : none);
+        }
+    }
+    p.items.swap(out);
+  }
   p.chunk = chunk;
   p.rpi = rpi;
   int max_r = 1;

@@ -13,6 +13,10 @@ namespace hvd {
 // whose results (the first sub-chunk's page ids included) sit in SGPRs.
 typedef const __attribute__((address_space(4))) AttnItem ConstItem;
 
+// Slack of the online softmax's reference max (base-2 units): the largest
+// weight 2^(s - m) is 2^kAttnLazy.
+constexpr float kAttnLazy = 8.f;
+
 // NP = pages staged per sub-chunk (the launch picks it from the chunk
 // length), so short decode chunks issue only the loads they need.  NW waves
 // hold TPW row tiles each: an item covers up to 16*NW*TPW query rows (64 for
@@ -273,9 +277,21 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
           }
           bm = fmaxf(bm, __shfl_xor(bm, 16));
           bm = fmaxf(bm, __shfl_xor(bm, 32));
-          const float mn = fmaxf(m[q], bm * a.scale_log2);
-          const float ms = mn == -INFINITY ? 0.f : mn;  // nothing visible yet: every weight is 0
-          const float alpha = __builtin_amdgcn_exp2f(m[q] - ms);
+          // Lazy rescaling: a row's reference m moves only when a score
+          // exceeds it by more than kAttnLazy (base-2 units).  The weights
+          // 2^(s - m) then stay below 2^kAttnLazy (well inside the fp16 P
+          // operand's range), (m, l, O) stay consistent, and the
+          // accumulators are rescaled only when some row's reference moves.
+          const float cand = bm * a.scale_log2;
+          if (__builtin_amdgcn_ballot_w64(cand > m[q] + kAttnLazy)) {
+            const bool grow = cand > m[q] + kAttnLazy;
+            const float alpha = grow ? __builtin_amdgcn_exp2f(m[q] - cand) : 1.f;  // 0 from -inf
+            lsum[q] *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
+            if (grow) m[q] = cand;
+          }
+          const float ms = m[q] == -INFINITY ? 0.f : m[q];  // nothing visible yet: every weight is 0
           float ps = 0.f;
 #pragma unroll
           for (int b = 0; b < SG; ++b)
@@ -284,12 +300,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
               sc[q][b][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][b][j], a.scale_log2, -ms));
               ps += sc[q][b][j];
             }
-          lsum[q] = lsum[q] * alpha + ps;
-          m[q] = mn;
-          if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {  // the max moved for some row
-#pragma unroll
-            for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
-          }
+          lsum[q] += ps;
           // B operand of block pair c: positions 32c' + {4lg..4lg+3} and
           // 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
 #pragma unroll
