@@ -59,6 +59,7 @@ constexpr int kFlowRows = 32;                 // rows of the one-launch step (tw
 constexpr int kAttnMinItems = 256;            // attention workgroups wanted per launch
 constexpr int kCUs = 256;                     // compute units of the MI355X
 constexpr int kAttnRows = 128;     // query rows per attention work item
+constexpr int kAttnClasses = 4;    // attention row classes: items of 64, 128, 256 and 384 rows
 constexpr int kPartSlots = 4096;   // attention partial slots (multi-chunk items)
 constexpr size_t kMaxGraphs = 64;  // cached step graphs per KV handle
 // profiling families: GEMM by role, attention, combine, everything else
@@ -301,7 +302,7 @@ extern "C" void hvd_model_free(hvd_model m) {
 // rows per item), LM head on/off and the logits pointer.
 struct GraphKey {
   int M, B, lm_head, tree;
-  std::array<int, 12> attn;  // per row class: items, combine entries, chunk, combine rows
+  std::array<int, 4 * kAttnClasses> attn;  // per row class: items, combine entries, chunk, combine rows
   float* logits;
   bool operator<(const GraphKey& o) const {
     return std::tie(M, B, lm_head, tree, attn, logits) < std::tie(o.M, o.B, o.lm_head, o.tree, o.attn, o.logits);
@@ -410,12 +411,13 @@ size_t meta_capacity_ints(const hvd_config& c, int max_rows, int max_seqs, int p
   const size_t rg_verify = ((size_t)(c.max_draft + 1) * G + kAttnRows - 1) / kAttnRows;
   const size_t rg_prefill = ((size_t)prefill_rows(c) * G + kAttnRows - 1) / kAttnRows;
   const size_t units = std::max((size_t)max_seqs * rg_verify, rg_prefill) * c.n_kv_heads;
-  // items <= units + partial slots (at most 2 kPartSlots: 64-row items) and
-  // heads <= units, each of the three row classes padded up (to 64 and 16
+  // items <= units + partial slots (at most 2 kPartSlots: 64-row items),
+  // twice over for the no-op items that keep row groups 8 grid positions
+  // apart, and heads <= units, each row class padded up (to 64 and 16
   // entries); header and per-section alignment fit in the last term
   const size_t item_ints = sizeof(AttnItem) / 4;
   return (4 + 3) * (size_t)max_rows + sizeof(SeqMeta) / 4 * (size_t)max_seqs +
-         item_ints * (2 * units + 2 * kPartSlots + 3 * (64 + 16)) + 3 * (size_t)max_seqs * pt_stride + 64;
+         item_ints * (4 * units + 4 * kPartSlots + kAttnClasses * (64 + 16)) + 3 * (size_t)max_seqs * pt_stride + 64;
 }
 
 size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, void* base) {
@@ -433,7 +435,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->ss = cv.take<float>(Mp * (D / 16));
   // GEMM operands carry kGemmMaxMT extra fragments: a workgroup always reads
   // a full block of row tiles and drops the rows past the last tile
-  const size_t pad = (size_t)kGemmMaxMT * 512;
+  const size_t pad = (size_t)kGemmPadMT * 512;
   k->Nhi = cv.take<uint16_t>(Mp * D + pad);
   k->Nlo = cv.take<uint16_t>(Mp * D + pad);
   k->Q = cv.take<_Float16>(Mp * qd);
@@ -460,7 +462,7 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   // for its largest batch: kFlowRows rows
   k->flow_host.assign(c.n_layers, FlowLayer{});
   if (c.head_dim == 128) {
-    const size_t R = kFlowRows, fpad = (size_t)kGemmMaxMT * 512;
+    const size_t R = kFlowRows, fpad = (size_t)kGemmPadMT * 512;
     for (int l = 0; l < c.n_layers; ++l) {
       FlowLayer& f = k->flow_host[l];
       f.x_mid = cv.take<float>(R * D);
@@ -857,7 +859,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // head go to items of 64, 128 or 256 rows (256 for head dim 128 only;
   // longer row sets take several row groups), one launch per class, so a
   // long draft does not put every short one on the large kernel.
-  static const int kClassRows[3] = {kAttnRows / 2, kAttnRows, 2 * kAttnRows};
+  static const int kClassRows[kAttnClasses] = {kAttnRows / 2, kAttnRows, 2 * kAttnRows, 3 * kAttnRows};
   // One-launch step (flow.hip): verify batches of at most two row tiles,
   // head dim 128, every sequence's query rows per kv head in one 128-row
   // attention item; chain drafts only, outside a device-resident loop.
@@ -870,18 +872,28 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
                       attn_o_supported(dh, 2, MT, qd / 32, D / 16, k->n_cus);
   // the attention workgroups of that launch: the CUs' second slots beside the O strips
   const int ao_attn_wgs = attn_o ? std::min(2 * k->n_cus - D / 16, k->n_cus) : 0;
-  std::vector<int> members[3];
+  // Above 256 rows, 384-row items (three row tiles per wave) when 256-row
+  // items would leave a last row group of at most 64 rows -- a whole pass
+  // over the keys for a few rows -- and the 384-row items need fewer passes
+  // (260 rows: one, not two).  Otherwise the 256-row items are faster per
+  // row (measured: 32B multistep steps 15.5-17.8 -> 17.1-17.9 ms of
+  // attention with 384-row items for every sequence they save a pass on).
+  std::vector<int> members[kAttnClasses];
   int ao_rpi = kAttnRows / 2;  // attention + O launch: 64-row items unless a sequence has more rows
   for (int b = 0; b < B; ++b) {
     const int R = (seqs[b].k + 1) * G;
     if (R > kAttnRows / 2) ao_rpi = kAttnRows;
-    members[flow || attn_o ? 1 : R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2].push_back(b);
+    int cl = R <= kClassRows[0] ? 0 : (R <= kClassRows[1] || dh != 128) ? 1 : 2;
+    if (cl == 2 && (R - 1) % kClassRows[2] < kClassRows[0] &&
+        (R + kClassRows[3] - 1) / kClassRows[3] < (R + kClassRows[2] - 1) / kClassRows[2])
+      cl = 3;
+    members[flow || attn_o ? 1 : cl].push_back(b);
   }
-  Plan plans[3];
+  Plan plans[kAttnClasses];
   std::vector<AttnItem> items_all, heads_all;
-  std::array<int, 12> attn_key{};
+  std::array<int, 4 * kAttnClasses> attn_key{};
   size_t part_used = 0;
-  for (int cl = 0; cl < 3; ++cl) {
+  for (int cl = 0; cl < kAttnClasses; ++cl) {
     if (members[cl].empty()) continue;
     Plan& pl = plans[cl];
     if (!plan_attention(c, *k->hs, seqs, members[cl], flow ? k->flow_min_items : k->attn_min_items,
@@ -1009,7 +1021,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // fragments per weight byte); for long-K GEMMs 4 strips plus a K split;
   // otherwise 2 strips, or for one row tile 1 strip when that fills the GPU;
   // K-split if still too few.
-  auto skinny_shape = [&](int epi, int N, int K, int family, bool single, int& ns, int& splits) {
+  auto skinny_shape = [&](int epi, int N, int K, int family, bool single, int mblocks, int mt_block, int& ns,
+                          int& splits) {
     const int nb8 = N / 128 * mblocks, nb4 = N / 64 * mblocks, nb2 = N / 32 * mblocks;
     const int KT = K / 32, NT = N / 16;
     const int want = k->gemm_min_blocks;
@@ -1017,7 +1030,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     splits = 1;
     // 8 strips per workgroup halve the activation fragments per weight byte:
     // two row tiles, or three and four on the single-pass activation
-    if ((mt_block == 2 || (mt_block >= 3 && single && k->ns8_mt3)) && N % 128 == 0 && nb8 >= want) {
+    if ((mt_block == 2 || (mt_block >= 3 && mt_block <= 4 && single && k->ns8_mt3)) && N % 128 == 0 &&
+        nb8 >= want) {
       ns = 8;
     } else if (nb4 >= want) {
       ns = 4;
@@ -1071,7 +1085,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       a.part = sx.gemm_part;
       a.cnt = sx.gemm_cnt;
       int ns = 4, splits = 1;
-      skinny_shape(epis[i], Ns[i], Ks[i], fams[i], false, ns, splits);
+      skinny_shape(epis[i], Ns[i], Ks[i], fams[i], false, mblocks, mt_block, ns, splits);
       if (ns == 8) ns = 4;  // the one-launch step compiles 1, 2 and 4 strips
       f.ns[i] = ns;
       f.splits[i] = splits;
@@ -1313,18 +1327,20 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
     const bool single = lm_head && MT > 2 &&
                         ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
+    // five single-pass row tiles: one block, so the weights are read once
+    const int mblocks_g = single && MT == 5 ? 1 : mblocks, mt_block_g = single && MT == 5 ? 5 : mt_block;
     int ns = 4, splits = 1;
-    skinny_shape(epi, N, K, family, single, ns, splits);
+    skinny_shape(epi, N, K, family, single, mblocks_g, mt_block_g, ns, splits);
     if (epi == EPI_LM) {
       lm_parts = a.NT / ns;
       a.n_part = lm_parts;
     }
     ProfScope ps(k, family, (double)N * K * 2.0);
-    HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks, mt_block, !single, s));
+    HIP_TRY(launch_gemm(epi, a, ns, splits, mblocks_g, mt_block_g, !single, s));
     return HVD_OK;
   };
-  double kv_bytes_cl[3] = {0, 0, 0};  // KV bytes each attention launch reads
-  for (int cl = 0; cl < 3; ++cl)
+  double kv_bytes_cl[kAttnClasses] = {};  // KV bytes each attention launch reads
+  for (int cl = 0; cl < kAttnClasses; ++cl)
     for (int b : members[cl]) kv_bytes_cl[cl] += (double)(seqs[b].ctx + seqs[b].k + 1) * kvd * 2 * 2;
 
   for (int l = 0; l < c.n_layers; ++l) {
@@ -1435,7 +1451,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         a.MTtot = MT;
         a.tree_mask = d_mask;
         // one launch per row class, then the combine passes
-        for (int cl = 0; cl < 3; ++cl) {
+        for (int cl = 0; cl < kAttnClasses; ++cl) {
           const Plan& pl = plans[cl];
           if (pl.items.empty()) continue;
           a.items = d_items + pl.item0;
@@ -1444,7 +1460,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
           ProfScope ps(k, PF_ATTN, kv_bytes_cl[cl]);
           HIP_TRY(launch_attn(a, (int)pl.items.size(), pl.chunk, pl.rpi, k->attn_max_np, s));
         }
-        for (int cl = 0; cl < 3; ++cl) {
+        for (int cl = 0; cl < kAttnClasses; ++cl) {
           const Plan& pl = plans[cl];
           if (pl.heads.empty()) continue;
           CombineArgs cb{};

@@ -217,7 +217,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
     // for all tiles).  Every position is computed; those past the end are
     // masked, so no load is conditional.  Tile 0 is live whenever any is.
     constexpr int NB = CH / 16;                      // 16-position blocks
-    constexpr int SG = NB < 4 / TPW ? NB : 4 / TPW;  // blocks per score group (register budget)
+    // blocks per score group (register budget; at least one block pair)
+    constexpr int SG0 = 4 / TPW < 2 ? 2 : 4 / TPW;
+    constexpr int SG = NB < SG0 ? NB : SG0;
     if (tile_on[0]) {
       int lim[TPW];  // last visible position of each tile's rows, sub-chunk-relative
 #pragma unroll

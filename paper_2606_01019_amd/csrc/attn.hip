@@ -102,6 +102,10 @@ hipError_t launch_attn(const AttnArgs& a, int n_items, int chunk, int rows_per_i
     case 256:
       if (a.dh == 128) return launch_attn_dh<128, 8, 2>(a, n_items, np < 8 ? np : 8, s);
       return hipErrorInvalidValue;
+    case 384:  // three row tiles per wave: 2-page sub-chunks only (register budget)
+      if (a.dh != 128) return hipErrorInvalidValue;
+      hvd_launch((verify_attn<128, 2, 8, 3>), dim3(n_items), dim3(512), attn_lds_bytes(128, 2), s, a);
+      return hipGetLastError();
   }
   return hipErrorInvalidValue;
 }
@@ -157,6 +161,7 @@ hipError_t attn_set_lds_limit() {
   if (e == hipSuccess) e = set_lds<128, 2, 8, 2>();
   if (e == hipSuccess) e = set_lds<128, 4, 8, 2>();
   if (e == hipSuccess) e = set_lds<128, 8, 8, 2>();
+  if (e == hipSuccess) e = set_lds<128, 2, 8, 3>();
   return e;
 }
 

@@ -58,6 +58,14 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
   switch (mt) {
     case 1: launch_one<1, NS, EPI, true>(a, splits, mblocks, s); break;
     case 2: launch_one<2, NS, EPI, true>(a, splits, mblocks, s); break;
+    case 5:  // one block of five single-pass row tiles (65-80 rows): the weights are read once
+      if constexpr (kSingle && NS <= 4) {
+        if (!hi_lo) {
+          launch_one<5, NS, EPI, false>(a, splits, mblocks, s);
+          break;
+        }
+      }
+      return hipErrorInvalidValue;
     case 3:
     case 4:
       if constexpr (NS == 8) {  // 8-strip blocks at 3-4 row tiles: single pass only (LDS)

@@ -345,7 +345,8 @@ bool attn_o_supported(int dh, int np, int MT, int KT, int NT, int n_cus);
 hipError_t launch_attn_o(const AttnOArgs& a, int np, int rows_per_item, int MT, hipStream_t s);
 hipError_t attn_o_set_lds_limit();
 
-constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup
+constexpr int kGemmMaxMT = 4;  // 16-row tiles of one GEMM workgroup (5 for single-pass GEMMs of 65-80 rows)
+constexpr int kGemmPadMT = 5;  // row tiles of padding after every GEMM operand
 
 // Static per-device scratch of hvd_verify_noalloc (scratch.hip): its device
 // address on the current device, taken once per device.

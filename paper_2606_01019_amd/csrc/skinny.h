@@ -47,7 +47,7 @@ template <int MT, int NS, int EPI>
 struct EpiRegs {
   static constexpr int ROWS = MT * 16, COLS = NS * 16;
   static constexpr bool NORM = EPI != EPI_RESID;  // GEMM input is RMS-normalised
-  static constexpr int TPR = ROWS <= 16 ? 32 : ROWS <= 32 ? 16 : 8;  // threads per row of sums of squares
+  static constexpr int TPR = ROWS <= 16 ? 32 : ROWS <= 32 ? 16 : ROWS <= 64 ? 8 : 4;  // threads per row of sums of squares
   static constexpr int SSQ = 4;  // float4 of sums of squares per thread held here (more: read late)
   static constexpr int XQ = EPI == EPI_RESID ? (ROWS * COLS / 4 + 511) / 512 : 1;
   static constexpr int RQ = EPI == EPI_QKV ? (ROWS * COLS / 2 + 511) / 512 : 1;
