@@ -1030,8 +1030,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     splits = 1;
     // 8 strips per workgroup halve the activation fragments per weight byte:
     // two row tiles, or three and four on the single-pass activation
-    if ((mt_block == 2 || (mt_block >= 3 && mt_block <= 4 && single && k->ns8_mt3)) && N % 128 == 0 &&
-        nb8 >= want) {
+    if ((mt_block == 2 || (mt_block >= 3 && (mt_block <= 4 || epi == EPI_SILU || epi == EPI_LM) && single && k->ns8_mt3)) &&
+        N % 128 == 0 && nb8 >= want) {
       ns = 8;
     } else if (nb4 >= want) {
       ns = 4;

@@ -16,6 +16,10 @@ namespace hvd {
 // these launches are not limited by weight bytes in flight.)
 constexpr int gemm_occupancy(int MT) { return MT <= 2 ? 4 : 2; }
 constexpr int gemm_depth(int MT, int NS, bool HL) {
+  // 8 strips x 5 row tiles (gate/up, LM head at 65-80 rows): the accumulators leave
+  // room for one stage; measured faster than 4 strips with three stages
+  // (twice the workgroups, which then run in two rounds at one per CU)
+  if (MT == 5 && NS == 8) return 1;
   const int budget = gemm_occupancy(MT) == 4 ? 80 : (HL ? 160 : 128);
   const int d = budget / (4 * (NS + (HL ? 2 : 1) * MT));
   return d < 1 ? 1 : (d > 8 ? 8 : d);
@@ -403,7 +407,7 @@ __device__ __forceinline__ SkinnyCoord skinny_coord() {
 // not fit), the reduced tile and the epilogue inputs.
 template <int MT, int NS, int EPI>
 struct SkinnySmem {
-  static constexpr int NH = (NS == 8 && MT == 4) ? 2 : 1;
+  static constexpr int NH = (NS == 8 && MT >= 4) ? 2 : 1;
   float red[4][NS / NH][MT][256];
   float tile[MT * 16][NS * 16 + 1];
   EpiPre<MT, NS, EPI> pre;
