@@ -450,7 +450,8 @@ size_t carve_kv(hvd_kv_s* k, const hvd_config& c, int max_seqs, int n_pages, voi
   k->gemm_cnt = cv.take<uint32_t>(kGemmCounters);
   k->inv_rms = cv.take<float>(Mp);
   k->g = cv.take<int32_t>(Mp);
-  k->out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)max_seqs);  // [B][2] results, then [B][63] tree paths
+  // [B][2] results, then [B][63] tree paths, then an error word
+  k->out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)max_seqs + 1);
   k->counter = cv.take<uint32_t>(64);
   k->part_o = cv.take<float>((size_t)kPartSlots * kAttnRows * c.head_dim);
   k->part_ml = cv.take<float>((size_t)kPartSlots * kAttnRows * 2);
@@ -533,7 +534,7 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   }
   carve_kv(k, c, max_seqs, n_pages, k->base);
   if (hipHostMalloc((void**)&k->meta_host, k->meta_ints * 4, hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&k->out_host, (2 + kMaxTreeNodes) * (size_t)max_seqs * 4, hipHostMallocDefault) !=
+      hipHostMalloc((void**)&k->out_host, ((2 + kMaxTreeNodes) * (size_t)max_seqs + 1) * 4, hipHostMallocDefault) !=
           hipSuccess) {
     if (k->meta_host) (void)hipHostFree(k->meta_host);
     if (k->owned) (void)hipFree(k->base);
@@ -863,7 +864,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // Attention + merge + O GEMM as one launch (attn_o.hip): up to two row
   // tiles, head dim 128, an O GEMM of K = 4096 with at most one strip per CU;
   // every sequence's rows in 128-row items.
-  const bool attn_o = !flow && k->use_attn_o && !acap && (MT == 1 || MT == 2) &&
+  const bool attn_o = !flow && k->use_attn_o && lm_head && !acap && (MT == 1 || MT == 2) &&
                       attn_o_supported(dh, 2, MT, qd / 32, D / 16, k->n_cus);
   // the attention workgroups of that launch: the CUs' second slots beside the O strips
   const int ao_attn_wgs = attn_o ? std::min(2 * k->n_cus - D / 16, k->n_cus) : 0;
@@ -1212,7 +1213,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     ac.out = sx.out;
     ac.counter = sx.counter;
     ac.path = sx.out + 2 * B;
-    ac.flow_err = sx.flow_cnt;
+    ac.err_word = sx.flow_cnt;
+    ac.err_index = 2 * B;
     ProfScope ps(k, PF_OTHER, 0.0);
     HIP_TRY(launch_accept(ac, s));
     return HVD_OK;
@@ -1546,6 +1548,10 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     ac.counter = sx.counter;
     ac.tree_parent = d_parent;
     ac.path = sx.out + 2 * B;
+    if (attn_o) {  // bounded waits inside the attention + O launches
+      ac.err_word = sx.flow_cnt;
+      ac.err_index = (tree ? 2 + kMaxTreeNodes : 2) * B;
+    }
     if (acap) {
       ac.astate = acap->state;
       ac.hist = acap->hist;
@@ -1625,12 +1631,13 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     HIP_TRY(hipGraphLaunch(it->second, s));
   }
   if (lm_head)  // results, and for trees the accepted paths behind them
-    HIP_TRY(hipMemcpyAsync(k->out_host, sx.out, ((tree ? 2 + kMaxTreeNodes : 2) * (size_t)B + (flow ? 1 : 0)) * 4,
+    HIP_TRY(hipMemcpyAsync(k->out_host, sx.out,
+                           ((tree ? 2 + kMaxTreeNodes : 2) * (size_t)B + (flow || attn_o ? 1 : 0)) * 4,
                            hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (k->prof) prof_collect(k);
-  if (flow && k->out_host[2 * B] != 0)
-    return set_err(HVD_ERR_DEVICE, "one-launch verify step: a dependency wait gave up (results invalid)");
+  if (lm_head && (flow || attn_o) && k->out_host[(tree ? 2 + kMaxTreeNodes : 2) * B] != 0)
+    return set_err(HVD_ERR_DEVICE, "a bounded in-kernel wait gave up (results invalid)");
   return HVD_OK;
 }
 
@@ -1676,7 +1683,7 @@ hvd_status carve_static(hvd_kv_s* k, int M, int B, StepScratch& sx) {
   sx.counter = cv.take<uint32_t>(64);
   sx.gemm_cnt = cv.take<uint32_t>(kGemmCounters);
   sx.flow_cnt = cv.take<uint32_t>(kFlowCounterWords);
-  sx.out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)B);
+  sx.out = cv.take<int32_t>((2 + kMaxTreeNodes) * (size_t)B + 1);
   sx.g = cv.take<int32_t>(Mp);
   sx.inv_rms = cv.take<float>(Mp);
   sx.lm_val = cv.take<float>(Mp * (size_t)k->n_part_lm);

@@ -175,7 +175,8 @@ struct AcceptArgs {
   int32_t* astate;
   int32_t* hist;
   int hist_cap;
-  const uint32_t* flow_err;  // nullable: the one-launch step's error word, copied to out[2B]
+  const uint32_t* err_word;  // nullable: the step's error word of bounded in-kernel waits, copied to out[err_index]
+  int err_index;             // after the results (and a tree step's paths)
 };
 // Moves the K/V of each tree sequence's accepted path from the nodes'
 // positions (ctx + 1 + node) to the chain positions ctx + 1 .. ctx + a.

@@ -183,7 +183,7 @@ __global__ __launch_bounds__(256) void argmax_accept(AcceptArgs a) {
   }
   __syncthreads();  // every thread has read the step count
   if (threadIdx.x == 0) {
-    if (a.flow_err) a.out[2 * a.B] = (int32_t)*a.flow_err;
+    if (a.err_word) a.out[a.err_index] = (int32_t)*a.err_word;
     *a.counter = 0u;
     if (a.astate) a.astate[2 * a.B] = step + 1;
   }
