@@ -225,8 +225,15 @@ extern "C" hvd_status hvd_model_load(const hvd_config* cfg, const uint16_t* cons
     delete m;
     return e;
   };
-  if (hipMalloc(&staging, stage_elems * 2) != hipSuccess || hipMalloc(&dmap, map_elems * 4) != hipSuccess)
-    return fail(set_err(HVD_ERR_OOM, "hipMalloc of load staging failed"));
+  hipError_t ea = hipMalloc(&staging, stage_elems * 2);
+  if (ea == hipSuccess) ea = hipMalloc(&dmap, map_elems * 4);
+  if (ea != hipSuccess) {
+    size_t free_b = 0, total_b = 0;
+    (void)hipMemGetInfo(&free_b, &total_b);
+    return fail(set_err(HVD_ERR_OOM, std::string("hipMalloc of load staging (") + std::to_string(stage_elems * 2) +
+                                         " bytes) failed: " + hipGetErrorString(ea) + "; device memory free " +
+                                         std::to_string(free_b) + " of " + std::to_string(total_b) + " bytes"));
+  }
 
   auto ident = [](size_t n) {
     std::vector<int32_t> r(n);

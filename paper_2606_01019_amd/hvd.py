@@ -75,6 +75,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     global _lib
     if _lib is not None:
         return _lib
+    # torch first: it loads its own HIP runtime, which libhvd.so then shares
+    # (loaded the other way round, the process would hold two runtimes)
+    import torch  # noqa: F401
     if not os.path.exists(path):
         raise RuntimeError(f"libhvd.so not built at {path}: run `python -m paper_2606_01019_amd.build`")
     L = ctypes.CDLL(path)
