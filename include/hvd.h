@@ -265,14 +265,14 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   measured slightly faster for single-sequence verifies.  Results are
  *   identical either way.  Profiling (hvd_profile_enable) always launches
  *   eagerly.
- * HVD_OPT_MLP_SINGLE (default 1): in verify forwards of more than 32 rows,
- *   the gate/up and down GEMMs take the fp16 activation alone (11 bits)
- *   instead of the fp16 hi + lo pair (~22 bits), halving their activation
- *   traffic and MFMA work; 0 keeps the pair.  Prefill always uses the pair.
- *   Logit differences stay within the verify step's tolerance.
+ * HVD_OPT_MLP_SINGLE (default 1): in verify forwards the gate/up and down
+ *   GEMMs take the fp16 activation alone (11 bits) instead of the fp16
+ *   hi + lo pair (~22 bits), halving their activation traffic and MFMA
+ *   work; 0 keeps the pair.  Prefill always uses the pair.  Logit
+ *   differences stay within the verify step's tolerance.
  * HVD_OPT_LM_SINGLE (default 1): likewise for the LM-head GEMM of verify
- *   forwards of more than 32 rows (its rounding error, ~1e-4 on the logits,
- *   is far below the tolerance); 0 keeps the pair.
+ *   forwards (its rounding error, ~1e-4 on the logits, is far below the
+ *   tolerance); 0 keeps the pair.
  * HVD_OPT_FLOW (default 0): 1 runs verify steps of at most 32 rows (head dim
  *   128, at most 128 query rows per kv head per sequence, chain drafts) as
  *   one kernel launch in which each phase's workgroups request their weights

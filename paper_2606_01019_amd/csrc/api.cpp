@@ -1331,8 +1331,10 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, sx.inv_rms, s));
       return HVD_OK;
     }
-    // verify batches over 32 rows: MLP GEMMs on the hi activation part (as the tiled path)
-    const bool single = lm_head && MT > 2 &&
+    // verify forwards: MLP and LM-head GEMMs on the hi activation part (as the
+    // tiled path); measured at batch 1, context 2048: 3.48 -> 3.39 ms per step at
+    // k = 8 (gate/up 38.3 -> 36.0 us, down 23.9 -> 22.9 us per layer)
+    const bool single = lm_head &&
                         ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
     // five single-pass row tiles: one block, so the weights are read once
     const int mblocks_g = single && MT == 5 ? 1 : mblocks, mt_block_g = single && MT == 5 ? 5 : mt_block;

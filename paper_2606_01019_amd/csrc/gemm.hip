@@ -56,8 +56,24 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
   // single-pass activations only for the MLP and LM-head GEMMs at 3-4 row tiles
   constexpr bool kSingle = EPI == EPI_SILU || EPI == EPI_RESID || EPI == EPI_LM;
   switch (mt) {
-    case 1: launch_one<1, NS, EPI, true>(a, splits, mblocks, s); break;
-    case 2: launch_one<2, NS, EPI, true>(a, splits, mblocks, s); break;
+    case 1:
+      if constexpr (kSingle) {
+        if (!hi_lo) {
+          launch_one<1, NS, EPI, false>(a, splits, mblocks, s);
+          break;
+        }
+      }
+      launch_one<1, NS, EPI, true>(a, splits, mblocks, s);
+      break;
+    case 2:
+      if constexpr (kSingle) {
+        if (!hi_lo) {
+          launch_one<2, NS, EPI, false>(a, splits, mblocks, s);
+          break;
+        }
+      }
+      launch_one<2, NS, EPI, true>(a, splits, mblocks, s);
+      break;
     case 5:  // one block of five single-pass row tiles (65-80 rows): the weights are read once
              // (8 strips for gate/up and the LM head only: the residual epilogue's LDS would not fit)
       if constexpr (kSingle && (NS <= 4 || EPI == EPI_SILU || EPI == EPI_LM)) {

@@ -273,13 +273,13 @@ class KVCache:
         return a.value, b.value, bool(c.value)
 
     def set_mlp_single(self, on: bool):
-        """Large-batch verify MLP GEMMs on the fp16 activation alone (default)
-        or on the fp16 hi + lo pair."""
+        """Verify MLP GEMMs on the fp16 activation alone (default) or on the
+        fp16 hi + lo pair."""
         _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_MLP_SINGLE, 1 if on else 0))
 
     def set_lm_single(self, on: bool):
-        """Large-batch verify LM head on the fp16 activation alone (default)
-        or on the fp16 hi + lo pair."""
+        """Verify LM head on the fp16 activation alone (default) or on the
+        fp16 hi + lo pair."""
         _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_LM_SINGLE, 1 if on else 0))
 
     def set_flow(self, on: bool):
