@@ -387,6 +387,7 @@ struct hvd_kv_s {
   float* part_ml = nullptr;
   int32_t* meta_dev = nullptr;
   int32_t* meta_host = nullptr;
+  const int32_t* meta_host_dev = nullptr;  // meta_host as the device sees it
   size_t meta_ints = 0;
   int32_t* out_host = nullptr;
   StepScratch sx;                 // the handle's own step scratch
@@ -547,6 +548,13 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
     if (k->owned) (void)hipFree(k->base);
     delete k;
     return set_err(HVD_ERR_OOM, "pinned host staging allocation failed");
+  }
+  if (hipHostGetDevicePointer((void**)&k->meta_host_dev, k->meta_host, 0) != hipSuccess) {
+    (void)hipHostFree(k->meta_host);
+    (void)hipHostFree(k->out_host);
+    if (k->owned) (void)hipFree(k->base);
+    delete k;
+    return set_err(HVD_ERR_DEVICE, "device address of the pinned metadata staging failed");
   }
   // Zero the whole workspace once: padding rows of every operand stay finite.
   // (KV pages are zeroed too; their contents are only read once written.)
@@ -1002,7 +1010,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     }
   }
   int32_t* const meta_dev = acap ? acap->meta : k->meta_dev;
-  HIP_TRY(hipMemcpyAsync(meta_dev, h, off * 4, hipMemcpyHostToDevice, s));
+  if (acap) HIP_TRY(hipMemcpyAsync(meta_dev, h, off * 4, hipMemcpyHostToDevice, s));
+  else HIP_TRY(launch_copy_words(meta_dev, k->meta_host_dev, off, s));  // the previous step has finished with it
   if (acap) {
     // the page-table updates are applied once, here; the replays carry none
     // (replaying them could undo later updates of other sequences)

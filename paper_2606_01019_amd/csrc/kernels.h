@@ -334,6 +334,9 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int B, hipStream_t s);
 hipError_t launch_async_plan(const AsyncPlanArgs& a, hipStream_t s);
 hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* pt, int pt_stride, hipStream_t s);
+// n 32-bit words from src (device-accessible, e.g. pinned host memory) to dst
+// (device); both 16-byte aligned.
+hipError_t launch_copy_words(int32_t* dst, const int32_t* src, size_t n, hipStream_t s);
 // One-launch verify step over MT (1 or 2) row tiles; false if this shape has
 // no compiled variant (head dim, strips per workgroup, pages per sub-chunk).
 bool flow_supported(int MT, int dh, int np, const int* ns);

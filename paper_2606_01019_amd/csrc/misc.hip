@@ -2,6 +2,8 @@
 // gather with the first RMSNorm's operand, and the fused argmax finalize +
 // greedy accept.
 #include "common.h"
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace hvd {
@@ -297,6 +299,24 @@ __global__ __launch_bounds__(256) void pt_update(const int32_t* upd, const int32
 
 hipError_t launch_pt_update(const int32_t* upd, const int32_t* n_upd, int32_t* pt, int pt_stride, hipStream_t s) {
   hvd_launch(pt_update, dim3(1), dim3(256), 0, s, upd, n_upd, pt, pt_stride);
+  return hipGetLastError();
+}
+
+// The step's metadata from pinned host memory into device memory, read by
+// a kernel (16 bytes per lane): it starts a few microseconds after launch,
+// where a DMA copy first waits for its copy engine.
+__global__ __launch_bounds__(256) void copy_words(int32_t* __restrict__ dst, const int32_t* __restrict__ src, int n) {
+  const int q = n >> 2;  // whole 16-byte units
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < q; i += gridDim.x * 256)
+    ((uint4*)dst)[i] = ((const uint4*)src)[i];
+  for (int i = 4 * q + blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) dst[i] = src[i];
+}
+
+hipError_t launch_copy_words(int32_t* dst, const int32_t* src, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (n > (size_t)INT32_MAX || ((uintptr_t)dst & 15) || ((uintptr_t)src & 15)) return hipErrorInvalidValue;
+  const int blocks = (int)std::min<size_t>(64, (n / 4 + 255) / 256 + 1);
+  hvd_launch(copy_words, dim3(blocks), dim3(256), 0, s, dst, src, (int)n);
   return hipGetLastError();
 }
 

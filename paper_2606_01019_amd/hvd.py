@@ -90,11 +90,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hvd_kv_bytes": (SZ, [ctypes.POINTER(Config), I32, I32]),
         "hvd_kv_alloc": (I32, [P, I32, I32, P, SZ, P, ctypes.POINTER(P)]),
         "hvd_kv_free": (None, [P]),
-        "hvd_prefill": (I32, [P, P, I32, PI32, I32]),
-        "hvd_verify": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
-        "hvd_verify_noalloc": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
-        "hvd_verify_tree": (I32, [P, P, I32, PI32, PI32, PI32, PI32, PI32, PI32, PI32, PI32, P]),
-        "hvd_commit": (I32, [P, P, I32, PI32, PI32]),
+        "hvd_prefill": (I32, [P, P, I32, P, I32]),
+        "hvd_verify": (I32, [P, P, I32, P, P, P, P, P, P, P]),
+        "hvd_verify_noalloc": (I32, [P, P, I32, P, P, P, P, P, P, P]),
+        "hvd_verify_tree": (I32, [P, P, I32, P, P, P, P, P, P, P, P, P]),
+        "hvd_commit": (I32, [P, P, I32, P, P]),
         "hvd_truncate": (I32, [P, I32, I32, I32]),
         "hvd_seq_free": (I32, [P, I32]),
         "hvd_seq_info": (I32, [P, I32, PI32, PI32, PI32]),
@@ -104,7 +104,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    ctypes.POINTER(ctypes.c_double)]),
         "hvd_kv_set_option": (I32, [P, I32, I32]),
         "hvd_last_error": (ctypes.c_char_p, []),
-        "hvd_async_begin": (I32, [P, P, I32, PI32, PI32, PI32, I32, P, P, P, P, I32, PI32, ctypes.POINTER(P)]),
+        "hvd_async_begin": (I32, [P, P, I32, P, P, P, I32, P, P, P, P, I32, P, ctypes.POINTER(P)]),
         "hvd_async_step": (I32, [P, I32]),
         "hvd_async_end": (I32, [P, PI32]),
         "hvd_flow_trace": (I32, [P, P, ctypes.c_int64]),
@@ -135,7 +135,9 @@ def _i32(a):
 
 
 def _ptr(a):
-    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if a is not None and a.size else None
+    # the address as an int (the int32-array parameters are declared void*):
+    # ctypes' data_as costs microseconds per call on the step's path
+    return a.ctypes.data if a is not None and a.size else None
 
 
 def _stream(stream):
@@ -217,8 +219,11 @@ class KVCache:
         ids = _i32(seq_ids)
         ctx = _i32(ctx_lens)
         lens = _i32([len(d) for d in drafts])
-        flat = _i32(np.concatenate([np.asarray(d, dtype=np.int64).reshape(-1) for d in drafts])
-                    if len(drafts) else np.zeros(0))
+        if len(drafts) == 1:
+            flat = _i32(np.asarray(drafts[0]).reshape(-1))
+        else:
+            flat = _i32(np.concatenate([np.asarray(d, dtype=np.int64).reshape(-1) for d in drafts])
+                        if len(drafts) else np.zeros(0))
         acc = np.zeros(ids.size, dtype=np.int32)
         nxt = np.zeros(ids.size, dtype=np.int32)
         lp = None
