@@ -120,3 +120,27 @@ def check_golden(rep: Report, L, rec, sample_ids, a_gpu, next_gpu, tol=LOGIT_TOL
         assert a_gpu == rec["accepted"] and next_gpu == rec["next"], (a_gpu, rec["accepted"], next_gpu, rec["next"])
         return False
     return a_gpu != rec["accepted"] or next_gpu != rec["next"]
+
+
+def load_whole_rows(name):
+    """Whole oracle logit rows stored beside a record (tests/golden/<name>,
+    written by make_golden.py): {key: float64 rows}, or None when absent.
+    Values are int16 multiples of the stored step (|quantisation| <= step/2)."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", name)
+    if not os.path.exists(path):
+        return None
+    z = np.load(path)
+    step = float(z["step"])
+    return {k: z[k].astype(np.float64) * step for k in z.files if k != "step"}, step
+
+
+def check_whole_rows(L, stored, step, tol=LOGIT_TOL):
+    """Rows 0 and k of one verify (L [k+1, V]) against the oracle's whole
+    rows; returns the max abs difference (asserted <= tol + step/2)."""
+    k = L.shape[0] - 1
+    got = np.asarray(L, dtype=np.float64)[[0, k]]
+    assert got.shape == stored.shape, (got.shape, stored.shape)
+    err = float(np.abs(got - stored).max())
+    assert err <= tol + step / 2, f"whole-row logit error {err:.3e} > {tol}"
+    return err

@@ -12,6 +12,9 @@ path of the same code would need twice the memory and time); a reduced-depth
 pin (tests/test_oracle_precision.py) bounds the float32/float64 difference.
 
 Usage: python tests/golden/make_golden.py cfg2 [cfg3 cfg4 cfg5 tree2 cfg5_full] [--spill DIR]
+       python tests/golden/make_golden.py rows_cfg2 [rows_cfg3 rows_cfg4 rows64_cfg2] --spill DIR
+(the rows_ passes add whole logit rows to an existing record, rows64_ the
+float64 oracle's rows; see case_rows_8b)
 """
 
 import json
@@ -372,6 +375,63 @@ def case_cfg5_full(spill=None, n_steps=4, resident=38):
             "full_rows": "cfg5_full_rows.npz", "full_row_step": FULL_ROW_STEP}
 
 
+def _rows_8b_verifies(name):
+    """(key, context, draft, stored step record) of every verify of an 8B
+    record whose rows 0 and k are kept whole."""
+    cfg = SHAPE_8B
+    with open(os.path.join(HERE, f"{name}.json")) as f:
+        gold = json.load(f)
+    if name in ("cfg2", "cfg3"):
+        make = wt.zipf_context if gold["context_kind"] == "zipf" else wt.segment_context
+        ctx = make(wt.rng_for(*gold["context_seed"]), gold["context_len"], cfg.vocab)
+        return gold, [(f"step{i}", ctx, st) for i, st in enumerate(gold["steps"])]
+    assert name == "cfg4"
+    plans = batches.mixed_batch_plan()
+    return gold, [(f"seq{r['seq']}", batches.mixed_batch_context(plans[r["seq"]], cfg.vocab), r)
+                  for r in gold["seqs"]]
+
+
+def case_rows_8b(name, spill=None, dtype=np.float32):
+    """Whole logit rows for an existing 8B record (cfg2, cfg3 or cfg4): the
+    oracle with streamed bf16 weights re-runs the verify of every stored draft
+    on the same context and keeps rows 0 and k whole (int16 multiples of
+    FULL_ROW_STEP).  In float32 (oracle/streamed.py; <name>_rows.npz) the
+    re-run must reproduce the stored record: sampled logits within 2e-3 (the
+    two float32 oracles differ only in summation order) and the same argmax,
+    accepted length and next token away from near ties.  In float64 (the
+    plain OracleModel widening each streamed matrix; <name>_rows_f64.npz)
+    nothing is asserted: tests/test_oracle_precision.py bounds the float32
+    drift at full depth from the two files."""
+    from oracle.streamed import StreamedOracleModel
+    cfg = SHAPE_8B
+    f64 = np.dtype(dtype) == np.float64
+    gold, items = _rows_8b_verifies(name)
+    ids = np.asarray(gold["sample_ids"])
+    store = SpillStore(cfg, 0, spill)
+    m = OracleModel(cfg, store, dtype=np.float64, cache=False) if f64 else StreamedOracleModel(cfg, store)
+    rows, worst, last_ctx, st = {}, 0.0, None, None
+    for key, ctx, rec in items:
+        if ctx is not last_ctx:
+            log(f"rows {name}: {key} prefill {len(ctx)}")
+            st = oracle.prefill(m, ctx)
+            last_ctx = ctx
+        d = np.asarray(rec["draft"], dtype=np.int64)
+        res = oracle.verify(m, st, d)
+        dev = float(np.abs(res.logits[:, ids] - np.asarray(rec["sample_logits"])).max())
+        worst = max(worst, dev)
+        if not f64:
+            assert dev <= 2e-3, f"{name} {key}: re-run differs from the stored record by {dev:.2e}"
+            clear = np.asarray(rec["margin"]) >= 2e-3
+            assert np.array_equal(np.asarray(res.argmax)[clear], np.asarray(rec["argmax"])[clear]), key
+            if clear[:rec["accepted"] + 1].all():
+                assert res.accepted == rec["accepted"] and res.next_token == rec["next"], key
+        rows[key] = quantize_rows(res.logits[[0, len(d)]])
+        log(f"rows {name}: {key} k={len(d)} accepted={res.accepted} re-run vs record {dev:.2e}")
+    out = f"{name}_rows_f64.npz" if f64 else f"{name}_rows.npz"
+    np.savez_compressed(os.path.join(HERE, out), step=np.float64(FULL_ROW_STEP), **rows)
+    log(f"rows {name}: wrote {out} ({len(rows)} verifies), worst re-run vs record {worst:.2e}")
+
+
 def main():
     import argparse
     ap = argparse.ArgumentParser()
@@ -383,6 +443,10 @@ def main():
     cases = {"cfg2": case_cfg2, "cfg3": case_cfg3, "cfg4": case_cfg4, "cfg5": case_cfg5, "tree2": case_tree2,
              "cfg5_full": lambda: case_cfg5_full(args.spill, args.steps, args.resident)}
     for name in args.cases:
+        if name.startswith("rows_") or name.startswith("rows64_"):  # whole rows of an existing record
+            tag, rec = name.split("_", 1)
+            case_rows_8b(rec, args.spill, np.float64 if tag == "rows64" else np.float32)
+            continue
         t0 = time.time()
         out = cases[name]()
         path = os.path.join(HERE, f"{name}.json")

@@ -1,0 +1,83 @@
+"""Workload 5 at its full depth: the 32B shape with all 64 layers (64 q / 8
+kv heads of 128, SwiGLU 27648, vocab 152064), 8 sequences at context 8192,
+the first verify + commit steps of the multistep plan (k in 4..64).
+Sequences 0 and 1 follow a float32 oracle record written layer-streamed by
+tests/golden/make_golden.py (cfg5_full): sampled logits and each row's
+oracle top ids, argmax, accepted length and next token, and rows 0 and k of
+every verify compared whole (stored as int16 multiples of 2^-11, so the
+stored value is within 2.5e-4 of the oracle's).  Tolerances as everywhere:
+logits max-abs 2e-2; decisions exact except near ties (top-2 margin < 2e-2).
+The worst logit difference at this depth is printed."""
+
+import os
+
+import numpy as np
+import pytest
+
+from tests._parity import Report, check_golden, check_whole_rows, load_whole_rows
+from tests.conftest import load_golden
+from workloads import SHAPE_32B, batches, make_weights, tokens as wt
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def test_multistep_32b_full_depth_against_oracle_record():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    if not os.path.exists(os.path.join(HERE, "golden", "cfg5_full.json")):
+        pytest.skip("no full-depth oracle record")
+    import paper_2606_01019_amd as hvd
+    gold = load_golden("cfg5_full.json")
+    rows_gold, step_q = load_whole_rows(gold["full_rows"])
+    cfg = SHAPE_32B
+    assert gold["n_layers"] == cfg.n_layers
+    V = cfg.vocab
+    print("generating 32B weights (64 layers)", flush=True)
+    w = make_weights(cfg, seed=42)
+    model = hvd.Model(cfg, w)
+    del w
+    plans = batches.multistep_plan()
+    n_seqs = len(plans[0])
+    kv = hvd.KVCache(model, max_seqs=n_seqs, n_pages=n_seqs * ((8192 + 16 * 66) // 16 + 4))
+    ctxs = [batches.multistep_context(b, 8192, V) for b in range(n_seqs)]
+    for b in range(n_seqs):
+        kv.prefill(b, ctxs[b])
+    print("prefill done", flush=True)
+    lens = [8191] * n_seqs
+    gseq = {g["seq"]: g["steps"] for g in gold["seqs"]}
+    live = {b: True for b in gseq}
+    rep = Report()
+    worst_row = 0.0
+    for s in range(gold["n_steps"]):
+        row = plans[s]
+        drafts = []
+        for b in range(n_seqs):
+            if b in gseq and live[b]:
+                drafts.append(np.asarray(gseq[b][s]["draft"], dtype=np.int32))
+            else:
+                drafts.append(wt.random_chain(wt.rng_for("draft", 5, b, s, 1), row[b].k, V))
+        M = sum(len(d) + 1 for d in drafts)
+        lg = torch.empty((M, V), dtype=torch.float32, device="cuda")
+        a, n = kv.verify(list(range(n_seqs)), lens, drafts, logits=lg)
+        L = lg.cpu().numpy().astype(np.float64)
+        r0 = 0
+        for b in range(n_seqs):
+            k = len(drafts[b])
+            if b in gseq and live[b]:
+                Lb = L[r0:r0 + k + 1]
+                worst_row = max(worst_row, check_whole_rows(Lb, rows_gold[f"seq{b}_step{s}"], step_q))
+                if check_golden(rep, Lb, gseq[b][s], gold["sample_ids"], int(a[b]), int(n[b])):
+                    live[b] = False  # a near tie sent the GPU down another branch
+                    print(f"sequence {b} left the oracle trajectory at step {s} (near tie)", flush=True)
+            r0 += k + 1
+        kv.commit(list(range(n_seqs)))
+        lens = [lens[b] + int(a[b]) + 1 for b in range(n_seqs)]
+        print(f"step {s}: {M} rows, {rep}, whole rows max|dlogit| so far {worst_row:.3e}", flush=True)
+    assert rep.rows > 0
+    print(f"64 layers: worst max|dlogit| {max(rep.max_err, worst_row):.3e} (sampled {rep.max_err:.3e}, "
+          f"whole rows {worst_row:.3e})", flush=True)
+    kv.close()
+    model.close()

@@ -13,13 +13,16 @@ tests/golden/make_golden.py from the oracle alone):
   152064) at 4 layers, 8 sequences at context 8192, 16 verify + commit steps
   with k in 4..64; sequences 0 and 1 follow the oracle's trajectory.
 
-Tolerances as everywhere: logits max-abs 2e-2; argmax, accepted length and
+Where make_golden.py has kept them (cfg3_rows.npz, cfg4_rows.npz), rows 0
+and k of every checked verify are also compared whole, over the full
+vocabulary.  Tolerances as everywhere: logits max-abs 2e-2; argmax, accepted length and
 next token exact except near ties (top-2 margin < 2e-2)."""
 
 import numpy as np
 import pytest
 
-from tests._parity import LOGIT_TOL, TIE_MARGIN, Report, check_golden, top2_margin
+from tests._parity import (LOGIT_TOL, TIE_MARGIN, Report, check_golden, check_whole_rows, load_whole_rows,
+                           top2_margin)
 from tests.conftest import load_golden
 from workloads import SHAPE_32B, SHAPE_8B, batches, make_weights, tokens as wt
 
@@ -42,14 +45,17 @@ def test_long_context_cache_drafts(model8b):
     ctx = wt.segment_context(wt.rng_for(*gold["context_seed"]), gold["context_len"], SHAPE_8B.vocab)
     kv.prefill(0, ctx)
     c0, p0 = len(ctx) - 1, int(ctx[-1])
+    whole = load_whole_rows("cfg3_rows.npz")
     rep = Report()
-    for st in gold["steps"]:
+    for i, st in enumerate(gold["steps"]):
         d = np.asarray(st["draft"], dtype=np.int32)
         lg = torch.empty((len(d) + 1, SHAPE_8B.vocab), dtype=torch.float32, device="cuda")
         a, n = kv.verify([0], [c0], [d], logits=lg)
-        check_golden(rep, lg.cpu().numpy(), st, gold["sample_ids"], int(a[0]), int(n[0]))
+        L = lg.cpu().numpy()
+        check_golden(rep, L, st, gold["sample_ids"], int(a[0]), int(n[0]))
+        wr = check_whole_rows(L, whole[0][f"step{i}"], whole[1]) if whole is not None else float("nan")
         kv.truncate(0, c0, p0)
-        print(f"k={len(d)}: accepted={int(a[0])} (oracle {st['accepted']}) {rep}", flush=True)
+        print(f"k={len(d)}: accepted={int(a[0])} (oracle {st['accepted']}) {rep} whole rows {wr:.3e}", flush=True)
 
 
 def test_mixed_batch(model8b):
@@ -80,9 +86,13 @@ def test_mixed_batch(model8b):
     a, n = kv.verify(ids, ctx_lens, drafts, logits=lg)
     L = _split_rows(lg.cpu().numpy(), drafts)
     rep = Report()
+    whole = load_whole_rows("cfg4_rows.npz")
+    worst_row = 0.0
     for b in gold["sampled"]:
         check_golden(rep, L[b], recs[b], gold["sample_ids"], int(a[b]), int(n[b]))
-    print(f"batch of {len(plans)} sequences, {M} rows: {rep}", flush=True)
+        if whole is not None:
+            worst_row = max(worst_row, check_whole_rows(L[b], whole[0][f"seq{b}"], whole[1]))
+    print(f"batch of {len(plans)} sequences, {M} rows: {rep} whole rows {worst_row:.3e}", flush=True)
     # two unchecked sequences verified alone must agree with the batched rows
     for p in plans:
         kv.truncate(p.seq, p.ctx_len - 1, int(ctxs[p.seq][-1]))
