@@ -44,12 +44,12 @@ int prefill_rows(const hvd_config& c) {
   return std::max(128, std::min(512, 2048 / G));
 }
 // Up to 8 row tiles (128 rows) the skinny kernel in row blocks of <= 4
-// tiles beats the tiled kernel and its K-split finish (measured: 65-row
-// verifies and 128-row prefill chunks of the 8B shape)
+// tiles beats the tiled kernel (measured: 65-row verifies and 128-row
+// prefill chunks of the 8B shape)
 constexpr int kSkinnyMaxMT = 8;
 constexpr int kGemmMinBlocks = 192;          // GEMM workgroups below which the shape changes
 constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (one per CU)
-constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its finish pass
+constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its reduction
 constexpr size_t kGemmPartBytes = 64u << 20;  // split-K partial tiles of one GEMM launch
 constexpr int kGemmCounters = 16384;          // split-K arrival counters (output blocks of one launch)
 constexpr int kFlowCounterWords = 1 << 17;    // one-launch step: error word and per-layer counters
@@ -1056,7 +1056,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     } else if (nb2 >= want) {
       ns = 2;
     } else if (mt_block == 1 && epi != EPI_SILU && nb2 * 2 >= want) {
-      ns = 1;  // one strip per workgroup beats a K split plus its finish pass
+      ns = 1;  // one strip per workgroup beats a K split plus its reduction
     } else {
       ns = 2;
       splits = std::max(1, std::min((kGemmSplitTarget + nb2 - 1) / nb2, KT / 64));
@@ -1330,6 +1330,7 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       if (forced) splits = std::max(1, std::min(k->tiled_force[family][1], a.KT / 32));
       else if (nblk < want_t) splits = std::max(1, std::min({4, (want_t + nblk - 1) / nblk, a.KT / 32}));
       while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > sx.gemm_part_bytes) --splits;
+      if (splits > 1 && nblk > kGemmCounters) splits = 1;  // one arrival counter per output tile
       const bool mlp = epi == EPI_SILU || family == PF_DOWN;
       if (epi == EPI_LM) {
         lm_parts = N / tile_bn[tile];

@@ -6,6 +6,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace hvd {
 
 // Item reads go through the constant address space: items are read-only
@@ -43,8 +45,23 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
   constexpr int RPI = 16 * NW * TPW;    // query rows per item
   constexpr int CH = NP * kPage;        // positions per sub-chunk
   constexpr int KSEG = DH / 8;          // 16-byte segments per K row
-  constexpr int VU = CH / 4;            // 8-byte units per V row in LDS
-  constexpr int VM = VU < 16 ? VU : 16; // V swizzle span (units)
+  // V^T in LDS: row d holds the sub-chunk's CH positions in 16-byte
+  // granules, granule 4b + j of 32-position block b holding positions
+  // 32b + 4j .. 32b + 4j + 3 and 32b + 16 + 4j .. + 3 -- exactly the eight
+  // K values one lane group needs as the B operand of a 16x16x32 MFMA over
+  // that block (one 16-byte read, no register shuffling).  Granules are
+  // XOR-swizzled by row so that the 16 rows one read instruction touches at
+  // a time land in distinct banks (64 banks of 4 bytes).
+  constexpr int VGR = CH / 8;                        // granules per row
+  constexpr int VGM = VGR < 16 ? VGR : 16;           // swizzle span (granules)
+  constexpr unsigned VRB = CH >= 128 ? 1 : 128 / CH; // rows per 256 bytes
+  auto vgran = [](int gr, int d) __attribute__((always_inline)) {
+    return (gr & ~(VGM - 1)) | ((gr & (VGM - 1)) ^ (int)(((unsigned)d / VRB) & (VGM - 1)));
+  };
+  // half-word offset within a row of 8-byte unit u (positions 4u .. 4u+3)
+  auto vslot = [&](int u, int d) __attribute__((always_inline)) {
+    return vgran(((u >> 3) << 2) | (u & 3), d) * 8 + ((u >> 2) & 1) * 4;
+  };
   constexpr int LPP = 4 * DH / NT;      // 16-byte loads per thread per page (K and V: 4*DH units)
   static_assert(NP >= 2 && NP <= kItemPages && (NP & (NP - 1)) == 0, "pages per sub-chunk");
   static_assert(LPP >= 1 && LPP * NT == 4 * DH, "page units per thread");
@@ -57,7 +74,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
   static_assert(Hooks::kPending >= 0 && Hooks::kPending < 64, "loads left in flight");
   constexpr int BUF_BYTES = CH * DH * 2 * 2;       // K and V of one sub-chunk
   _Float16* sK = (_Float16*)smem;                  // [CH][DH], segment-swizzled
-  _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], 8-byte-unit-swizzled
+  _Float16* sV = (_Float16*)(smem + CH * DH * 2);  // [DH][CH], granule-regrouped and swizzled
 
   const int kdr = ip->k;
   if (kdr < 0) return;  // grid padding
@@ -195,9 +212,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
             x[e] &= keep;
           }
           const int u0 = pp >> 2;  // 8-byte units (4 positions)
-          uint2* row = (uint2*)(sV + (size_t)d * CH);
-          row[(u0 & ~(VM - 1)) | ((u0 & (VM - 1)) ^ (d & (VM - 1)))] = uint2{x[0], x[1]};
-          row[((u0 + 1) & ~(VM - 1)) | (((u0 + 1) & (VM - 1)) ^ (d & (VM - 1)))] = uint2{x[2], x[3]};
+          _Float16* row = sV + (size_t)d * CH;
+          *(uint2*)(row + vslot(u0, d)) = uint2{x[0], x[1]};
+          *(uint2*)(row + vslot(u0 + 1, d)) = uint2{x[2], x[3]};
         }
       }
     __syncthreads();
@@ -229,111 +246,139 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
       }
       // smallest of them over the wave (its first row: rows ascend)
       const int lim_min = tree ? ctx - 1 - sub : ctx + (rg * RPI + wave * 16) / G - sub;
+      // Waves of two row tiles: the group loop is instantiated per count NQ
+      // of live tiles (a prefix of the wave's tiles), so no per-tile branch
+      // sits inside it, and K and V fragments are read ahead of their
+      // MFMAs.  One tile (whose 4-wave items run two to a CU) measured
+      // slower with the read-ahead's registers; three fill the registers:
+      // there, one instance that tests each tile, fragments read where used.
+      constexpr bool KPIPE = TPW == 2;
+      auto live = [&](int q) __attribute__((always_inline)) { return KPIPE || q == 0 || tile_on[q]; };
+      auto run = [&](auto nq) __attribute__((always_inline)) {
+        constexpr int NQ = decltype(nq)::value;
 #pragma unroll 1
-      for (int g0 = 0; g0 < NB; g0 += SG) {  // not unrolled: keeps each group's LDS reads in its group
-        f32x4 sc[TPW][SG];
+        for (int g0 = 0; g0 < NB; g0 += SG) {  // not unrolled: keeps each group's LDS reads in its group
+          f32x4 sc[TPW][SG];
+          // K fragments one head-dim step ahead of the MFMAs that use them
+          // (three-tile waves: read per step, for registers)
+          f16x8 kf[KPIPE ? 2 : 1][SG];
+          auto read_k = [&](int kd, f16x8 (&dst)[SG]) __attribute__((always_inline)) {
+            const int sg = kd * 4 + lg;
 #pragma unroll
-        for (int kd = 0; kd < DH / 32; ++kd) {
-          const int sg = kd * 4 + lg;
-          f16x8 kf[SG];
+            for (int b = 0; b < SG; ++b) {
+              const int p = (g0 + b) * 16 + (lane & 15);
+              dst[b] = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
+            }
+          };
+          if constexpr (KPIPE) read_k(0, kf[0]);
 #pragma unroll
-          for (int b = 0; b < SG; ++b) {
-            const int p = (g0 + b) * 16 + (lane & 15);
-            kf[b] = *(const f16x8*)(sK + p * DH + ((sg ^ (p & 15)) & (KSEG - 1)) * 8);
+          for (int kd = 0; kd < DH / 32; ++kd) {
+            if constexpr (KPIPE) {
+              if (kd + 1 < DH / 32) read_k(kd + 1, kf[(kd + 1) & 1]);
+            } else {
+              read_k(kd, kf[0]);
+            }
+#pragma unroll
+            for (int q = 0; q < NQ; ++q)
+              if (live(q)) {
+#pragma unroll
+                for (int b = 0; b < SG; ++b)
+                  sc[q][b] = mfma_f16(kf[KPIPE ? kd & 1 : 0][b], qf[q][kd], kd ? sc[q][b] : f32x4{0.f, 0.f, 0.f, 0.f});
+              }
           }
+          // V fragments of the first block pair, requested before the softmax
+          // so that their LDS latency overlaps it
+          auto read_v = [&](int c, f16x8 (&dst)[DH / 16]) __attribute__((always_inline)) {
+            const int gr = 2 * g0 + 4 * c + lg;  // granule of block g0/2 + c for this lane group
 #pragma unroll
-          for (int q = 0; q < TPW; ++q)
-            if (q == 0 || tile_on[q]) {
+            for (int dt = 0; dt < DH / 16; ++dt) {
+              const int d = dt * 16 + (lane & 15);
+              dst[dt] = *(const f16x8*)(sV + (size_t)d * CH + vgran(gr, d) * 8);
+            }
+          };
+          f16x8 vv[DH / 16];
+          if constexpr (KPIPE) read_v(0, vv);
+          f16x8 pf[TPW][SG / 2 > 0 ? SG / 2 : 1];
+          // whole group visible to every row of the wave (wave-uniform): no mask
+          const bool full = (g0 + SG) * 16 <= min(lim_min + 1, n_pos);
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) {
+            if (!live(q)) continue;
+            // running max m in log2 units; scores scaled inside the exp2's fma
+            float bm = -INFINITY;
+            if (full) {
 #pragma unroll
               for (int b = 0; b < SG; ++b)
-                sc[q][b] = mfma_f16(kf[b], qf[q][kd], kd ? sc[q][b] : f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int j = 0; j < 4; ++j) bm = fmaxf(bm, sc[q][b][j]);
+            } else {
+#pragma unroll
+              for (int b = 0; b < SG; ++b)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                  const int pa = (g0 + b) * 16 + lg * 4 + j;
+                  bool vis = pa <= lim[q];
+                  if (tree) {  // the context, then the row's ancestors (bit j = position ctx + j)
+                    const int rel = pa + sub - ctx;
+                    vis = rel < 0 || ((anc[q] >> (rel & 63)) & 1);
+                  }
+                  sc[q][b][j] = (vis && pa < n_pos) ? sc[q][b][j] : -INFINITY;
+                  bm = fmaxf(bm, sc[q][b][j]);
+                }
             }
-        }
-        f16x8 pf[TPW][SG / 2 > 0 ? SG / 2 : 1];
-        // whole group visible to every row of the wave (wave-uniform): no mask
-        const bool full = (g0 + SG) * 16 <= min(lim_min + 1, n_pos);
+            bm = rows_max(bm);
+            // Lazy rescaling: a row's reference m moves only when a score
+            // exceeds it by more than kAttnLazy (base-2 units).  The weights
+            // 2^(s - m) then stay below 2^kAttnLazy (well inside the fp16 P
+            // operand's range), (m, l, O) stay consistent, and the
+            // accumulators are rescaled only when some row's reference moves.
+            const float cand = bm * a.scale_log2;
+            if (__builtin_amdgcn_ballot_w64(cand > m[q] + kAttnLazy)) {
+              const bool grow = cand > m[q] + kAttnLazy;
+              const float alpha = grow ? __builtin_amdgcn_exp2f(m[q] - cand) : 1.f;  // 0 from -inf
+              lsum[q] *= alpha;
 #pragma unroll
-        for (int q = 0; q < TPW; ++q) {
-          if (q > 0 && !tile_on[q]) continue;
-          // running max m in log2 units; scores scaled inside the exp2's fma
-          float bm = -INFINITY;
-          if (full) {
-#pragma unroll
-            for (int b = 0; b < SG; ++b)
-#pragma unroll
-              for (int j = 0; j < 4; ++j) bm = fmaxf(bm, sc[q][b][j]);
-          } else {
+              for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
+              if (grow) m[q] = cand;
+            }
+            const float ms = m[q] == -INFINITY ? 0.f : m[q];  // nothing visible yet: every weight is 0
+            float ps = 0.f;
 #pragma unroll
             for (int b = 0; b < SG; ++b)
 #pragma unroll
               for (int j = 0; j < 4; ++j) {
-                const int pa = (g0 + b) * 16 + lg * 4 + j;
-                bool vis = pa <= lim[q];
-                if (tree) {  // the context, then the row's ancestors (bit j = position ctx + j)
-                  const int rel = pa + sub - ctx;
-                  vis = rel < 0 || ((anc[q] >> (rel & 63)) & 1);
-                }
-                sc[q][b][j] = (vis && pa < n_pos) ? sc[q][b][j] : -INFINITY;
-                bm = fmaxf(bm, sc[q][b][j]);
+                sc[q][b][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][b][j], a.scale_log2, -ms));
+                ps += sc[q][b][j];
+              }
+            lsum[q] += ps;
+            // B operand of block pair c: positions 32c' + {4lg..4lg+3} and
+            // 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
+#pragma unroll
+            for (int c = 0; c < SG / 2; ++c)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                pf[q][c][j] = (_Float16)sc[q][2 * c][j];
+                pf[q][c][4 + j] = (_Float16)sc[q][2 * c + 1][j];
               }
           }
-          bm = fmaxf(bm, __shfl_xor(bm, 16));
-          bm = fmaxf(bm, __shfl_xor(bm, 32));
-          // Lazy rescaling: a row's reference m moves only when a score
-          // exceeds it by more than kAttnLazy (base-2 units).  The weights
-          // 2^(s - m) then stay below 2^kAttnLazy (well inside the fp16 P
-          // operand's range), (m, l, O) stay consistent, and the
-          // accumulators are rescaled only when some row's reference moves.
-          const float cand = bm * a.scale_log2;
-          if (__builtin_amdgcn_ballot_w64(cand > m[q] + kAttnLazy)) {
-            const bool grow = cand > m[q] + kAttnLazy;
-            const float alpha = grow ? __builtin_amdgcn_exp2f(m[q] - cand) : 1.f;  // 0 from -inf
-            lsum[q] *= alpha;
 #pragma unroll
-            for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] *= alpha;
-            if (grow) m[q] = cand;
-          }
-          const float ms = m[q] == -INFINITY ? 0.f : m[q];  // nothing visible yet: every weight is 0
-          float ps = 0.f;
+          for (int c = 0; c < SG / 2; ++c) {
+            if (c > 0 || !KPIPE) read_v(c, vv);
 #pragma unroll
-          for (int b = 0; b < SG; ++b)
+            for (int q = 0; q < NQ; ++q)
+              if (live(q)) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              sc[q][b][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][b][j], a.scale_log2, -ms));
-              ps += sc[q][b][j];
-            }
-          lsum[q] += ps;
-          // B operand of block pair c: positions 32c' + {4lg..4lg+3} and
-          // 32c' + 16 + {4lg..4lg+3}, c' = g0/2 + c
-#pragma unroll
-          for (int c = 0; c < SG / 2; ++c)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              pf[q][c][j] = (_Float16)sc[q][2 * c][j];
-              pf[q][c][4 + j] = (_Float16)sc[q][2 * c + 1][j];
-            }
-        }
-#pragma unroll
-        for (int c = 0; c < SG / 2; ++c) {
-          const int ua = 4 * g0 + 8 * c + lg, ub = ua + 4;
-          uint2 va[DH / 16], vb[DH / 16];
-#pragma unroll
-          for (int dt = 0; dt < DH / 16; ++dt) {
-            const int d = dt * 16 + (lane & 15);
-            const uint2* row = (const uint2*)(sV + (size_t)d * CH);
-            va[dt] = row[(ua & ~(VM - 1)) | ((ua & (VM - 1)) ^ (d & (VM - 1)))];
-            vb[dt] = row[(ub & ~(VM - 1)) | ((ub & (VM - 1)) ^ (d & (VM - 1)))];
-          }
-#pragma unroll
-          for (int q = 0; q < TPW; ++q)
-            if (q == 0 || tile_on[q]) {
-#pragma unroll
-              for (int dt = 0; dt < DH / 16; ++dt) {
-                const u32x4 vv = {va[dt].x, va[dt].y, vb[dt].x, vb[dt].y};
-                o[q][dt] = mfma_f16(__builtin_bit_cast(f16x8, vv), pf[q][c], o[q][dt]);
+                for (int dt = 0; dt < DH / 16; ++dt) o[q][dt] = mfma_f16(vv[dt], pf[q][c], o[q][dt]);
               }
-            }
+          }
         }
+      };
+      if constexpr (TPW == 1 || !KPIPE) {
+        run(std::integral_constant<int, TPW>{});
+      } else if (tile_on[TPW - 1]) {
+        run(std::integral_constant<int, TPW>{});
+      } else {
+        run(std::integral_constant<int, 1>{});
       }
     }
   }
@@ -341,9 +386,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, ConstItem* ip, unsi
 #pragma unroll
   for (int q = 0; q < TPW; ++q) {
     if (!tile_on[q]) continue;
-    float l = lsum[q];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
+    const float l = rows_sum(lsum[q]);
     const int r = tile_row[q];
     const bool rvalid = r < R;
     if (nch == 1) {

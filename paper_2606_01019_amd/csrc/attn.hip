@@ -18,8 +18,10 @@
 // to fp16, are the B operand of O^T = V^T P^T with the contraction index
 // permuted consistently on both operands (positions {4g..4g+3, 16+4g..16+4g+3}
 // for lane group g).  V is stored transposed inside each 16-token page
-// ([dh][16]) and kept transposed in LDS.  LDS rows are XOR-swizzled so the
-// 16 lanes of a fragment read hit distinct banks.
+// ([dh][16]) and kept transposed in LDS, where each row's positions are
+// regrouped so that a lane group's eight contraction positions of a 32-key
+// block sit in one 16-byte granule (one LDS read per V fragment).  LDS rows
+// are XOR-swizzled so the 16 lanes of a fragment read hit distinct banks.
 // Online softmax in fp32 base 2 (the hardware exp2, whose results below
 // 2^-126 flush to zero); rows see only their causal prefix (for a token
 // tree: the context and the positions of their own path, from a per-row

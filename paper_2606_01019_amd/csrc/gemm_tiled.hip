@@ -19,7 +19,8 @@
 // tiles with the row blocks of a column block adjacent: the weight tile is
 // fetched from HBM once into that XCD's L2 and re-read from there by the
 // other row blocks.  A K split (gridDim covers S splits) writes fp32 partial
-// tiles that gemm_tiled_finish sums in split order before the epilogue.
+// tiles; the last split of a tile to arrive sums them in split order and runs
+// the epilogue.
 //
 // The epilogue works on the accumulator registers: MFMA 32x32 output element
 // (row 8*(r/4) + 4*(lane/32) + r%4, column lane%32) of register r.  Partner
@@ -436,64 +437,57 @@ __global__ __launch_bounds__(64 * WY * WX, tiled_occupancy(WM, WN)) void gemm_ti
   const int row_w = tc.rb * BM + wy * 32 * WM;
   const int col_w = tc.cb * BN + wx * 32 * WN;
   if (S > 1) {
-    // partial tile of this split, lane-native order: float4 group g of lane l
-    // at ((tile*NW + wave)*4*WM*WN + g)*64 + l
-    const size_t tile = ((size_t)tc.split * RB + tc.rb) * CB + tc.cb;
-    float4* dst = (float4*)a.part + (tile * NW + wave) * (4 * WM * WN) * 64 + lane;
+    // K split: publish this split's partial tile with device-scope
+    // (write-through) stores, in lane-native order (float4 group g of
+    // accumulator (i, j) of lane l at ((i*WN + j)*4 + g)*64 + l of the
+    // wave's slice), then count arrivals.  The last split of the tile to
+    // arrive reads every split's partial back, its own included, and sums
+    // them in split order (the same order whichever arrives last, so results
+    // are deterministic), then runs the epilogue: no second kernel.
+    const int unit = tc.rb * CB + tc.cb;
+    auto slice = [&](int sp) {
+      return a.part + ((((size_t)sp * RB + tc.rb) * CB + tc.cb) * NW + wave) * (size_t)(16 * WM * WN * 64);
+    };
+    float* mine = slice(tc.split);
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
       for (int j = 0; j < WN; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
-          dst[((i * WN + j) * 4 + g) * 64] =
-              float4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-    return;
+          st_f4_dev(mine, (uint32_t)((((i * WN + j) * 4 + g) * 64 + lane) * 16),
+                    float4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]});
+    __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));  // this thread's stores are done
+    __syncthreads();
+    // the arrival verdict goes through the (now idle) operand ring
+    uint32_t* verdict = (uint32_t*)&sbuf[0][0][0];
+    if (tid == 0) *verdict = atomicAdd(a.cnt + unit, 1u) == (uint32_t)S - 1u;
+    __syncthreads();
+    if (!*verdict) return;
+    if (tid == 0) store_dev_u32(a.cnt + unit, 0u);  // every split has arrived: ready for the next launch
+    for (int sp = 0; sp < S; ++sp) {
+      const float* src = slice(sp);
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const float4 x = ld_f4_dev(src, (uint32_t)((((i * WN + j) * 4 + g) * 64 + lane) * 16));
+            if (sp == 0) {
+              acc[i][j][4 * g] = x.x;
+              acc[i][j][4 * g + 1] = x.y;
+              acc[i][j][4 * g + 2] = x.z;
+              acc[i][j][4 * g + 3] = x.w;
+            } else {
+              acc[i][j][4 * g] += x.x;
+              acc[i][j][4 * g + 1] += x.y;
+              acc[i][j][4 * g + 2] += x.z;
+              acc[i][j][4 * g + 3] += x.w;
+            }
+          }
+    }
   }
-  tiled_epilogue<WY, WX, WM, WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
-}
-
-// Sum of the S partial tiles (in split order), then the epilogue.  One
-// workgroup per (column block, row block), same numbering as gemm_tiled.
-template <int WY, int WX, int WM, int WN, int EPI>
-__global__ __launch_bounds__(64 * WY * WX) void gemm_tiled_finish(GemmArgs a, const float* __restrict__ inv_rms,
-                                                                  int RB, int CB, int S) {
-  constexpr int NW = WY * WX;
-  constexpr int BM = 32 * WM * WY, BN = 32 * WN * WX;
-  __shared__ float2 lm_best[EPI == EPI_LM ? WX * BM : 1];
-  __shared__ int lm_idx[EPI == EPI_LM ? WX * BM : 1];
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wy = wave / WX, wx = wave % WX;
-  const TileCoord tc = tile_coord(blockIdx.x, gridDim.x, RB, CB);
-  f32x16 acc[WM][WN];
-#pragma unroll
-  for (int i = 0; i < WM; ++i)
-#pragma unroll
-    for (int j = 0; j < WN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-  for (int sp = 0; sp < S; ++sp) {
-    const size_t tile = ((size_t)sp * RB + tc.rb) * CB + tc.cb;
-    const float4* p = (const float4*)a.part + (tile * NW + wave) * (4 * WM * WN) * 64 + lane;
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        float4 v[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) v[g] = p[((i * WN + j) * 4 + g) * 64];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          acc[i][j][4 * g] += v[g].x;
-          acc[i][j][4 * g + 1] += v[g].y;
-          acc[i][j][4 * g + 2] += v[g].z;
-          acc[i][j][4 * g + 3] += v[g].w;
-        }
-      }
-  }
-  const int row_w = tc.rb * BM + wy * 32 * WM;
-  const int col_w = tc.cb * BN + wx * 32 * WN;
   tiled_epilogue<WY, WX, WM, WN, EPI>(a, acc, row_w, col_w, inv_rms, lm_best, lm_idx, tc.cb);
 }
 
@@ -516,9 +510,6 @@ static hipError_t launch_t(const GemmArgs& a, const float* inv_rms, int splits, 
   const int total = CB * RB * splits;
   hvd_launch((gemm_tiled<WY, WX, WM, WN, EPI, HI_LO>), dim3(total), dim3(NT), 0, s, a, inv_rms, RB, CB,
                      splits);
-  if (splits > 1)
-    hvd_launch((gemm_tiled_finish<WY, WX, WM, WN, EPI>), dim3(CB * RB), dim3(NT), 0, s, a, inv_rms, RB, CB,
-                       splits);
   return hipGetLastError();
 }
 
