@@ -66,7 +66,7 @@ def counter_traffic():
     if rec is None:
         return None
     h = hashlib.sha256()
-    for name in ("gemm.hip", "common.h"):
+    for name in ("gemm.hip", "skinny.h", "common.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_2606_01019_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return rec["traffic_bytes_per_launch"] if h.hexdigest()[:16] == rec["source_sha256_16"] else None
