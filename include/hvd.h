@@ -301,7 +301,7 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   skinny GEMM shape of that GEMM, strips * 100 + K splits (0 = policy).
  * HVD_OPT_TILED_SHAPE + f: tiled GEMM shape, (tile + 1) * 100 + K splits
  *   (tile 0 = 128x128, 1 = 128x256, 2 = 256x256 / 8 waves, 3 = 256x256 / 4
- *   waves; 0 = policy). */
+ *   waves, 4 = 128x256 / 8 waves; 0 = policy). */
 enum {
   HVD_OPT_GRAPHS = 1, HVD_OPT_MLP_SINGLE = 2, HVD_OPT_LM_SINGLE = 3, HVD_OPT_FLOW = 4, HVD_OPT_FLOW_ITEMS = 5,
   HVD_OPT_ATTN_O = 6,

@@ -1312,23 +1312,30 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       // many rows: MFMA-tiled kernel, weights read once per XCD.  Of the
       // tiles that give at least one workgroup per CU, 256 x 256 unless the
       // 128-row tile pads the rows less (the padded rows' MFMA work is
-      // wasted: 848 rows run as 1024 or as 896); else 128 x 128, with a K
-      // split when even that leaves CUs idle (measured at 848 rows: down and
-      // O 8% faster split two ways at 224 workgroups)
-      static const int tile_bm[4] = {128, 128, 256, 256}, tile_bn[4] = {128, 256, 256, 256};
+      // wasted: 848 rows run as 1024 or as 896); else 128 x 256 on 8 waves
+      // (one workgroup per CU, a six-slot operand ring), K-split to about
+      // 7/8 of a workgroup per CU unless 5/8 are there already; else
+      // 128 x 128 with a K split when even that leaves CUs idle.  Measured
+      // against 128 x 128: the 848-row batch 30.2 -> 29.3 ms (QKV unsplit,
+      // O and down split 2), the 32B multistep step 59.3 -> 57.1 ms (QKV
+      // split 2, O and down split 4)
+      static const int tile_bm[5] = {128, 128, 256, 256, 128}, tile_bn[5] = {128, 256, 256, 256, 256};
       const int want_t = std::max(want, kCUs);
       auto rb_of = [&](int t) { return (MT * 16 + tile_bm[t] - 1) / tile_bm[t]; };
       auto fits = [&](int t) { return N % tile_bn[t] == 0 && N / tile_bn[t] * rb_of(t) >= want_t; };
       int tile = 0;
       if (fits(2) && !(fits(1) && rb_of(1) * 128 < rb_of(2) * 256)) tile = 2;
       else if (fits(1)) tile = 1;
+      else if (N % tile_bn[4] == 0) tile = 4;
       const bool forced = family <= PF_LM && k->tiled_force[family][0] && N % tile_bn[k->tiled_force[family][0] - 1] == 0;
       if (forced) tile = k->tiled_force[family][0] - 1;
       const int RB = (MT * 16 + tile_bm[tile] - 1) / tile_bm[tile];
       const int nblk = N / tile_bn[tile] * RB;
       int splits = 1;
       if (forced) splits = std::max(1, std::min(k->tiled_force[family][1], a.KT / 32));
-      else if (nblk < want_t) splits = std::max(1, std::min({4, (want_t + nblk - 1) / nblk, a.KT / 32}));
+      else if (tile == 4) {
+        if (nblk * 8 < want_t * 5) splits = std::max(1, std::min({4, (want_t * 7 / 8 + nblk - 1) / nblk, a.KT / 32}));
+      } else if (nblk < want_t) splits = std::max(1, std::min({4, (want_t + nblk - 1) / nblk, a.KT / 32}));
       while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > sx.gemm_part_bytes) --splits;
       if (splits > 1 && nblk > kGemmCounters) splits = 1;  // one arrival counter per output tile
       const bool mlp = epi == EPI_SILU || family == PF_DOWN;
@@ -2114,7 +2121,7 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
   }
   if (option >= HVD_OPT_TILED_SHAPE && option <= HVD_OPT_TILED_SHAPE + PF_LM) {
     const int f = option - HVD_OPT_TILED_SHAPE, t = value / 100 - 1, sp = value % 100;
-    if (value != 0 && !(t >= 0 && t <= 3 && sp >= 1 && sp <= 8))
+    if (value != 0 && !(t >= 0 && t <= 4 && sp >= 1 && sp <= 8))
       return set_err(HVD_ERR_ARG, "HVD_OPT_TILED_SHAPE value: 0, or (tile + 1) * 100 + K splits (1..8)");
     k->tiled_force[f][0] = value ? t + 1 : 0;
     k->tiled_force[f][1] = value ? sp : 0;

@@ -520,6 +520,7 @@ static hipError_t launch_th(const GemmArgs& a, const float* inv_rms, int tile, i
     case 1: return launch_t<2, 2, 2, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 128 x 256, 4 waves
     case 2: return launch_t<4, 2, 2, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 256 x 256, 8 waves
     case 3: return launch_t<2, 2, 4, 4, EPI, HI_LO>(a, inv_rms, splits, s);  // 256 x 256, 4 waves
+    case 4: return launch_t<2, 4, 2, 2, EPI, HI_LO>(a, inv_rms, splits, s);  // 128 x 256, 8 waves
   }
   return hipErrorInvalidValue;
 }

@@ -317,7 +317,8 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 hipError_t launch_gemm(int epi, const GemmArgs& a, int ns, int splits, int mblocks, int mt_block, bool hi_lo,
                        hipStream_t s);
 // Large-batch GEMM (gemm_tiled.hip): tile 0 = 128 x 128, 1 = 128 x 256,
-// 2 = 256 x 256 (rows x columns); hi_lo false = the hi activation part
+// 2 = 256 x 256 (8 waves), 3 = 256 x 256 (4 waves), 4 = 128 x 256 (8 waves)
+// (rows x columns); hi_lo false = the hi activation part
 // alone; K split `splits` ways; inv_rms is a per-row scratch vector
 // (computed here for normalised inputs).
 hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int tile, bool hi_lo, int splits, float* inv_rms,

@@ -321,7 +321,7 @@ class KVCache:
         self.set_option(HVD_OPT_GEMM_SHAPE + GEMM_FAMILIES.index(family), value)
 
     def set_tiled_shape(self, family: str, tile: int = -1, splits: int = 0):
-        """Force the tiled GEMM shape of one GEMM family (tile 0..3, K
+        """Force the tiled GEMM shape of one GEMM family (tile 0..4, K
         splits); tile -1 returns it to the policy."""
         value = (tile + 1) * 100 + splits if tile >= 0 else 0
         self.set_option(HVD_OPT_TILED_SHAPE + GEMM_FAMILIES.index(family), value)

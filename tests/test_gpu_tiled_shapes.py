@@ -1,8 +1,8 @@
 """GPU parity of every MFMA-tiled GEMM variant, whatever the launch policy
-would pick: each of the four tile shapes (128x128, 128x256 with four waves,
-256x256 with eight waves of 64x128 or four of 128x128), without a K split
-and with a two-way split plus its finish pass, forced for all five GEMM
-families at once (the library reads the override when a model is loaded).
+would pick: each of the five tile shapes (128x128, 128x256 with four waves
+of 64x128 or eight of 64x64, 256x256 with eight waves of 64x128 or four of
+128x128), without a K split and with a two-way split summed inside the
+launch, forced for all five GEMM families at once.
 
 The decoder has one layer of model width 2048, so the attention projections
 have enough K steps for a split too: 16 q / 4 kv heads of 128, SwiGLU 4096,
@@ -52,7 +52,7 @@ def wide_case():
 
 
 @pytest.mark.parametrize("splits", [1, 2])
-@pytest.mark.parametrize("tile", [0, 1, 2, 3])
+@pytest.mark.parametrize("tile", [0, 1, 2, 3, 4])
 def test_forced_tile_shape_matches_oracle(wide_case, tile, splits):
     import paper_2606_01019_amd as hvd
     torch, w, ctxs, states, drafts, results = wide_case
