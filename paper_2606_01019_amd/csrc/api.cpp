@@ -378,7 +378,8 @@ struct hvd_kv_s {
   float* gemm_part = nullptr;
   uint32_t* gemm_cnt = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
-  bool mlp_single = true;    // large-batch verify MLP GEMMs on the hi activation part only
+  bool mlp_single_gu = true;    // verify gate/up GEMMs on the hi activation part only
+  bool mlp_single_down = true;  // verify down GEMMs likewise
   bool lm_single = true;     // large-batch verify LM head on the hi activation part only
   int32_t* g = nullptr;
   int32_t* out = nullptr;
@@ -1344,7 +1345,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
         a.n_part = lm_parts;
       }
       ProfScope ps(k, family, (double)N * K * 2.0);
-      const bool single = lm_head && ((mlp && k->mlp_single) || (epi == EPI_LM && k->lm_single));
+      const bool single = lm_head && ((mlp && (epi == EPI_SILU ? k->mlp_single_gu : k->mlp_single_down)) ||
+                                      (epi == EPI_LM && k->lm_single));
       HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, sx.inv_rms, s));
       return HVD_OK;
     }
@@ -1352,7 +1354,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     // tiled path); measured at batch 1, context 2048: 3.48 -> 3.39 ms per step at
     // k = 8 (gate/up 38.3 -> 36.0 us, down 23.9 -> 22.9 us per layer)
     const bool single = lm_head &&
-                        ((k->mlp_single && (epi == EPI_SILU || family == PF_DOWN)) || (k->lm_single && epi == EPI_LM));
+                        ((epi == EPI_SILU && k->mlp_single_gu) || (family == PF_DOWN && k->mlp_single_down) ||
+                         (k->lm_single && epi == EPI_LM));
     // five single-pass row tiles: one block, so the weights are read once
     const int mblocks_g = single && MT == 5 ? 1 : mblocks, mt_block_g = single && MT == 5 ? 5 : mt_block;
     int ns = 4, splits = 1;
@@ -2104,7 +2107,16 @@ extern "C" hvd_status hvd_kv_set_option(hvd_kv k, int32_t option, int32_t value)
     }
     case HVD_OPT_MLP_SINGLE:
     case HVD_OPT_LM_SINGLE:
-      (option == HVD_OPT_MLP_SINGLE ? k->mlp_single : k->lm_single) = value != 0;
+      if (value < 0 || value > (option == HVD_OPT_MLP_SINGLE ? 3 : 1))
+        return set_err(HVD_ERR_ARG, option == HVD_OPT_MLP_SINGLE
+                                        ? "HVD_OPT_MLP_SINGLE value: 0 (pair), 1 (both single), 2 (gate/up), 3 (down)"
+                                        : "HVD_OPT_LM_SINGLE value: 0 or 1");
+      if (option == HVD_OPT_MLP_SINGLE) {
+        k->mlp_single_gu = value == 1 || value == 2;
+        k->mlp_single_down = value == 1 || value == 3;
+      } else {
+        k->lm_single = value != 0;
+      }
       for (auto& g : k->graphs) (void)hipGraphExecDestroy(g.second);  // captured with the old choice
       k->graphs.clear();
       return HVD_OK;
