@@ -278,8 +278,8 @@ def leg_hvd_loop(model, reps):
     cfg = model.cfg
     n, n_new = 2048, 256
     kv = hvd.KVCache(model, max_seqs=2, n_pages=2 * ((n + n_new + 160) // 16 + 8))
-    # fp16 hi + lo activations in every verify: the single-pass MLP and LM
-    # head of verifies over 32 rows resolve near ties differently from the
+    # fp16 hi + lo activations in every verify: with the single-pass MLP and
+    # LM head, a long verify can resolve a near tie differently from the
     # one-row steps that produced the earlier request's stream, which would
     # end the retried request's agreement with it early
     kv.set_mlp_single(False)
@@ -342,7 +342,7 @@ def leg_hvd_loop(model, reps):
             res[name]["tokens_equal_to_earlier_response"] = same(out, earlier)
     res["earlier_response"] = {"reruns": rounds, "tokens_equal_to_greedy": same(earlier, ref)}
     # the same requests on the library's default numerics (MLP and LM head of
-    # verifies over 32 rows on the single fp16 activation)
+    # every verify forward on the single fp16 activation)
     kv.set_mlp_single(True)
     kv.set_lm_single(True)
     res["default_numerics"] = {}
