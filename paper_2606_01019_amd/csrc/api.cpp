@@ -379,7 +379,7 @@ struct hvd_kv_s {
   uint32_t* gemm_cnt = nullptr;
   float* inv_rms = nullptr;  // per-row inverse RMS for the large-batch GEMMs
   bool mlp_single_gu = true;     // verify gate/up GEMMs on the hi activation part only
-  bool mlp_single_down = false;  // verify down GEMMs on the hi + lo pair (its rounding weighs twice gate/up's)
+  bool mlp_single_down = false;  // verify down GEMMs on the hi + lo pair (the cheaper of the two to keep)
   bool lm_single = true;     // large-batch verify LM head on the hi activation part only
   int32_t* g = nullptr;
   int32_t* out = nullptr;
@@ -1356,8 +1356,10 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
     const bool single = lm_head &&
                         ((epi == EPI_SILU && k->mlp_single_gu) || (family == PF_DOWN && k->mlp_single_down) ||
                          (k->lm_single && epi == EPI_LM));
-    // five single-pass row tiles: one block, so the weights are read once
-    const int mblocks_g = single && MT == 5 ? 1 : mblocks, mt_block_g = single && MT == 5 ? 5 : mt_block;
+    // five row tiles (65-80 rows): one block, so the weights are read once --
+    // single-pass GEMMs, and the residual GEMMs (O, down) on the hi + lo pair
+    const bool five = MT == 5 && (single || epi == EPI_RESID);
+    const int mblocks_g = five ? 1 : mblocks, mt_block_g = five ? 5 : mt_block;
     int ns = 4, splits = 1;
     skinny_shape(epi, N, K, family, single, mblocks_g, mt_block_g, ns, splits);
     if (epi == EPI_LM) {

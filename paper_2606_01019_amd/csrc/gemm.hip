@@ -74,11 +74,18 @@ static hipError_t launch_ns(const GemmArgs& a, int splits, int mblocks, int mt, 
       }
       launch_one<2, NS, EPI, true>(a, splits, mblocks, s);
       break;
-    case 5:  // one block of five single-pass row tiles (65-80 rows): the weights are read once
-             // (8 strips for gate/up and the LM head only: the residual epilogue's LDS would not fit)
+    case 5:  // one block of five row tiles (65-80 rows): the weights are read once.  Single
+             // pass (8 strips for gate/up and the LM head only: the residual epilogue's LDS
+             // would not fit), or the hi + lo pair for the residual GEMMs at up to 4 strips
       if constexpr (kSingle && (NS <= 4 || EPI == EPI_SILU || EPI == EPI_LM)) {
         if (!hi_lo) {
           launch_one<5, NS, EPI, false>(a, splits, mblocks, s);
+          break;
+        }
+      }
+      if constexpr (EPI == EPI_RESID && NS <= 4) {
+        if (hi_lo) {
+          launch_one<5, NS, EPI, true>(a, splits, mblocks, s);
           break;
         }
       }
