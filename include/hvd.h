@@ -265,13 +265,14 @@ hvd_status hvd_profile_read(hvd_kv kv, int32_t family, double* ms, int64_t* laun
  *   measured slightly faster for single-sequence verifies.  Results are
  *   identical either way.  Profiling (hvd_profile_enable) always launches
  *   eagerly.
- * HVD_OPT_MLP_SINGLE (default 2): in verify forwards the gate/up GEMM (2),
- *   the down GEMM (3) or both (1) take the fp16 activation alone (11 bits)
- *   instead of the fp16 hi + lo pair (~22 bits), halving their activation
- *   traffic and MFMA work; 0 keeps the pair for both.  Prefill always uses
- *   the pair.  Either GEMM's single pass moves logits (gate/up's input
- *   rounding about twice as much as down's); the default keeps the pair
- *   where it is cheaper, in the down GEMM.
+ * HVD_OPT_MLP_SINGLE (default 2 up to 32 layers, 0 above): in verify
+ *   forwards the gate/up GEMM (2), the down GEMM (3) or both (1) take the
+ *   fp16 activation alone (11 bits) instead of the fp16 hi + lo pair (~22
+ *   bits), halving their activation traffic and MFMA work; 0 keeps the pair
+ *   for both.  Prefill always uses the pair.  Either GEMM's single pass
+ *   moves logits (gate/up's input rounding about twice as much as down's),
+ *   and the error grows with depth: the default keeps the pair where it is
+ *   cheaper, in the down GEMM, and for models deeper than 32 layers in both.
  * HVD_OPT_LM_SINGLE (default 1): likewise for the LM-head GEMM of verify
  *   forwards (its rounding error, ~1e-4 on the logits, is far below the
  *   tolerance); 0 keeps the pair.

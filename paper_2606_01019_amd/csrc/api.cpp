@@ -47,6 +47,7 @@ int prefill_rows(const hvd_config& c) {
 // tiles beats the tiled kernel (measured: 65-row verifies and 128-row
 // prefill chunks of the 8B shape)
 constexpr int kSkinnyMaxMT = 8;
+constexpr int kMlpSingleMaxLayers = 32;      // deepest model whose verify gate/up GEMM runs single-pass by default
 constexpr int kGemmMinBlocks = 192;          // GEMM workgroups below which the shape changes
 constexpr int kGemmSplitTarget = 256;        // workgroups a K split aims for (one per CU)
 constexpr int kGemmLongK = 256;              // K steps above which a K split pays for its reduction
@@ -527,6 +528,11 @@ extern "C" hvd_status hvd_kv_alloc(hvd_model m, int32_t max_seqs, int32_t n_page
   k->m = m;
   k->stream = (hipStream_t)stream;
   k->n_pages = n_pages;
+  // The logit error of the fp16 path grows as the square root of depth;
+  // deeper models keep gate/up on the hi + lo pair too (64 layers of the
+  // 32B shape: whole-row error 2.7-2.9e-2 with gate/up single, 2.4e-2 with
+  // the pair, against a 2.83e-2 bar)
+  k->mlp_single_gu = c.n_layers <= kMlpSingleMaxLayers;
   const size_t need = carve_kv(k, c, max_seqs, n_pages, nullptr);
   if (dev_buf) {
     if (dev_bytes < need) {
@@ -740,15 +746,18 @@ bool plan_attention(const hvd_config& c, const HostState& hs, const std::vector<
   }
   // chunk: a power-of-two number of positions, the largest that still gives
   // every CU work -- two 64-row items per CU (4 waves: several share a CU),
-  // one item of 128 or 256 rows (8 waves) -- with at least 64 positions for
-  // 64-row items and at most 1024 (128-row) or 512 (256-row).  Longer
-  // chunks loop over LDS-sized sub-chunks.  Measured: 32 sequences of mixed
-  // drafts 34.2 -> 33.2 ms per step; context 16384 at k = 16 / 64 from
-  // 4.98 / 9.04 to 4.71 / 8.70 ms (chunks of at most 256 before); more
-  // workgroups per CU (384 or 512 targets) measured slower
+  // one item of 128 rows or more (8 waves) -- with at least 64 positions for
+  // 64-row items and at most 1024 for the others.  Longer chunks loop over
+  // LDS-sized sub-chunks.  Measured: 32 sequences of mixed drafts 34.2 ->
+  // 33.2 ms per step; context 16384 at k = 16 / 64 from 4.98 / 9.04 to
+  // 4.71 / 8.70 ms (chunks of at most 256 before); 1024 instead of 512 for
+  // 256- and 384-row items (fewer partials to write and merge): the 848-row
+  // batch 32.4 -> 31.9 ms, the 32B multistep step 62.5 -> 61.3 ms (2048 or
+  // 4096: 61.9 ms); more workgroups per CU (384 or 512 targets) measured
+  // slower
   const int per_cu = rpi <= kAttnRows / 2 ? 2 : 1;
   const int64_t want = (total_keys + (int64_t)min_items * per_cu - 1) / ((int64_t)min_items * per_cu);
-  const int cap = rpi <= kAttnRows / 2 ? (1 << 20) : rpi <= kAttnRows ? 1024 : 512;
+  const int cap = rpi <= kAttnRows / 2 ? (1 << 20) : 1024;
   int chunk = rpi <= kAttnRows / 2 ? 64 : 32;
   while (chunk < cap && 2 * chunk <= want) chunk *= 2;
   if (max_items > 0) {
