@@ -1333,9 +1333,15 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       const int want_t = std::max(want, kCUs);
       auto rb_of = [&](int t) { return (MT * 16 + tile_bm[t] - 1) / tile_bm[t]; };
       auto fits = [&](int t) { return N % tile_bn[t] == 0 && N / tile_bn[t] * rb_of(t) >= want_t; };
+      const bool mlp = epi == EPI_SILU || family == PF_DOWN;
+      const bool single = lm_head && ((mlp && (epi == EPI_SILU ? k->mlp_single_gu : k->mlp_single_down)) ||
+                                      (epi == EPI_LM && k->lm_single));
       int tile = 0;
       if (fits(2) && !(fits(1) && rb_of(1) * 128 < rb_of(2) * 256)) tile = 2;
-      else if (fits(1)) tile = 1;
+      // the hi + lo pair's 32 KB K steps leave the 4-wave 128 x 256 tile one
+      // workgroup per CU and a three-slot ring: the 8-wave tile's four slots
+      // serve it better (32B multistep, gate/up on the pair: 69.1 -> 67.3 ms)
+      else if (fits(1)) tile = single ? 1 : 4;
       else if (N % tile_bn[4] == 0) tile = 4;
       const bool forced = family <= PF_LM && k->tiled_force[family][0] && N % tile_bn[k->tiled_force[family][0] - 1] == 0;
       if (forced) tile = k->tiled_force[family][0] - 1;
@@ -1348,14 +1354,11 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       } else if (nblk < want_t) splits = std::max(1, std::min({4, (want_t + nblk - 1) / nblk, a.KT / 32}));
       while (splits > 1 && (size_t)splits * RB * tile_bm[tile] * N * 4 > sx.gemm_part_bytes) --splits;
       if (splits > 1 && nblk > kGemmCounters) splits = 1;  // one arrival counter per output tile
-      const bool mlp = epi == EPI_SILU || family == PF_DOWN;
       if (epi == EPI_LM) {
         lm_parts = N / tile_bn[tile];
         a.n_part = lm_parts;
       }
       ProfScope ps(k, family, (double)N * K * 2.0);
-      const bool single = lm_head && ((mlp && (epi == EPI_SILU ? k->mlp_single_gu : k->mlp_single_down)) ||
-                                      (epi == EPI_LM && k->lm_single));
       HIP_TRY(launch_gemm_tiled(epi, a, tile, !single, splits, sx.inv_rms, s));
       return HVD_OK;
     }
