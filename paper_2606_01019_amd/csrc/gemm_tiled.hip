@@ -459,11 +459,11 @@ __global__ __launch_bounds__(64 * WY * WX, tiled_occupancy(WM, WN)) void gemm_ti
                     float4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]});
     __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));  // this thread's stores are done
     __syncthreads();
-    // the arrival verdict goes through the (now idle) operand ring
-    uint32_t* verdict = (uint32_t*)&sbuf[0][0][0];
-    if (tid == 0) *verdict = atomicAdd(a.cnt + unit, 1u) == (uint32_t)S - 1u;
+    // whether this split arrived last goes through the (now idle) operand ring
+    uint32_t* last_flag = (uint32_t*)&sbuf[0][0][0];
+    if (tid == 0) *last_flag = atomicAdd(a.cnt + unit, 1u) == (uint32_t)S - 1u;
     __syncthreads();
-    if (!*verdict) return;
+    if (!*last_flag) return;
     if (tid == 0) store_dev_u32(a.cnt + unit, 0u);  // every split has arrived: ready for the next launch
     for (int sp = 0; sp < S; ++sp) {
       const float* src = slice(sp);
