@@ -480,12 +480,22 @@ __device__ __forceinline__ void skinny_tile(const GemmArgs& a, const SkinnyCoord
 #pragma unroll
     for (int n = 0; n < NS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)kt * a.wk + lane);
   };
+  // A lane holds one row's 8 halves (row = lane % 16 of its tile).  Lanes of
+  // rows at or past a.M read their lane group's last live row instead of the
+  // operand's padding: the same cache lines as the live lanes, so a tile
+  // with few live rows costs few line reads (those rows' outputs are dropped)
+  int alane[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int live = min(16, max(1, a.M - (mt0 + m) * 16));
+    alane[m] = m * 64 + min(lane & 15, live - 1) + (lane & 48);
+  }
   auto load_a = [&](int u, int j) __attribute__((always_inline)) {
     const int kt = kb + j * kKG;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      qh[u][m] = hp[kt * astride + m * 64 + lane];
-      if constexpr (HL) ql[u][m] = lp[kt * astride + m * 64 + lane];
+      qh[u][m] = hp[kt * astride + alane[m]];
+      if constexpr (HL) ql[u][m] = lp[kt * astride + alane[m]];
     }
   };
   auto load = [&](int u, int j) __attribute__((always_inline)) {
