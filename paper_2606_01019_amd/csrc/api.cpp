@@ -1043,7 +1043,8 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
   // Strips per workgroup and K splits of the weight-streaming GEMM (measured
   // on the 8B verify shapes): 4 strips per workgroup when that alone gives
   // enough workgroups (8 for two row tiles, which halves the activation
-  // fragments per weight byte); for long-K GEMMs 4 strips plus a K split;
+  // fragments per weight byte); for long-K GEMMs 4 strips plus a K split
+  // (2 strips and a two-way split at up to 8 rows);
   // otherwise 2 strips, or for one row tile 1 strip when that fills the GPU;
   // K-split if still too few.
   auto skinny_shape = [&](int epi, int N, int K, int family, bool single, int mblocks, int mt_block, int& ns,
@@ -1060,6 +1061,13 @@ hvd_status forward(hvd_kv_s* k, const std::vector<SeqMeta>& seqs, std::vector<Ro
       ns = 8;
     } else if (nb4 >= want) {
       ns = 4;
+    } else if (KT >= kGemmLongK && mt_block == 1 && mblocks == 1 && M <= 8 && nb2 * 2 >= want) {
+      // up to 8 live rows: each activation fragment reads one line per 16-lane
+      // group, so two strips with a two-way split beat four strips with a
+      // four-way split (down, 8B shape: 23.1 -> 22.2 us per layer at 2-8
+      // rows; at 9-16 rows 24.5 against 23.7, so those keep four strips)
+      ns = 2;
+      splits = 2;
     } else if (KT >= kGemmLongK) {
       ns = 4;
       splits = std::max(1, std::min((kGemmSplitTarget + nb4 - 1) / nb4, KT / 64));
