@@ -472,30 +472,48 @@ __device__ __forceinline__ void skinny_tile(const GemmArgs& a, const SkinnyCoord
   const u32x4* lp = (const u32x4*)a.Alo + (size_t)mt0 * 64;
 
   // Stage u of the prefetch queue holds the fragments of one K step.  Row
-  // tiles past this block's last are read from the operand's padding and
-  // computed, then dropped (no per-tile branches in the loop).
+  // tiles past this block's last are computed, then dropped (no per-tile
+  // branches in the loop); their lanes count as rows past a.M below.
   u32x4 qb[U][NS], qh[U][MT], ql[U][HL ? MT : 1];
   auto load_w = [&](int u, int j) __attribute__((always_inline)) {
     const int kt = kb + j * kKG;
 #pragma unroll
     for (int n = 0; n < NS; ++n) qb[u][n] = __builtin_nontemporal_load(wp[n] + (size_t)kt * a.wk + lane);
   };
-  // A lane holds one row's 8 halves (row = lane % 16 of its tile).  Lanes of
-  // rows at or past a.M read their lane group's last live row instead of the
-  // operand's padding: the same cache lines as the live lanes, so a tile
-  // with few live rows costs few line reads (those rows' outputs are dropped)
+  // A lane holds one row's 8 halves (row = lane % 16 of its tile); the
+  // outputs of rows at or past a.M are dropped, so those lanes need no data.
+  // Blocks of one or two row tiles: those lanes skip the load and keep what
+  // their register held (zero at first), which also saves the data return.
+  // Larger blocks (where the branches measured slower): those lanes read
+  // their 16-lane group's last live row, the cache lines the live lanes
+  // fetch anyway.  Either way a tile with at most 8 live rows reads one of
+  // its group's two 128-byte lines.
+  constexpr bool MASKED = MT <= 2;
+  bool lok[MT];
   int alane[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     const int live = min(16, max(1, a.M - (mt0 + m) * 16));
-    alane[m] = m * 64 + min(lane & 15, live - 1) + (lane & 48);
+    lok[m] = (mt0 + m) * 16 + (lane & 15) < a.M;
+    alane[m] = m * 64 + (MASKED ? lane : min(lane & 15, live - 1) + (lane & 48));
+  }
+  if constexpr (MASKED) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        qh[u][m] = u32x4{0u, 0u, 0u, 0u};
+        if constexpr (HL) ql[u][m] = u32x4{0u, 0u, 0u, 0u};
+      }
   }
   auto load_a = [&](int u, int j) __attribute__((always_inline)) {
     const int kt = kb + j * kKG;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      qh[u][m] = hp[kt * astride + alane[m]];
-      if constexpr (HL) ql[u][m] = lp[kt * astride + alane[m]];
+      if (!MASKED || lok[m]) {
+        qh[u][m] = hp[kt * astride + alane[m]];
+        if constexpr (HL) ql[u][m] = lp[kt * astride + alane[m]];
+      }
     }
   };
   auto load = [&](int u, int j) __attribute__((always_inline)) {
